@@ -1,0 +1,240 @@
+"""ctypes front end of the CPU oracle (test infrastructure only).
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The product path (the HIP library and its binding) never
+does.  Every function converts numpy inputs, calls the plain-C oracle in
+`mixrt_oracle.c` and returns numpy outputs.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lib = None
+
+_DT = {np.dtype(np.float32): 0, np.dtype(np.float16): 1}
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            from . import build as _b
+            _b.build()
+        _lib = C.CDLL(_LIB_PATH)
+        _declare(_lib)
+    return _lib
+
+
+def _declare(L):
+    P = C.c_void_p
+    L.orc_half_to_double.restype = C.c_double
+    L.orc_half_to_double.argtypes = [C.c_uint16]
+    L.orc_level_resolutions.restype = C.c_int
+    L.orc_level_resolutions.argtypes = [C.c_int, C.c_int, C.c_int, P]
+    L.orc_sh_real.restype = C.c_double
+    L.orc_sh_real.argtypes = [C.c_int, C.c_int, C.c_double, C.c_double, C.c_double]
+    L.orc_sh_basis.restype = None
+    L.orc_sh_basis.argtypes = [C.c_int, P, P]
+    L.orc_camera_ray.restype = None
+    L.orc_camera_ray.argtypes = [P, C.c_int, C.c_int, C.c_int, C.c_int, P, P]
+    L.orc_tex_bilinear.restype = None
+    L.orc_tex_bilinear.argtypes = [P, C.c_int, C.c_int, C.c_int, C.c_double, C.c_double, P]
+    L.orc_calibrate.restype = None
+    L.orc_calibrate.argtypes = [P, P, P, C.c_int, P]
+    L.orc_contract.restype = None
+    L.orc_contract.argtypes = [P, P]
+    L.orc_hash_level.restype = None
+    L.orc_hash_level.argtypes = [P, C.c_int32, C.c_int, C.c_int, C.c_int, P, P, P, P, P]
+    L.orc_hash_encode.restype = C.c_int
+    L.orc_hash_encode.argtypes = [C.c_int64, P, C.c_int, C.c_int, C.c_int, C.c_int,
+                                  C.c_int, C.c_int, P, P, P, P, P]
+    L.orc_mlp.restype = C.c_int
+    L.orc_mlp.argtypes = [C.c_int64, P, C.c_int, P, P, P]
+    L.orc_composite.restype = None
+    L.orc_composite.argtypes = [C.c_int64, C.c_int, P, C.c_double, P, P]
+    L.orc_render_pixels.restype = C.c_int
+    L.orc_render_pixels.argtypes = [P, C.c_int64, P, P, C.c_int]
+    L.orc_pixel_samples.restype = C.c_int
+    L.orc_pixel_samples.argtypes = [P, C.c_int64, P, P, P, P]
+    L.orc_max_threads.restype = C.c_int
+    L.orc_max_threads.argtypes = []
+
+
+def _p(a: np.ndarray):
+    return C.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def _c(a, dtype):
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+class _OrcScene(C.Structure):
+    _fields_ = [
+        ("views", C.c_int), ("H", C.c_int), ("W", C.c_int),
+        ("g0", C.c_void_p), ("cams", C.c_void_p),
+        ("tex_R", C.c_int), ("tex_V", C.c_int), ("tex_dtype", C.c_int), ("tex", C.c_void_p),
+        ("L", C.c_int), ("log2T", C.c_int), ("F", C.c_int), ("n_min", C.c_int),
+        ("n_max", C.c_int), ("table_dtype", C.c_int), ("table", C.c_void_p),
+        ("n_layers", C.c_int), ("widths", C.c_void_p), ("view_sh_dim", C.c_int),
+        ("weights", C.c_void_p), ("K", C.c_int), ("delta", C.c_double),
+    ]
+
+
+# --- elementary steps ---------------------------------------------------------
+
+def half_to_double(bits) -> np.ndarray:
+    bits = np.asarray(bits, dtype=np.uint16).reshape(-1)
+    f = lib().orc_half_to_double
+    return np.array([f(int(b)) for b in bits], dtype=np.float64)
+
+
+def level_resolutions(L: int, n_min: int, n_max: int) -> np.ndarray:
+    out = np.zeros(L, np.int32)
+    if lib().orc_level_resolutions(L, n_min, n_max, _p(out)):
+        raise ValueError("bad level schedule")
+    return out
+
+
+def sh_real(l: int, m: int, d) -> float:
+    return lib().orc_sh_real(l, m, float(d[0]), float(d[1]), float(d[2]))
+
+
+def sh_basis(n: int, d) -> np.ndarray:
+    d = _c(d, np.float64).reshape(-1, 3)
+    out = np.zeros((d.shape[0], n), np.float64)
+    for r in range(d.shape[0]):
+        row = np.zeros(n, np.float64)
+        lib().orc_sh_basis(n, _p(np.ascontiguousarray(d[r])), _p(row))
+        out[r] = row
+    return out
+
+
+def camera_ray(cam, W: int, H: int, i: int, j: int):
+    cam = _c(cam, np.float32)
+    o = np.zeros(3)
+    d = np.zeros(3)
+    lib().orc_camera_ray(_p(cam), W, H, i, j, _p(o), _p(d))
+    return o, d
+
+
+def tex_bilinear(tex: np.ndarray, u: float, v: float) -> np.ndarray:
+    tex = np.ascontiguousarray(tex)
+    R, R2, V = tex.shape
+    assert R == R2
+    out = np.zeros(V)
+    lib().orc_tex_bilinear(_p(tex), _DT[tex.dtype], R, V, float(u), float(v), _p(out))
+    return out
+
+
+def calibrate(p, d, m) -> np.ndarray:
+    p, d, m = _c(p, np.float64), _c(d, np.float64), _c(m, np.float64)
+    out = np.zeros(3)
+    lib().orc_calibrate(_p(p), _p(d), _p(m), m.size, _p(out))
+    return out
+
+
+def contract(q) -> np.ndarray:
+    q = _c(q, np.float64)
+    out = np.zeros(3)
+    lib().orc_contract(_p(q), _p(out))
+    return out
+
+
+def hash_encode(x: np.ndarray, table: np.ndarray, n_min: int, n_max: int):
+    """x [n,3] fp32 in [0,1]; table [L,T,F] f32/f16.  Returns corner [n,L,3],
+    idx [n,L,8], w [n,L,8] and feat [n,L*F]."""
+    x = _c(x, np.float32).reshape(-1, 3)
+    table = np.ascontiguousarray(table)
+    L, T, F = table.shape
+    n = x.shape[0]
+    corner = np.zeros((n, L, 3), np.int32)
+    idx = np.zeros((n, L, 8), np.uint32)
+    w = np.zeros((n, L, 8), np.float64)
+    feat = np.zeros((n, L * F), np.float64)
+    rc = lib().orc_hash_encode(n, _p(x), L, n_min, n_max, int(T).bit_length() - 1, F,
+                               _DT[table.dtype], _p(table), _p(corner), _p(idx), _p(w),
+                               _p(feat))
+    if rc:
+        raise ValueError("hash_encode: bad arguments")
+    return corner, idx, w, feat
+
+
+def mlp(inp: np.ndarray, weights) -> np.ndarray:
+    """inp [n, w0] (double); weights: list of [in,out] fp16 arrays."""
+    inp = _c(inp, np.float64)
+    widths = np.array([weights[0].shape[0]] + [w.shape[1] for w in weights], np.int32)
+    flat = np.concatenate([np.asarray(w, np.float16).reshape(-1) for w in weights])
+    bits = flat.view(np.uint16).copy()
+    n = inp.shape[0]
+    out = np.zeros((n, 4))
+    if lib().orc_mlp(n, _p(inp), len(weights), _p(widths), _p(bits), _p(out)):
+        raise ValueError("mlp: bad arguments")
+    return out
+
+
+def composite(srgb: np.ndarray, delta: float, bg) -> np.ndarray:
+    """srgb [rays,K,4]; bg [rays,3] or [3]."""
+    srgb = _c(srgb, np.float64)
+    rays, K, _ = srgb.shape
+    bg = np.broadcast_to(np.asarray(bg, np.float64), (rays, 3)).copy()
+    out = np.zeros((rays, 4))
+    lib().orc_composite(rays, K, _p(srgb), float(delta), _p(bg), _p(out))
+    return out
+
+
+# --- the whole path -------------------------------------------------------------
+
+class OracleScene:
+    """Binds a synth.Scene to the oracle's scene descriptor."""
+
+    def __init__(self, scene):
+        cfg = scene.cfg
+        self.scene = scene
+        self.K = cfg.K
+        self._keep = []
+        g0 = np.ascontiguousarray(scene.g0, np.float32)
+        cams = np.ascontiguousarray(scene.cams, np.float32)
+        widths = np.array(cfg.widths, np.int32)
+        wbits = scene.weights_flat.view(np.uint16).copy()
+        self._keep += [g0, cams, widths, wbits, scene.tex, scene.table]
+        s = _OrcScene()
+        s.views, s.H, s.W = cfg.views, cfg.rows_kept, cfg.W
+        s.g0, s.cams = g0.ctypes.data, cams.ctypes.data
+        s.tex_R, s.tex_V = cfg.tex_R, cfg.tex_V
+        s.tex_dtype = _DT[scene.tex.dtype]
+        s.tex = scene.tex.ctypes.data
+        s.L, s.log2T, s.F = cfg.L, cfg.log2_T, cfg.F
+        s.n_min, s.n_max = cfg.N_min, cfg.N_max
+        s.table_dtype = _DT[scene.table.dtype]
+        s.table = scene.table.ctypes.data
+        s.n_layers = len(cfg.widths) - 1
+        s.widths = widths.ctypes.data
+        s.view_sh_dim = cfg.view_sh_dim
+        s.weights = wbits.ctypes.data
+        s.K, s.delta = cfg.K, float(cfg.delta)
+        self.desc = s
+
+    def render_pixels(self, pix, threads: int = 1) -> np.ndarray:
+        pix = _c(pix, np.int64).reshape(-1)
+        out = np.zeros((pix.size, 4))
+        rc = lib().orc_render_pixels(C.byref(self.desc), pix.size, _p(pix), _p(out), threads)
+        if rc:
+            raise ValueError("render_pixels: bad scene")
+        return out
+
+    def pixel_samples(self, pix):
+        pix = _c(pix, np.int64).reshape(-1)
+        x = np.zeros((pix.size, self.K, 3), np.float32)
+        xd = np.zeros((pix.size, self.K, 3), np.float64)
+        hit = np.zeros(pix.size, np.int32)
+        lib().orc_pixel_samples(C.byref(self.desc), pix.size, _p(pix), _p(x), _p(xd), _p(hit))
+        return x, xd, hit
+
+
+def max_threads() -> int:
+    return lib().orc_max_threads()

@@ -1,0 +1,316 @@
+"""Seeded synthetic inputs shaped like the MixRT workloads.
+
+This module only *draws* inputs: G-buffers, cameras, displacement textures,
+hash tables and MLP weights.  It holds none of the rendering arithmetic (no
+pixel-to-ray mapping, displacement, contraction, hashing, MLP or compositing),
+so both the HIP path and the CPU oracle can consume its arrays without sharing
+any of the method's code.
+
+The paper measures on trained indoor Unbounded-360 scenes rendered at
+1280x720 (Sec. 5.1.1); neither the dataset nor trained assets are available, so
+these generators stand in for them with the same shapes: an indoor room seen
+from inside (depths 0.5-20), a texture atlas addressed by per-surface UV
+charts, hash tables and MLPs with the sizes listed per configuration.
+
+Screen-space room: every visible surface of the procedural room is planar, and
+a planar surface seen through any pinhole camera has an inverse depth that is
+affine in the pixel coordinates.  The generator therefore writes inverse depth
+directly as an affine function of normalised screen coordinates and keeps the
+nearest surface per pixel.  This gives the spatial coherence of a rasterised
+G-buffer (adjacent pixels hit adjacent points) without evaluating any camera
+ray.
+"""
+from __future__ import annotations
+
+import dataclasses
+import hashlib
+from dataclasses import dataclass, field
+
+import numpy as np
+
+# Data-type codes shared with the C ABI descriptor fields (values, not code).
+DT_F32 = 0
+DT_F16 = 1
+DT_U8 = 2
+
+_DT_CODE = {"f32": DT_F32, "f16": DT_F16, "u8": DT_U8}
+_NP_DT = {"f32": np.float32, "f16": np.float16, "u8": np.uint8}
+
+
+@dataclass(frozen=True)
+class SceneConfig:
+    """One workload: image size, sampling, texture, hash grid and MLP shapes."""
+
+    name: str
+    views: int
+    H: int
+    W: int
+    K: int
+    delta: float
+    gbuf: str                 # "iid" (cache-hostile) or "room" (coherent)
+    tex_R: int
+    tex_V: int
+    tex_dtype: str            # "f32" | "f16"
+    tex_range: float          # texture values ~ U[-tex_range, tex_range]
+    L: int
+    log2_T: int
+    F: int
+    N_min: int
+    N_max: int
+    table_dtype: str          # "f32" | "f16"
+    table_range: float        # table values ~ U[-table_range, table_range]
+    widths: tuple             # (in, hidden..., 4)
+    view_sh_dim: int          # 0 or 16
+    w_std: float              # weights ~ N(0, w_std), stored fp16
+    seed: int
+    fov_y_deg: float = 60.0
+    t_term: float = 1e-4
+    head_scale: float = 1.0   # multiplies the output-layer weights
+    bg: tuple = (0.0, 0.0, 0.0)
+    rows: int = 0             # >0: keep only the first `rows` image rows
+
+    @property
+    def T(self) -> int:
+        return 1 << self.log2_T
+
+    @property
+    def rays(self) -> int:
+        return self.views * self.rows_kept * self.W
+
+    @property
+    def rows_kept(self) -> int:
+        return self.rows if self.rows else self.H
+
+    @property
+    def samples(self) -> int:
+        return self.rays * self.K
+
+    def replace(self, **kw) -> "SceneConfig":
+        return dataclasses.replace(self, **kw)
+
+
+# --- the workloads -----------------------------------------------------------
+
+TINY64 = SceneConfig(
+    name="tiny64", views=1, H=64, W=64, K=4, delta=0.01, gbuf="iid",
+    tex_R=64, tex_V=4, tex_dtype="f32", tex_range=0.05,
+    L=8, log2_T=14, F=2, N_min=16, N_max=256, table_dtype="f32",
+    table_range=1e-2, widths=(16, 32, 4), view_sh_dim=0, w_std=0.1, seed=1)
+
+# Same shapes, but densities and features large enough that every sample
+# matters: alpha in roughly [0.1, 0.99] per sample, colours spread over (0,1).
+TINY64_DENSE = TINY64.replace(name="tiny64_dense", delta=0.5, table_range=1.0,
+                              head_scale=8.0, bg=(0.2, 0.4, 0.6), seed=11)
+
+VIEW720P = SceneConfig(
+    name="view720p", views=1, H=720, W=1280, K=8, delta=0.01, gbuf="room",
+    tex_R=1024, tex_V=8, tex_dtype="f16", tex_range=0.05,
+    L=16, log2_T=19, F=2, N_min=16, N_max=4096, table_dtype="f16",
+    table_range=1e-2, widths=(48, 64, 64, 4), view_sh_dim=16, w_std=0.05,
+    seed=2)
+
+VIEW720P_DENSE = VIEW720P.replace(name="view720p_dense", delta=0.25,
+                                  table_range=1.0, w_std=0.2, head_scale=2.0,
+                                  bg=(0.2, 0.4, 0.6), seed=12)
+
+BATCH8X1080P = VIEW720P.replace(name="batch8x1080p", views=8, H=1080, W=1920,
+                                log2_T=21, N_max=8192, seed=3)
+
+
+def sweep_config(rays: int, K: int, dense: bool = False) -> SceneConfig:
+    """First `rays` rays of a coherent 4096x4096 view, on the 720p grid/MLP."""
+    assert rays % 4096 == 0
+    base = VIEW720P_DENSE if dense else VIEW720P
+    return base.replace(name=f"sweep_r{rays}_k{K}" + ("_dense" if dense else ""),
+                        H=4096, W=4096, rows=rays // 4096, K=K, seed=4)
+
+
+# The deployed grid of the paper's implementation details: four levels,
+# resolution 256 to 4096, 2^21 entries of four features, one query per pixel.
+DEPLOYED720P = VIEW720P.replace(name="deployed720p", K=1, L=4, log2_T=21, F=4,
+                                N_min=256, N_max=4096, widths=(32, 64, 64, 4),
+                                seed=5)
+
+CONFIGS = {c.name: c for c in (TINY64, TINY64_DENSE, VIEW720P, VIEW720P_DENSE,
+                               BATCH8X1080P, DEPLOYED720P)}
+
+
+# --- scene container ----------------------------------------------------------
+
+@dataclass
+class Scene:
+    cfg: SceneConfig
+    g0: np.ndarray            # [views, rows, W, 4] f32: (t, u, v, 0)
+    g1: np.ndarray            # [views, rows, W, 4] f32: (nx, ny, nz, 0)
+    cams: np.ndarray          # [views, 16] f32: c2w row-major 3x4, fov_y_deg, bg rgb
+    tex: np.ndarray           # [R, R, V] f32/f16
+    table: np.ndarray         # [L, T, F] f32/f16
+    weights: list             # per layer [in, out] f16
+    extra: dict = field(default_factory=dict)
+
+    @property
+    def weights_flat(self) -> np.ndarray:
+        return np.concatenate([w.reshape(-1) for w in self.weights]).astype(np.float16)
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for a in (self.g0, self.g1, self.cams, self.tex, self.table, self.weights_flat):
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()
+
+
+def _rot_y(deg: float) -> np.ndarray:
+    a = np.deg2rad(deg)
+    c, s = np.cos(a), np.sin(a)
+    return np.array([[c, 0, s], [0, 1, 0], [-s, 0, c]])
+
+
+def _rot_x(deg: float) -> np.ndarray:
+    a = np.deg2rad(deg)
+    c, s = np.cos(a), np.sin(a)
+    return np.array([[1, 0, 0], [0, c, -s], [0, s, c]])
+
+
+def _camera_rows(cfg: SceneConfig, rng: np.random.Generator) -> np.ndarray:
+    cams = np.zeros((cfg.views, 16), np.float32)
+    for v in range(cfg.views):
+        if cfg.gbuf == "iid":
+            R = np.eye(3)
+            o = np.zeros(3)
+        elif cfg.views == 1:
+            R = _rot_y(15.0) @ _rot_x(-5.0)
+            o = np.array([0.3, 0.2, -0.1])
+        else:  # a 360-degree capture pattern: poses on a circle, facing out
+            yaw = 360.0 * v / cfg.views
+            R = _rot_y(yaw) @ _rot_x(-5.0)
+            o = 0.5 * np.array([np.sin(np.deg2rad(yaw)), 0.0, np.cos(np.deg2rad(yaw))])
+            o[1] = 0.2
+        c2w = np.concatenate([R, o[:, None]], axis=1)
+        cams[v, :12] = c2w.reshape(-1)
+        cams[v, 12] = cfg.fov_y_deg
+        cams[v, 13:16] = cfg.bg
+    return cams
+
+
+def _iid_gbuffer(cfg: SceneConfig, rng: np.random.Generator):
+    n = cfg.views * cfg.rows_kept * cfg.W
+    g0 = np.zeros((n, 4), np.float32)
+    g0[:, 0] = rng.uniform(1.0, 4.0, n)
+    g0[:, 1:3] = rng.uniform(0.0, 1.0, (n, 2))
+    g1 = np.zeros((n, 4), np.float32)
+    g1[:, 2] = 1.0  # facing a camera that looks down -z
+    shape = (cfg.views, cfg.rows_kept, cfg.W, 4)
+    return g0.reshape(shape), g1.reshape(shape)
+
+
+def _room_view(rng: np.random.Generator, H: int, W: int, rows: int):
+    """One screen-space indoor view: walls, floor, ceiling, boxes, blobs."""
+    jj, ii = np.mgrid[0:rows, 0:W].astype(np.float64)
+    xs = (ii + 0.5 - W / 2) / (H / 2)          # horizontal, aspect-scaled
+    ys = (jj + 0.5 - H / 2) / (H / 2)          # vertical, +1 at the bottom
+    # Room surfaces: inverse depth affine in (xs, ys); the nearest wins.
+    back = 1.0 / rng.uniform(8.0, 18.0)
+    kf, kc = rng.uniform(0.5, 0.9), rng.uniform(0.3, 0.6)
+    kl, kr = rng.uniform(0.25, 0.5), rng.uniform(0.25, 0.5)
+    yh = rng.uniform(-0.15, 0.15)
+    xh = rng.uniform(-0.2, 0.2)
+    surf_inv = np.stack([
+        np.full_like(xs, back),                # back wall
+        kf * (ys - yh),                        # floor
+        -kc * (ys - yh),                       # ceiling
+        -kl * (xs - xh),                       # left wall
+        kr * (xs - xh),                        # right wall
+    ])
+    normals = np.array([[0, 0, 1], [0, 1, 0], [0, -1, 0], [1, 0, 0], [-1, 0, 0]],
+                       np.float64)
+    sid = np.argmax(surf_inv, axis=0)
+    inv = np.take_along_axis(surf_inv, sid[None], 0)[0]
+    nrm = normals[sid]
+    # Per-surface UV charts: affine in screen space, wrapped into [0, 1).
+    coef = rng.uniform(-0.6, 0.6, (5, 2, 3))
+    u = np.zeros_like(xs)
+    v = np.zeros_like(xs)
+    for s in range(5):
+        m = sid == s
+        u[m] = coef[s, 0, 0] * xs[m] + coef[s, 0, 1] * ys[m] + coef[s, 0, 2]
+        v[m] = coef[s, 1, 0] * xs[m] + coef[s, 1, 1] * ys[m] + coef[s, 1, 2]
+    aspect = W / H
+    # Boxes: planar screen rectangles nearer than the room.
+    for _ in range(int(rng.integers(6, 12))):
+        cx, cy = rng.uniform(-aspect, aspect), rng.uniform(-0.6, 0.9)
+        hw, hh = rng.uniform(0.05, 0.4), rng.uniform(0.05, 0.4)
+        a0 = 1.0 / rng.uniform(0.6, 6.0)
+        ax, ay = rng.uniform(-0.1, 0.1, 2) * a0
+        binv = a0 + ax * (xs - cx) + ay * (ys - cy)
+        m = (np.abs(xs - cx) < hw) & (np.abs(ys - cy) < hh) & (binv > inv)
+        inv[m] = binv[m]
+        c = rng.uniform(-1.0, 1.0, (2, 3))
+        u[m] = c[0, 0] * xs[m] + c[0, 1] * ys[m] + c[0, 2]
+        v[m] = c[1, 0] * xs[m] + c[1, 1] * ys[m] + c[1, 2]
+        n = rng.normal(size=3)
+        n[2] = abs(n[2]) + 1.0
+        nrm[m] = n / np.linalg.norm(n)
+    # Perturbed blobs: screen disks with a bulging inverse depth.
+    for _ in range(int(rng.integers(2, 5))):
+        cx, cy = rng.uniform(-aspect, aspect), rng.uniform(-0.5, 0.8)
+        rad = rng.uniform(0.08, 0.35)
+        t0 = rng.uniform(0.8, 5.0)
+        rho2 = ((xs - cx) ** 2 + (ys - cy) ** 2) / rad ** 2
+        wob = 1.0 + 0.05 * np.sin(7.0 * np.arctan2(ys - cy, xs - cx))
+        inside = rho2 < wob ** 2
+        bulge = np.sqrt(np.clip(1.0 - rho2 / wob ** 2, 0.0, 1.0))
+        binv = 1.0 / (t0 - 0.4 * t0 * rad * bulge)
+        m = inside & (binv > inv)
+        inv[m] = binv[m]
+        u[m] = 0.5 + 0.5 * (xs[m] - cx) / rad
+        v[m] = 0.5 + 0.5 * (ys[m] - cy) / rad
+        nz = np.maximum(bulge[m], 1e-3)
+        nn = np.stack([(xs[m] - cx) / rad, -(ys[m] - cy) / rad, nz], -1)
+        nrm[m] = nn / np.linalg.norm(nn, axis=-1, keepdims=True)
+    with np.errstate(divide="ignore"):
+        t = np.clip(1.0 / np.maximum(inv, 1e-9), 0.5, 20.0)
+    u = u - np.floor(u)
+    v = v - np.floor(v)
+    g0 = np.stack([t, u, v, np.zeros_like(t)], -1).astype(np.float32)
+    g1 = np.concatenate([nrm, np.zeros_like(t)[..., None]], -1).astype(np.float32)
+    return g0, g1
+
+
+def _room_gbuffer(cfg: SceneConfig, rng: np.random.Generator):
+    g0s, g1s = [], []
+    for _ in range(cfg.views):
+        a, b = _room_view(rng, cfg.H, cfg.W, cfg.rows_kept)
+        g0s.append(a)
+        g1s.append(b)
+    return np.stack(g0s), np.stack(g1s)
+
+
+def make_scene(cfg: SceneConfig) -> Scene:
+    """Draw every input of `cfg` in a fixed order: G-buffer, camera, texture,
+    table, weights."""
+    rng = np.random.default_rng(cfg.seed)
+    if cfg.gbuf == "iid":
+        g0, g1 = _iid_gbuffer(cfg, rng)
+    else:
+        g0, g1 = _room_gbuffer(cfg, rng)
+    cams = _camera_rows(cfg, rng)
+    tex = rng.uniform(-cfg.tex_range, cfg.tex_range,
+                      (cfg.tex_R, cfg.tex_R, cfg.tex_V)).astype(_NP_DT[cfg.tex_dtype])
+    table = rng.uniform(-cfg.table_range, cfg.table_range,
+                        (cfg.L, cfg.T, cfg.F)).astype(np.float32)
+    table = table.astype(_NP_DT[cfg.table_dtype])
+    assert cfg.widths[0] == cfg.L * cfg.F + cfg.view_sh_dim
+    assert cfg.widths[-1] == 4
+    weights = []
+    for m in range(len(cfg.widths) - 1):
+        w = rng.normal(0.0, cfg.w_std, (cfg.widths[m], cfg.widths[m + 1]))
+        if m == len(cfg.widths) - 2:
+            w = w * cfg.head_scale
+        weights.append(w.astype(np.float16))
+    return Scene(cfg=cfg, g0=np.ascontiguousarray(g0), g1=np.ascontiguousarray(g1),
+                 cams=cams, tex=np.ascontiguousarray(tex),
+                 table=np.ascontiguousarray(table), weights=weights)
+
+
+def dtype_code(name: str) -> int:
+    return _DT_CODE[name]
