@@ -1,0 +1,163 @@
+"""Benchmark of the MixRT per-pixel rendering path on one MI355X.
+
+One step = one mixrt_render call over one frame of the 1280x720 workload
+(every stage of the path: ray setup, Eq. 2 calibration, K samples,
+contraction, hash encoding, MLP, compositing), inputs already resident in
+HBM.  Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+MFMA_F16_PEAK_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
+
+
+def algorithmic_work(cfg):
+    """Bytes the method must move and MLP flops it must do, per frame.
+
+    Per sample: the 8 corner entries of every level (L * 8 * F * element size).
+    Per ray: the G-buffer record read (16 B: t, u, v, pad), the 4 bilinear
+    texels (4 * V * element size) and the RGBA written (16 B).
+    MLP: 2 * sum of in*out over layers per sample."""
+    eb = 2 if cfg.table_dtype == "f16" else 4
+    xb = 2 if cfg.tex_dtype == "f16" else 4
+    per_sample_hash = cfg.L * 8 * cfg.F * eb
+    per_ray = 16 + 4 * cfg.tex_V * xb + 16
+    flops_per_sample = 2 * sum(a * b for a, b in zip(cfg.widths[:-1], cfg.widths[1:]))
+    return {
+        "hash_bytes": cfg.samples * per_sample_hash,
+        "ray_bytes": cfg.rays * per_ray,
+        "mlp_flops": cfg.samples * flops_per_sample,
+        "per_sample_hash_bytes": per_sample_hash,
+        "per_ray_bytes": per_ray,
+        "flops_per_sample": flops_per_sample,
+    }
+
+
+def cpu_baseline(scene, budget_s: float):
+    """The oracle, as it is, on a bounded random sample of the frame's pixels."""
+    import oracle
+    threads = oracle.max_threads()
+    orc = oracle.OracleScene(scene)
+    rng = np.random.default_rng(0)
+    probe = rng.choice(scene.cfg.rays, 2000, replace=False)
+    t0 = time.perf_counter()
+    orc.render_pixels(probe, threads=threads)
+    dt = time.perf_counter() - t0
+    n = int(min(scene.cfg.rays, max(2000, 2000 * budget_s / max(dt, 1e-6))))
+    pix = rng.choice(scene.cfg.rays, n, replace=False)
+    t0 = time.perf_counter()
+    orc.render_pixels(pix, threads=threads)
+    dt = time.perf_counter() - t0
+    return {"value": n / dt / 1e6, "unit": "Mpix/s", "cores": threads, "kind": "oracle",
+            "sample": f"{n} random pixels of one {scene.cfg.W}x{scene.cfg.H} frame "
+                      f"({dt:.1f} s wall, OpenMP over pixels)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="view720p")
+    ap.add_argument("--cpu-budget", type=float, default=10.0,
+                    help="seconds of oracle work for the CPU baseline (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
+              "(the path shards by view with no per-frame collective; see the design notes)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2312_11841_amd import mixrt, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg = synth.CONFIGS[args.workload]
+    print(f"bench: generating {cfg.name} ({cfg.rays} rays, K={cfg.K})", file=sys.stderr,
+          flush=True)
+    scene = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(scene, "cuda:0")
+    out = torch.empty((cfg.rays, 4), dtype=torch.float32, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    r = mixrt.Renderer(0, stream=stream)
+
+    for _ in range(args.warmup):
+        r.render(ds, out)
+    torch.cuda.synchronize()
+    print(f"bench: warmup done, timing {args.steps} frames", file=sys.stderr, flush=True)
+
+    # The render kernel is the only kernel of a step; HIP events on the
+    # renderer's stream bracket exactly the timed launches.
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    start.record(stream)
+    for _ in range(args.steps):
+        r.render(ds, out)
+    end.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms = start.elapsed_time(end) / args.steps
+    r.close()
+
+    work = algorithmic_work(cfg)
+    sec = ms * 1e-3
+    total_bytes = work["hash_bytes"] + work["ray_bytes"]
+    achieved = total_bytes / sec / 1e9
+    mpix = cfg.rays / sec / 1e6
+    line = {
+        "metric": "Mpix/s and ms/frame at 1280x720 (1 GPU); hash-encode GB/s, MLP MFMA util",
+        "value": round(mpix, 2),
+        "unit": "Mpix/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "ms_per_frame": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32 (fp16 storage, fp16 MFMA with fp32 accumulation)",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{cfg.name}: {cfg.views}x{cfg.W}x{cfg.H} px, K={cfg.K}, "
+                        f"hash L={cfg.L} T=2^{cfg.log2_T} F={cfg.F} {cfg.table_dtype} "
+                        f"N {cfg.N_min}-{cfg.N_max}, texture {cfg.tex_R}^2x{cfg.tex_V} "
+                        f"{cfg.tex_dtype}, MLP {'-'.join(map(str, cfg.widths))} fp16",
+            "rays": cfg.rays,
+            "samples": cfg.samples,
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "kernel": "render_kernel (fused path, the only kernel of a step)",
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": None,
+            "algorithmic_bytes_per_launch": total_bytes,
+        },
+        "hash_encode_GBps": round(work["hash_bytes"] / sec / 1e9, 1),
+        "mlp_mfma_util": round(work["mlp_flops"] / sec / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+        "mlp_tflops": round(work["mlp_flops"] / sec / 1e12, 2),
+        "wall_s_timed": round(t_wall, 3),
+    }
+    if args.cpu_budget > 0:
+        line["cpu_baseline"] = cpu_baseline(scene, args.cpu_budget)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,232 @@
+/*
+ * mixrt.h -- C ABI of the MI355X (gfx950) MixRT per-pixel rendering library.
+ *
+ * The library renders pixels the way "MixRT: Mixed Neural Representations
+ * For Real-Time NeRF Rendering" (arXiv 2312.11841) describes its fragment
+ * stage (Sec. 5.1.2 and Fig. 2): for every pixel, take the coarse-mesh hit
+ * from a G-buffer (Fig. 2 step 1), calibrate it with the view-dependent
+ * displacement map (Sec. 4.3.2, Eq. 2), place K samples along the ray around
+ * the calibrated point, contract them (Sec. 2.1), query each in the
+ * multiresolution hash grid (Sec. 3.1, 4.3.3), decode density and colour with
+ * the small MLP (Sec. 3.1), and alpha-composite the samples (Sec. 3.1, Eq. 1).
+ *
+ * Conventions for every entry point:
+ *  - Return value: MIXRT_OK (0) or a negative mixrt_status.  No exception
+ *    crosses the ABI and the library never aborts the process.  On failure a
+ *    message is available from mixrt_last_error() (per context) and from
+ *    mixrt_thread_error() (per thread, also for calls without a context).
+ *  - Device pointers are caller-owned device memory: the library reads or
+ *    writes them only inside the work it enqueues and never frees or retains
+ *    them.  Pointers to descriptors and cameras are host memory, read during
+ *    the call only.
+ *  - Work is enqueued asynchronously on the context's HIP stream; inputs
+ *    must stay valid and unmodified until that work completes (e.g. until
+ *    mixrt_sync()).  The same inputs give bitwise identical outputs.
+ *  - Arrays are dense, row-major, in the layouts stated per field.
+ */
+#ifndef MIXRT_H
+#define MIXRT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+enum mixrt_status {
+    MIXRT_OK = 0,
+    MIXRT_EINVAL = -1,        /* null pointer, bad size or inconsistent shape */
+    MIXRT_ENOMEM = -2,        /* device allocation failed */
+    MIXRT_EDEVICE = -3,       /* HIP runtime error (launch or device failure) */
+    MIXRT_EUNSUPPORTED = -4   /* valid request outside what this build serves */
+};
+
+/* Element types of stored arrays. */
+enum mixrt_dtype { MIXRT_F32 = 0, MIXRT_F16 = 1, MIXRT_U8 = 2 };
+
+/* Displacement forms (Eq. 2). */
+enum mixrt_disp_mode {
+    /* The V channels at p_t are coefficients of the first V real spherical
+     * harmonics of the view direction d (bands by degree, m = -l..l); their
+     * weighted sum s is a signed length and p_cali = p + s d. */
+    MIXRT_DISP_ALONG_RAY = 0
+};
+
+/* Context creation flags. */
+enum mixrt_flags {
+    MIXRT_FLAG_SYNC_CHECK = 1u   /* synchronise after each call and report
+                                    device errors as MIXRT_EDEVICE */
+};
+
+#define MIXRT_MAX_VIEWS 16
+#define MIXRT_MAX_LEVELS 32
+#define MIXRT_MAX_TEX_CHANNELS 16
+#define MIXRT_MAX_SAMPLES 64
+#define MIXRT_MAX_LAYERS 8
+
+typedef struct mixrt_ctx mixrt_ctx;
+
+typedef struct {
+    int32_t device;      /* HIP device ordinal; must be a gfx950 device */
+    void *hip_stream;    /* hipStream_t the context enqueues on (NULL: the
+                            device's null stream); caller-owned */
+    uint32_t flags;      /* mixrt_flags */
+} mixrt_create_info;
+
+/* The coarse-mesh hit per pixel (Fig. 2 step 1): rasterisation output. */
+typedef struct {
+    int32_t views, W, H; /* views * H * W pixels, view-major, row 0 at top */
+    const float *g0;     /* device [views][H][W][4]: (t, u, v, unused); t is
+                            the hit distance along the unit ray direction, a
+                            pixel with !(t > 0 && isfinite(t)) is a miss;
+                            (u, v) is the texture coordinate p_t.  16-byte
+                            aligned. */
+    const float *g1;     /* device [views][H][W][4] normal, or NULL; not read
+                            (Eq. 2 uses the view direction, not the normal) */
+} mixrt_gbuffer;
+
+/* One view's pinhole camera (Sec. 3.1: rays r = o + t d through pixels).
+ * OpenGL axes: the camera looks down -z with +y up; fov is vertical; pixel
+ * (i, j) is sampled through its centre (i + 0.5, j + 0.5). */
+typedef struct {
+    float c2w[12];       /* camera-to-world, row-major 3x4 [R | o] */
+    float fov_y_deg;     /* in (0, 180) */
+    float bg[3];         /* background colour blended with the transmittance
+                            left after the last sample */
+} mixrt_camera;
+
+/* View-dependent displacement map (Sec. 4.3.2, Eq. 2). */
+typedef struct {
+    int32_t R;           /* texture is R x R texels, addressed with texel
+                            centres at (i + 0.5) / R, clamp to edge, row from v */
+    int32_t V;           /* channels per texel, 1..16 */
+    int32_t dtype;       /* MIXRT_F32 or MIXRT_F16 */
+    int32_t mode;        /* mixrt_disp_mode */
+    const void *data;    /* device [R][R][V]; 16-byte aligned */
+} mixrt_disp_tex;
+
+/* Multiresolution hash grid (Sec. 3.1, 4.3.3, 5.1.2).  Level l has
+ * resolution N_l = floor(N_min * b^l + 1e-6) with b = (N_max/N_min)^(1/(L-1))
+ * and vertices 0..N_l per axis over the unit cube.  A level with
+ * (N_l + 1)^3 <= T indexes its vertices densely (x fastest); other levels use
+ * the spatial hash (v0 * 1 ^ v1 * 2654435761 ^ v2 * 805459861) mod T. */
+typedef struct {
+    int32_t L;           /* levels, 1..32 */
+    int32_t log2_T;      /* T = 2^log2_T entries per level, 4..28 */
+    int32_t F;           /* features per entry: 2 or 4 */
+    int32_t N_min, N_max;/* 1 <= N_min <= N_max <= 2^20 */
+    int32_t dtype;       /* MIXRT_F32 or MIXRT_F16 */
+    const void *data;    /* device [L][T][F]; 16-byte aligned */
+} mixrt_hash_grid;
+
+/* The small MLP (Sec. 3.1): input [h ; e] where h is the level-major
+ * concatenation of the L*F interpolated features and e the 16 real spherical
+ * harmonics of the view direction when view_sh_dim = 16.  Hidden layers use
+ * ReLU and no biases; the 4 outputs are (sigma_raw, r, g, b) with
+ * sigma = exp(sigma_raw), rgb = sigmoid. */
+typedef struct {
+    int32_t n_layers;    /* weight matrices, 2..MIXRT_MAX_LAYERS */
+    int32_t width[MIXRT_MAX_LAYERS + 1]; /* width[0] = L*F + view_sh_dim,
+                            hidden widths equal (16, 32 or 64), last = 4 */
+    int32_t view_sh_dim; /* 0 or 16 */
+    const uint16_t *data;/* device fp16 weights, layer m row-major
+                            [width[m]][width[m+1]], layers concatenated;
+                            16-byte aligned */
+} mixrt_mlp;
+
+/* Sampling around the calibrated point and compositing (Eq. 1). */
+typedef struct {
+    int32_t K;           /* samples per ray, 1..64, at offsets
+                            (k - (K-1)/2) * delta along d */
+    float delta;         /* sample spacing and the delta of Eq. 1, >= 0 */
+    float t_term;        /* stop compositing a ray once its transmittance
+                            drops below t_term (0: never), in [0, 1) */
+} mixrt_sampling;
+
+/* ---- lifecycle ---------------------------------------------------------- */
+
+/* Create a context bound to ci->device and ci->hip_stream.  Fails with
+ * MIXRT_EUNSUPPORTED unless the device is gfx950. *out is NULL on failure. */
+int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci);
+
+/* Release the context (not the caller's buffers or stream).  NULL is a
+ * no-op.  Pending work on the stream is not waited for. */
+int mixrt_destroy(mixrt_ctx *ctx);
+
+/* Wait for all work enqueued by the context; MIXRT_EDEVICE on a device
+ * error. */
+int mixrt_sync(mixrt_ctx *ctx);
+
+/* ---- validation (pure host: makes no HIP call, usable without a GPU) ------ */
+
+/* Check every descriptor of a render call; writes a NUL-terminated message
+ * of at most cap bytes to msg (may be NULL) on failure.  cams points to
+ * gbuf->views cameras.  Returns the status mixrt_render would return for
+ * these descriptors before launching anything. */
+int mixrt_validate(const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                   const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
+                   const mixrt_mlp *mlp, const mixrt_sampling *smp,
+                   char *msg, size_t cap);
+
+/* The level resolutions N_l of a grid (pure host).  out_N: host int32[L]. */
+int mixrt_level_resolutions(const mixrt_hash_grid *grid, int32_t *out_N);
+
+/* ---- the hot path ----------------------------------------------------------- */
+
+/* Render views * H * W pixels into out_rgba (device float [views][H][W][4]:
+ * composited rgb plus alpha = 1 - final transmittance).  A miss pixel gets
+ * (bg, 0).  Enqueued on the context's stream; no device memory is allocated. */
+int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                 const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
+                 const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
+
+/* ---- stage entry points (the same device code as mixrt_render) ------------ */
+
+/* Steps before the grid: ray, hit, Eq. 2 calibration, K samples, contraction
+ * and normalisation to [0,1]^3.  out_x: device float [views*H*W][K][3] (the
+ * exact fp32 positions mixrt_render feeds to the grid; zeros for a miss).
+ * out_hit: device int32 [views*H*W] (1 hit, 0 miss) or NULL. */
+int mixrt_debug_ray_setup(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                          const mixrt_disp_tex *disp, const mixrt_sampling *smp,
+                          float *out_x, int32_t *out_hit);
+
+/* Hash-grid queries of n positions x (device float [n][3] in [0,1]^3).
+ * Outputs (device, each may be NULL): out_corner int32 [n][L][3] lower voxel
+ * corner; out_idx uint32 [n][L][8] table index of corner beta with offset
+ * (beta&1, beta>>1&1, beta>>2&1); out_w float [n][L][8] trilinear weights;
+ * out_feat float [n][L*F] level-major features. */
+int mixrt_debug_hash_encode(mixrt_ctx *ctx, const mixrt_hash_grid *grid, const float *x,
+                            int64_t n, int32_t *out_corner, uint32_t *out_idx,
+                            float *out_w, float *out_feat);
+
+/* The MLP on n fp16 inputs (device [n][width[0]]); out4: device float
+ * [n][4] = (sigma, r, g, b) after exp / sigmoid. */
+int mixrt_debug_mlp(mixrt_ctx *ctx, const mixrt_mlp *mlp, const uint16_t *in_f16, int64_t n,
+                    float *out4);
+
+/* Compositing of rays * K samples (device float [rays][K][4] =
+ * (sigma, r, g, b)) over the background bg (host float[3]) into out_rgba
+ * (device float [rays][4]), with smp->delta and smp->t_term. */
+int mixrt_debug_composite(mixrt_ctx *ctx, const float *srgb, int64_t rays,
+                          const mixrt_sampling *smp, const float *bg, float *out_rgba);
+
+/* ---- errors ------------------------------------------------------------------- */
+
+/* Static description of a status code. */
+const char *mixrt_status_string(int status);
+
+/* Message of the context's last failed call ("" if none); owned by the
+ * context, valid until its next call or destruction. */
+const char *mixrt_last_error(const mixrt_ctx *ctx);
+
+/* Message of the calling thread's last failed call ("" if none); owned by
+ * the library, valid until that thread's next call. */
+const char *mixrt_thread_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MIXRT_H */

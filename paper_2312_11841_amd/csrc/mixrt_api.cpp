@@ -1,0 +1,466 @@
+// C ABI of the MixRT per-pixel rendering library (declared in include/mixrt.h).
+//
+// Host side: descriptor validation (pure host code, no HIP call), the level
+// resolution table, camera constants, and the launches of the kernels in
+// mixrt_kernels.hip on the context's stream.
+#include "mixrt.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+
+#include "mixrt_launch.hpp"
+
+struct mixrt_ctx {
+    int device = 0;
+    hipStream_t stream = nullptr;
+    uint32_t flags = 0;
+    int cus = 0;
+    std::string err;
+};
+
+namespace {
+
+thread_local std::string t_err;
+
+int fail(mixrt_ctx *ctx, int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    t_err = buf;
+    if (ctx) ctx->err = buf;
+    return code;
+}
+
+void clear_err(mixrt_ctx *ctx)
+{
+    t_err.clear();
+    if (ctx) ctx->err.clear();
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Level resolutions: geometric progression from N_min to N_max, floor with a
+// 1e-6 guard so that the end points are exact.
+void level_table(int L, int n_min, int n_max, int32_t *out)
+{
+    if (L == 1) {
+        out[0] = n_min;
+        return;
+    }
+    const double growth = std::exp((std::log((double)n_max) - std::log((double)n_min)) / (L - 1));
+    for (int l = 0; l < L; ++l)
+        out[l] = (int32_t)std::floor((double)n_min * std::pow(growth, (double)l) + 1e-6);
+}
+
+struct Msg {
+    char *buf;
+    size_t cap;
+};
+
+int vfail(Msg m, int code, const char *fmt, ...)
+{
+    char tmp[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(tmp, sizeof tmp, fmt, ap);
+    va_end(ap);
+    if (m.buf && m.cap) {
+        strncpy(m.buf, tmp, m.cap - 1);
+        m.buf[m.cap - 1] = 0;
+    }
+    return code;
+}
+
+int check_gbuf(const mixrt_gbuffer *g, const mixrt_camera *cams, Msg m)
+{
+    if (!g) return vfail(m, MIXRT_EINVAL, "gbuf is NULL");
+    if (g->views < 1 || g->views > MIXRT_MAX_VIEWS)
+        return vfail(m, MIXRT_EINVAL, "gbuf.views=%d outside 1..%d", g->views, MIXRT_MAX_VIEWS);
+    if (g->W < 1 || g->H < 1) return vfail(m, MIXRT_EINVAL, "gbuf W=%d H=%d", g->W, g->H);
+    if ((int64_t)g->views * g->H * g->W >= ((int64_t)1 << 31))
+        return vfail(m, MIXRT_EUNSUPPORTED, "more than 2^31-1 pixels per call");
+    if (!g->g0) return vfail(m, MIXRT_EINVAL, "gbuf.g0 is NULL");
+    if (!aligned16(g->g0)) return vfail(m, MIXRT_EINVAL, "gbuf.g0 not 16-byte aligned");
+    if (!cams) return vfail(m, MIXRT_EINVAL, "cams is NULL");
+    for (int v = 0; v < g->views; ++v) {
+        const mixrt_camera &c = cams[v];
+        if (!(c.fov_y_deg > 0.0f && c.fov_y_deg < 180.0f))
+            return vfail(m, MIXRT_EINVAL, "cams[%d].fov_y_deg=%g outside (0,180)", v, c.fov_y_deg);
+        for (int i = 0; i < 12; ++i)
+            if (!std::isfinite(c.c2w[i]))
+                return vfail(m, MIXRT_EINVAL, "cams[%d].c2w has a non-finite entry", v);
+    }
+    return MIXRT_OK;
+}
+
+int check_disp(const mixrt_disp_tex *d, Msg m)
+{
+    if (!d) return vfail(m, MIXRT_EINVAL, "disp is NULL");
+    if (d->R < 1 || d->R > (1 << 15)) return vfail(m, MIXRT_EINVAL, "disp.R=%d", d->R);
+    if (d->V < 1 || d->V > MIXRT_MAX_TEX_CHANNELS)
+        return vfail(m, MIXRT_EUNSUPPORTED, "disp.V=%d outside 1..%d", d->V, MIXRT_MAX_TEX_CHANNELS);
+    if (d->dtype != MIXRT_F32 && d->dtype != MIXRT_F16)
+        return vfail(m, MIXRT_EUNSUPPORTED, "disp.dtype=%d (F32 or F16)", d->dtype);
+    if (d->mode != MIXRT_DISP_ALONG_RAY)
+        return vfail(m, MIXRT_EUNSUPPORTED, "disp.mode=%d", d->mode);
+    if (!d->data) return vfail(m, MIXRT_EINVAL, "disp.data is NULL");
+    if (!aligned16(d->data)) return vfail(m, MIXRT_EINVAL, "disp.data not 16-byte aligned");
+    return MIXRT_OK;
+}
+
+int check_grid(const mixrt_hash_grid *g, Msg m)
+{
+    if (!g) return vfail(m, MIXRT_EINVAL, "grid is NULL");
+    if (g->L < 1 || g->L > MIXRT_MAX_LEVELS)
+        return vfail(m, MIXRT_EUNSUPPORTED, "grid.L=%d outside 1..%d", g->L, MIXRT_MAX_LEVELS);
+    if (g->log2_T < 4 || g->log2_T > 28)
+        return vfail(m, MIXRT_EUNSUPPORTED, "grid.log2_T=%d outside 4..28", g->log2_T);
+    if (g->F != 2 && g->F != 4) return vfail(m, MIXRT_EUNSUPPORTED, "grid.F=%d (2 or 4)", g->F);
+    if (g->N_min < 1 || g->N_max < g->N_min || g->N_max > (1 << 20))
+        return vfail(m, MIXRT_EINVAL, "grid N_min=%d N_max=%d", g->N_min, g->N_max);
+    if (g->dtype != MIXRT_F32 && g->dtype != MIXRT_F16)
+        return vfail(m, MIXRT_EUNSUPPORTED, "grid.dtype=%d (F32 or F16)", g->dtype);
+    if (!g->data) return vfail(m, MIXRT_EINVAL, "grid.data is NULL");
+    if (!aligned16(g->data)) return vfail(m, MIXRT_EINVAL, "grid.data not 16-byte aligned");
+    return MIXRT_OK;
+}
+
+// hidden width and hidden-layer count of a valid MLP
+int check_mlp(const mixrt_mlp *p, int expect_in, Msg m, int *hid, int *nhid)
+{
+    if (!p) return vfail(m, MIXRT_EINVAL, "mlp is NULL");
+    if (p->n_layers < 2 || p->n_layers > MIXRT_MAX_LAYERS)
+        return vfail(m, MIXRT_EUNSUPPORTED, "mlp.n_layers=%d outside 2..%d", p->n_layers,
+                     MIXRT_MAX_LAYERS);
+    if (p->view_sh_dim != 0 && p->view_sh_dim != 16)
+        return vfail(m, MIXRT_EUNSUPPORTED, "mlp.view_sh_dim=%d (0 or 16)", p->view_sh_dim);
+    if (expect_in >= 0 && p->width[0] != expect_in)
+        return vfail(m, MIXRT_EINVAL, "mlp.width[0]=%d but L*F+view_sh_dim=%d", p->width[0],
+                     expect_in);
+    if (p->width[p->n_layers] != 4)
+        return vfail(m, MIXRT_EINVAL, "mlp output width %d (must be 4)", p->width[p->n_layers]);
+    const int h = p->width[1];
+    for (int i = 1; i < p->n_layers; ++i)
+        if (p->width[i] != h)
+            return vfail(m, MIXRT_EUNSUPPORTED, "mlp hidden widths differ (%d vs %d)", p->width[i], h);
+    if (p->width[0] % 16 || (h != 16 && h != 32 && h != 64))
+        return vfail(m, MIXRT_EUNSUPPORTED, "mlp widths in=%d hidden=%d (in %%16, hidden 16/32/64)",
+                     p->width[0], h);
+    if (!mixrt::mlp_variant_supported(p->width[0], h, p->n_layers - 1))
+        return vfail(m, MIXRT_EUNSUPPORTED, "mlp %d->%dx%d->4 not built", p->width[0], h,
+                     p->n_layers - 1);
+    if (!p->data) return vfail(m, MIXRT_EINVAL, "mlp.data is NULL");
+    if (!aligned16(p->data)) return vfail(m, MIXRT_EINVAL, "mlp.data not 16-byte aligned");
+    *hid = h;
+    *nhid = p->n_layers - 1;
+    return MIXRT_OK;
+}
+
+int check_sampling(const mixrt_sampling *s, Msg m)
+{
+    if (!s) return vfail(m, MIXRT_EINVAL, "sampling is NULL");
+    if (s->K < 1 || s->K > MIXRT_MAX_SAMPLES)
+        return vfail(m, MIXRT_EUNSUPPORTED, "sampling.K=%d outside 1..%d", s->K, MIXRT_MAX_SAMPLES);
+    if (!(s->delta >= 0.0f) || !std::isfinite(s->delta))
+        return vfail(m, MIXRT_EINVAL, "sampling.delta=%g", s->delta);
+    if (!(s->t_term >= 0.0f && s->t_term < 1.0f))
+        return vfail(m, MIXRT_EINVAL, "sampling.t_term=%g outside [0,1)", s->t_term);
+    return MIXRT_OK;
+}
+
+int validate_all(const mixrt_gbuffer *gbuf, const mixrt_camera *cams, const mixrt_disp_tex *disp,
+                 const mixrt_hash_grid *grid, const mixrt_mlp *mlp, const mixrt_sampling *smp,
+                 Msg m, int *hid, int *nhid)
+{
+    int rc;
+    if ((rc = check_gbuf(gbuf, cams, m))) return rc;
+    if ((rc = check_disp(disp, m))) return rc;
+    if ((rc = check_grid(grid, m))) return rc;
+    if ((rc = check_sampling(smp, m))) return rc;
+    if (!mlp) return vfail(m, MIXRT_EINVAL, "mlp is NULL");
+    if ((rc = check_mlp(mlp, grid->L * grid->F + mlp->view_sh_dim, m, hid, nhid))) return rc;
+    if (!mixrt::render_variant_supported(disp->dtype == MIXRT_F16, grid->F,
+                                         grid->dtype == MIXRT_F16, mlp->width[0], *hid, *nhid))
+        return vfail(m, MIXRT_EUNSUPPORTED,
+                     "no render kernel for tex %s, grid F=%d %s, mlp %d->%dx%d->4",
+                     disp->dtype == MIXRT_F16 ? "f16" : "f32", grid->F,
+                     grid->dtype == MIXRT_F16 ? "f16" : "f32", mlp->width[0], *hid, *nhid);
+    return MIXRT_OK;
+}
+
+void fill_ray_params(mixrt::RayParams &rp, const mixrt_gbuffer *g, const mixrt_camera *cams,
+                     const mixrt_disp_tex *d, const mixrt_sampling *s)
+{
+    memset(&rp, 0, sizeof rp);
+    rp.g0 = (const float4 *)g->g0;
+    rp.views = g->views;
+    rp.W = g->W;
+    rp.H = g->H;
+    rp.rays = g->views * g->H * g->W;
+    rp.tex = d ? d->data : nullptr;
+    rp.tex_R = d ? d->R : 1;
+    rp.tex_V = d ? d->V : 0;
+    rp.K = s->K;
+    rp.delta = s->delta;
+    rp.t_term = s->t_term;
+    for (int v = 0; v < g->views; ++v) {
+        const mixrt_camera &c = cams[v];
+        mixrt::CamK &k = rp.cams[v];
+        for (int r = 0; r < 3; ++r) {
+            for (int q = 0; q < 3; ++q) k.R[3 * r + q] = c.c2w[4 * r + q];
+            k.o[r] = c.c2w[4 * r + 3];
+        }
+        const double half = 0.5 * (double)c.fov_y_deg * 3.14159265358979323846 / 180.0;
+        k.inv_f = (float)(std::tan(half) / (0.5 * (double)g->H));
+        for (int q = 0; q < 3; ++q) k.bg[q] = c.bg[q];
+    }
+}
+
+void fill_grid_params(mixrt::GridParams &gp, const mixrt_hash_grid *g)
+{
+    memset(&gp, 0, sizeof gp);
+    gp.table = g->data;
+    gp.log2_T = (uint32_t)g->log2_T;
+    gp.T_mask = (uint32_t)((1ull << g->log2_T) - 1);
+    gp.L = g->L;
+    int32_t N[MIXRT_MAX_LEVELS];
+    level_table(g->L, g->N_min, g->N_max, N);
+    const uint64_t T = 1ull << g->log2_T;
+    for (int l = 0; l < g->L; ++l) {
+        gp.N[l] = (uint32_t)N[l];
+        const uint64_t side = (uint64_t)N[l] + 1;
+        if (side * side * side <= T) gp.dense_mask |= 1u << l;
+    }
+}
+
+int finish_launch(mixrt_ctx *ctx, hipError_t e, const char *what)
+{
+    if (e != hipSuccess)
+        return fail(ctx, MIXRT_EDEVICE, "%s: launch failed: %s", what, hipGetErrorString(e));
+    if (ctx->flags & MIXRT_FLAG_SYNC_CHECK) {
+        e = hipStreamSynchronize(ctx->stream);
+        if (e == hipSuccess) e = hipGetLastError();
+        if (e != hipSuccess)
+            return fail(ctx, MIXRT_EDEVICE, "%s: device error: %s", what, hipGetErrorString(e));
+    }
+    return MIXRT_OK;
+}
+
+int bind_device(mixrt_ctx *ctx)
+{
+    hipError_t e = hipSetDevice(ctx->device);
+    if (e != hipSuccess)
+        return fail(ctx, MIXRT_EDEVICE, "hipSetDevice(%d): %s", ctx->device, hipGetErrorString(e));
+    return MIXRT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *mixrt_status_string(int s)
+{
+    switch (s) {
+    case MIXRT_OK: return "ok";
+    case MIXRT_EINVAL: return "invalid argument";
+    case MIXRT_ENOMEM: return "out of device memory";
+    case MIXRT_EDEVICE: return "device (HIP) error";
+    case MIXRT_EUNSUPPORTED: return "unsupported configuration";
+    default: return "unknown status";
+    }
+}
+
+const char *mixrt_last_error(const mixrt_ctx *ctx) { return ctx ? ctx->err.c_str() : ""; }
+
+const char *mixrt_thread_error(void) { return t_err.c_str(); }
+
+int mixrt_validate(const mixrt_gbuffer *gbuf, const mixrt_camera *cams, const mixrt_disp_tex *disp,
+                   const mixrt_hash_grid *grid, const mixrt_mlp *mlp, const mixrt_sampling *smp,
+                   char *msg, size_t cap)
+{
+    if (msg && cap) msg[0] = 0;
+    int hid = 0, nhid = 0;
+    return validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, cap}, &hid, &nhid);
+}
+
+int mixrt_level_resolutions(const mixrt_hash_grid *grid, int32_t *out_N)
+{
+    char buf[256];
+    if (!out_N) return fail(nullptr, MIXRT_EINVAL, "out_N is NULL");
+    if (!grid) return fail(nullptr, MIXRT_EINVAL, "grid is NULL");
+    if (grid->L < 1 || grid->L > MIXRT_MAX_LEVELS || grid->N_min < 1 || grid->N_max < grid->N_min ||
+        grid->N_max > (1 << 20)) {
+        snprintf(buf, sizeof buf, "grid L=%d N_min=%d N_max=%d", grid->L, grid->N_min, grid->N_max);
+        return fail(nullptr, MIXRT_EINVAL, "%s", buf);
+    }
+    level_table(grid->L, grid->N_min, grid->N_max, out_N);
+    return MIXRT_OK;
+}
+
+int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
+{
+    clear_err(nullptr);
+    if (!out) return fail(nullptr, MIXRT_EINVAL, "out is NULL");
+    *out = nullptr;
+    if (!ci) return fail(nullptr, MIXRT_EINVAL, "create_info is NULL");
+    int n = 0;
+    hipError_t e = hipGetDeviceCount(&n);
+    if (e != hipSuccess || n == 0)
+        return fail(nullptr, MIXRT_EDEVICE, "no HIP device: %s", hipGetErrorString(e));
+    if (ci->device < 0 || ci->device >= n)
+        return fail(nullptr, MIXRT_EINVAL, "device %d outside 0..%d", ci->device, n - 1);
+    hipDeviceProp_t prop;
+    e = hipGetDeviceProperties(&prop, ci->device);
+    if (e != hipSuccess)
+        return fail(nullptr, MIXRT_EDEVICE, "hipGetDeviceProperties: %s", hipGetErrorString(e));
+    if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
+        return fail(nullptr, MIXRT_EUNSUPPORTED, "device %d is %s, this library is built for gfx950",
+                    ci->device, prop.gcnArchName);
+    mixrt_ctx *ctx = new (std::nothrow) mixrt_ctx;
+    if (!ctx) return fail(nullptr, MIXRT_ENOMEM, "host allocation failed");
+    ctx->device = ci->device;
+    ctx->stream = (hipStream_t)ci->hip_stream;
+    ctx->flags = ci->flags;
+    ctx->cus = prop.multiProcessorCount;
+    *out = ctx;
+    return MIXRT_OK;
+}
+
+int mixrt_destroy(mixrt_ctx *ctx)
+{
+    delete ctx;
+    return MIXRT_OK;
+}
+
+int mixrt_sync(mixrt_ctx *ctx)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    int rc = bind_device(ctx);
+    if (rc) return rc;
+    hipError_t e = hipStreamSynchronize(ctx->stream);
+    if (e != hipSuccess)
+        return fail(ctx, MIXRT_EDEVICE, "stream synchronize: %s", hipGetErrorString(e));
+    return MIXRT_OK;
+}
+
+int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                 const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                 const mixrt_sampling *smp, float *out_rgba)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    int hid = 0, nhid = 0;
+    int rc = validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, sizeof msg}, &hid, &nhid);
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (!out_rgba) return fail(ctx, MIXRT_EINVAL, "out_rgba is NULL");
+    if (!aligned16(out_rgba)) return fail(ctx, MIXRT_EINVAL, "out_rgba not 16-byte aligned");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::RenderLaunch L;
+    fill_ray_params(L.rp, gbuf, cams, disp, smp);
+    fill_grid_params(L.gp, grid);
+    L.weights = (const _Float16 *)mlp->data;
+    L.out = (float4 *)out_rgba;
+    L.view_sh = mlp->view_sh_dim;
+    L.xf16 = disp->dtype == MIXRT_F16;
+    L.tf16 = grid->dtype == MIXRT_F16;
+    L.F = grid->F;
+    L.in = mlp->width[0];
+    L.hid = hid;
+    L.nhid = nhid;
+    L.cus = ctx->cus;
+    return finish_launch(ctx, mixrt::launch_render(L, ctx->stream), "render");
+}
+
+int mixrt_debug_ray_setup(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                          const mixrt_disp_tex *disp, const mixrt_sampling *smp, float *out_x,
+                          int32_t *out_hit)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    Msg m{msg, sizeof msg};
+    int rc;
+    if ((rc = check_gbuf(gbuf, cams, m)) || (rc = check_disp(disp, m)) ||
+        (rc = check_sampling(smp, m)))
+        return fail(ctx, rc, "%s", msg);
+    if (!out_x) return fail(ctx, MIXRT_EINVAL, "out_x is NULL");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::RayParams rp;
+    fill_ray_params(rp, gbuf, cams, disp, smp);
+    return finish_launch(ctx,
+                         mixrt::launch_ray_setup(rp, disp->dtype == MIXRT_F16, out_x, out_hit,
+                                                 ctx->stream),
+                         "ray_setup");
+}
+
+int mixrt_debug_hash_encode(mixrt_ctx *ctx, const mixrt_hash_grid *grid, const float *x, int64_t n,
+                            int32_t *out_corner, uint32_t *out_idx, float *out_w, float *out_feat)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    int rc = check_grid(grid, Msg{msg, sizeof msg});
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (n < 0 || n >= ((int64_t)1 << 31)) return fail(ctx, MIXRT_EINVAL, "n=%lld", (long long)n);
+    if (n > 0 && !x) return fail(ctx, MIXRT_EINVAL, "x is NULL");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::GridParams gp;
+    fill_grid_params(gp, grid);
+    return finish_launch(ctx,
+                         mixrt::launch_hash_encode(gp, grid->F, grid->dtype == MIXRT_F16, x, n,
+                                                   out_corner, out_idx, out_w, out_feat,
+                                                   ctx->stream),
+                         "hash_encode");
+}
+
+int mixrt_debug_mlp(mixrt_ctx *ctx, const mixrt_mlp *mlp, const uint16_t *in_f16, int64_t n,
+                    float *out4)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    int hid = 0, nhid = 0;
+    int rc = check_mlp(mlp, -1, Msg{msg, sizeof msg}, &hid, &nhid);
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (n < 0 || n >= ((int64_t)1 << 40)) return fail(ctx, MIXRT_EINVAL, "n=%lld", (long long)n);
+    if (n > 0 && (!in_f16 || !out4)) return fail(ctx, MIXRT_EINVAL, "in or out is NULL");
+    if ((rc = bind_device(ctx))) return rc;
+    return finish_launch(ctx,
+                         mixrt::launch_mlp(mlp->width[0], hid, nhid, (const _Float16 *)mlp->data,
+                                           (const _Float16 *)in_f16, n, (float4 *)out4,
+                                           ctx->stream),
+                         "mlp");
+}
+
+int mixrt_debug_composite(mixrt_ctx *ctx, const float *srgb, int64_t rays,
+                          const mixrt_sampling *smp, const float *bg, float *out_rgba)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    int rc = check_sampling(smp, Msg{msg, sizeof msg});
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (!bg) return fail(ctx, MIXRT_EINVAL, "bg is NULL");
+    if (rays < 0) return fail(ctx, MIXRT_EINVAL, "rays=%lld", (long long)rays);
+    if (rays > 0 && (!srgb || !out_rgba)) return fail(ctx, MIXRT_EINVAL, "srgb or out is NULL");
+    if (rays > 0 && (!aligned16(srgb) || !aligned16(out_rgba)))
+        return fail(ctx, MIXRT_EINVAL, "srgb/out_rgba not 16-byte aligned");
+    if ((rc = bind_device(ctx))) return rc;
+    return finish_launch(ctx,
+                         mixrt::launch_composite((const float4 *)srgb, rays, smp->K, smp->delta,
+                                                 smp->t_term, bg, (float4 *)out_rgba, ctx->stream),
+                         "composite");
+}
+
+}  // extern "C"

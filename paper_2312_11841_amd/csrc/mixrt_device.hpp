@@ -1,0 +1,544 @@
+// Device building blocks of the MixRT per-pixel path for gfx950 (CDNA4).
+//
+// Every stage of the path is one inline device function here; the fused
+// render kernel and the per-stage kernels call the same functions, so the
+// stage entry points exercise exactly the arithmetic mixrt_render runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mixrt {
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+constexpr int kMaxViews = 16;
+constexpr int kMaxLevels = 32;
+constexpr int kWave = 64;
+
+// Per-view camera constants, prepared on the host from mixrt_camera.
+struct CamK {
+    float R[9];      // rotation, row-major
+    float o[3];      // centre
+    float inv_f;     // 1 / focal length in pixels: f = (H/2) / tan(fov_y/2)
+    float bg[3];
+};
+
+struct RayParams {
+    const float4 *g0;
+    int32_t views, W, H;
+    int32_t rays;           // views * H * W (< 2^31)
+    const void *tex;
+    int32_t tex_R, tex_V;
+    int32_t K;
+    float delta;
+    float t_term;
+    CamK cams[kMaxViews];
+};
+
+struct GridParams {
+    const void *table;
+    uint32_t T_mask;        // T - 1
+    uint32_t log2_T;
+    int32_t L;
+    uint32_t dense_mask;    // bit l: level l indexes its vertices densely
+    uint32_t N[kMaxLevels];
+};
+
+// --------------------------------------------------------------------------
+// Sec. 3.1: one ray through the centre of each pixel.
+// --------------------------------------------------------------------------
+struct Ray {
+    float ox, oy, oz;
+    float dx, dy, dz;
+    int32_t view;
+};
+
+__device__ __forceinline__ Ray pixel_ray(const RayParams &p, int32_t ray)
+{
+    const uint32_t hw = (uint32_t)p.H * (uint32_t)p.W;
+    const uint32_t view = (uint32_t)ray / hw;
+    const uint32_t rem = (uint32_t)ray - view * hw;
+    const uint32_t j = rem / (uint32_t)p.W;
+    const uint32_t i = rem - j * (uint32_t)p.W;
+    const CamK &c = p.cams[view];
+    const float cx = ((float)i + 0.5f - 0.5f * (float)p.W) * c.inv_f;
+    const float cy = -(((float)j + 0.5f - 0.5f * (float)p.H) * c.inv_f);
+    float dx = c.R[0] * cx + c.R[1] * cy - c.R[2];
+    float dy = c.R[3] * cx + c.R[4] * cy - c.R[5];
+    float dz = c.R[6] * cx + c.R[7] * cy - c.R[8];
+    const float inv = 1.0f / sqrtf(dx * dx + dy * dy + dz * dz);
+    Ray r;
+    r.ox = c.o[0];
+    r.oy = c.o[1];
+    r.oz = c.o[2];
+    r.dx = dx * inv;
+    r.dy = dy * inv;
+    r.dz = dz * inv;
+    r.view = (int32_t)view;
+    return r;
+}
+
+// --------------------------------------------------------------------------
+// Real spherical harmonics of a unit direction, degrees 0..3 (16 functions,
+// ordered by degree then m = -l..l, orthonormal, no Condon-Shortley phase).
+// Written as Cartesian polynomials; the constants are the normalisations
+// sqrt((2l+1)/(4 pi) (l-|m|)!/(l+|m|)!) (times sqrt 2 for m != 0) folded into
+// each polynomial.
+// --------------------------------------------------------------------------
+template <int NB>
+__device__ __forceinline__ void sh_basis(float x, float y, float z, float *Y)
+{
+    static_assert(NB >= 1 && NB <= 16, "degree <= 3");
+    Y[0] = 0.28209479177387814f;
+    if (NB > 1) Y[1] = 0.48860251190291992f * y;
+    if (NB > 2) Y[2] = 0.48860251190291992f * z;
+    if (NB > 3) Y[3] = 0.48860251190291992f * x;
+    const float xx = x * x, yy = y * y, zz = z * z;
+    if (NB > 4) Y[4] = 1.0925484305920792f * x * y;
+    if (NB > 5) Y[5] = 1.0925484305920792f * y * z;
+    if (NB > 6) Y[6] = 0.31539156525252005f * (3.0f * zz - 1.0f);
+    if (NB > 7) Y[7] = 1.0925484305920792f * x * z;
+    if (NB > 8) Y[8] = 0.54627421529603959f * (xx - yy);
+    if (NB > 9) Y[9] = 0.59004358992664352f * y * (3.0f * xx - yy);
+    if (NB > 10) Y[10] = 2.8906114426405538f * x * y * z;
+    if (NB > 11) Y[11] = 0.45704579946446572f * y * (5.0f * zz - 1.0f);
+    if (NB > 12) Y[12] = 0.37317633259011540f * z * (5.0f * zz - 3.0f);
+    if (NB > 13) Y[13] = 0.45704579946446572f * x * (5.0f * zz - 1.0f);
+    if (NB > 14) Y[14] = 1.4453057213202769f * z * (xx - yy);
+    if (NB > 15) Y[15] = 0.59004358992664352f * x * (xx - 3.0f * yy);
+}
+
+// --------------------------------------------------------------------------
+// Eq. 2: bilinear fetch of the V texture channels at p_t (texel centres at
+// (i + 0.5)/R, clamp to edge), dotted with the SH basis of d: the signed
+// displacement length along the ray.
+// --------------------------------------------------------------------------
+template <typename XT>
+__device__ __forceinline__ float displacement(const void *tex_, int R, int V, float u, float v,
+                                              float dx, float dy, float dz)
+{
+    const XT *tex = (const XT *)tex_;
+    float a = u * (float)R - 0.5f;
+    float b = v * (float)R - 0.5f;
+    // keep non-finite or far-out coordinates on the edge texels
+    a = fminf(fmaxf(a, -1.0f), (float)R);
+    b = fminf(fmaxf(b, -1.0f), (float)R);
+    if (!(a == a)) a = 0.0f;
+    if (!(b == b)) b = 0.0f;
+    const float fa = floorf(a), fb = floorf(b);
+    const float wa = a - fa, wb = b - fb;
+    const int i0 = (int)fa, j0 = (int)fb;
+    const int ia0 = min(max(i0, 0), R - 1), ia1 = min(max(i0 + 1, 0), R - 1);
+    const int jb0 = min(max(j0, 0), R - 1), jb1 = min(max(j0 + 1, 0), R - 1);
+    const float w00 = (1.0f - wa) * (1.0f - wb), w01 = wa * (1.0f - wb);
+    const float w10 = (1.0f - wa) * wb, w11 = wa * wb;
+    const XT *t00 = tex + ((int64_t)jb0 * R + ia0) * V;
+    const XT *t01 = tex + ((int64_t)jb0 * R + ia1) * V;
+    const XT *t10 = tex + ((int64_t)jb1 * R + ia0) * V;
+    const XT *t11 = tex + ((int64_t)jb1 * R + ia1) * V;
+    float Y[16];
+    sh_basis<16>(dx, dy, dz, Y);
+    float s = 0.0f;
+    constexpr int EPV = 16 / (int)sizeof(XT);  // elements per 16-byte load
+    if (V % EPV == 0) {
+        // texels are whole 16-byte lines: one vector load per texel and chunk
+#pragma unroll
+        for (int c0 = 0; c0 < 16; c0 += EPV) {
+            if (c0 < V) {
+                XT e00[EPV], e01[EPV], e10[EPV], e11[EPV];
+                *(uint4 *)e00 = *(const uint4 *)(t00 + c0);
+                *(uint4 *)e01 = *(const uint4 *)(t01 + c0);
+                *(uint4 *)e10 = *(const uint4 *)(t10 + c0);
+                *(uint4 *)e11 = *(const uint4 *)(t11 + c0);
+#pragma unroll
+                for (int e = 0; e < EPV; ++e) {
+                    const float m = w00 * (float)e00[e] + w01 * (float)e01[e] +
+                                    w10 * (float)e10[e] + w11 * (float)e11[e];
+                    s += Y[c0 + e] * m;
+                }
+            }
+        }
+    } else {
+#pragma unroll
+        for (int c = 0; c < 16; ++c) {
+            if (c < V) {
+                const float m = w00 * (float)t00[c] + w01 * (float)t01[c] + w10 * (float)t10[c] +
+                                w11 * (float)t11[c];
+                s += Y[c] * m;
+            }
+        }
+    }
+    return s;
+}
+
+// --------------------------------------------------------------------------
+// Sec. 2.1: contraction of unbounded space into the ball of radius 2
+// (identity inside the unit ball, (2 - 1/r) q/r outside), then the affine
+// map of [-2, 2]^3 onto the grid's unit cube.
+// --------------------------------------------------------------------------
+__device__ __forceinline__ void contract_to_cube(float qx, float qy, float qz, float &x0,
+                                                 float &x1, float &x2)
+{
+    const float r2 = qx * qx + qy * qy + qz * qz;
+    float s = 1.0f;
+    if (r2 > 1.0f) {
+        const float r = sqrtf(r2);
+        s = (2.0f - 1.0f / r) / r;
+    }
+    x0 = fminf(fmaxf((qx * s + 2.0f) * 0.25f, 0.0f), 1.0f);
+    x1 = fminf(fmaxf((qy * s + 2.0f) * 0.25f, 0.0f), 1.0f);
+    x2 = fminf(fmaxf((qz * s + 2.0f) * 0.25f, 0.0f), 1.0f);
+    if (!(x0 == x0)) x0 = 0.0f;
+    if (!(x1 == x1)) x1 = 0.0f;
+    if (!(x2 == x2)) x2 = 0.0f;
+}
+
+// Steps before the grid for sample k of a ray: hit test, Eq. 2 calibration,
+// sample placement, contraction.  Returns false for a miss.
+template <typename XT>
+__device__ __forceinline__ bool sample_position(const RayParams &p, const Ray &r, float4 g, int k,
+                                                float &x0, float &x1, float &x2)
+{
+    const float t = g.x;
+    const bool hit = t > 0.0f && t < INFINITY;
+    if (!hit) {
+        x0 = x1 = x2 = 0.0f;
+        return false;
+    }
+    const float s = displacement<XT>(p.tex, p.tex_R, p.tex_V, g.y, g.z, r.dx, r.dy, r.dz);
+    const float off = t + s + ((float)k - 0.5f * (float)(p.K - 1)) * p.delta;
+    contract_to_cube(r.ox + off * r.dx, r.oy + off * r.dy, r.oz + off * r.dz, x0, x1, x2);
+    return true;
+}
+
+// --------------------------------------------------------------------------
+// Sec. 3.1 / 4.3.3: one level of the multiresolution hash encoding.
+// The voxel is chosen from the fp32 product x * N_l (one rounding, no
+// contraction into an FMA) so corners and indices are reproducible.
+// --------------------------------------------------------------------------
+template <int F, bool F16>
+struct TableEntry;
+
+template <>
+struct TableEntry<2, true> {
+    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    {
+        const uint32_t raw = ((const uint32_t *)t)[idx];
+        const h2 h = __builtin_bit_cast(h2, raw);
+        v[0] = (float)h.x;
+        v[1] = (float)h.y;
+    }
+};
+
+template <>
+struct TableEntry<2, false> {
+    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    {
+        const float2 f = ((const float2 *)t)[idx];
+        v[0] = f.x;
+        v[1] = f.y;
+    }
+};
+
+template <>
+struct TableEntry<4, true> {
+    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    {
+        const uint2 raw = ((const uint2 *)t)[idx];
+        const h2 a = __builtin_bit_cast(h2, raw.x), b = __builtin_bit_cast(h2, raw.y);
+        v[0] = (float)a.x;
+        v[1] = (float)a.y;
+        v[2] = (float)b.x;
+        v[3] = (float)b.y;
+    }
+};
+
+template <>
+struct TableEntry<4, false> {
+    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    {
+        const float4 f = ((const float4 *)t)[idx];
+        v[0] = f.x;
+        v[1] = f.y;
+        v[2] = f.z;
+        v[3] = f.w;
+    }
+};
+
+constexpr uint32_t kPrimeY = 2654435761u;
+constexpr uint32_t kPrimeZ = 805459861u;
+
+struct LevelDebug {
+    int32_t *corner;  // [3]
+    uint32_t *idx;    // [8]
+    float *w;         // [8]
+};
+
+template <int F, bool F16, bool DEBUG>
+__device__ __forceinline__ void hash_level(const void *table_l, uint32_t N, bool dense,
+                                           uint32_t T_mask, float x0, float x1, float x2,
+                                           float *feat, LevelDebug dbg)
+{
+    const float Nf = (float)N;
+    const float p0 = __fmul_rn(x0, Nf), p1 = __fmul_rn(x1, Nf), p2 = __fmul_rn(x2, Nf);
+    const int32_t top = (int32_t)N - 1;
+    const int32_t c0 = min(max((int32_t)floorf(p0), 0), top);
+    const int32_t c1 = min(max((int32_t)floorf(p1), 0), top);
+    const int32_t c2 = min(max((int32_t)floorf(p2), 0), top);
+    const float f0 = p0 - (float)c0, f1 = p1 - (float)c1, f2 = p2 - (float)c2;
+    uint32_t idx[8];
+    if (dense) {
+        const uint32_t s1 = N + 1u, s2 = s1 * s1;
+        const uint32_t base = (uint32_t)c0 + (uint32_t)c1 * s1 + (uint32_t)c2 * s2;
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            idx[b] = base + (uint32_t)(b & 1) + ((b & 2) ? s1 : 0u) + ((b & 4) ? s2 : 0u);
+    } else {
+        const uint32_t hy0 = (uint32_t)c1 * kPrimeY, hy1 = hy0 + kPrimeY;
+        const uint32_t hz0 = (uint32_t)c2 * kPrimeZ, hz1 = hz0 + kPrimeZ;
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            idx[b] = (((uint32_t)c0 + (uint32_t)(b & 1)) ^ ((b & 2) ? hy1 : hy0) ^
+                      ((b & 4) ? hz1 : hz0)) & T_mask;
+    }
+    float v[8][F];
+#pragma unroll
+    for (int b = 0; b < 8; ++b)
+        TableEntry<F, F16>::load(table_l, idx[b], v[b]);
+    const float g0[2] = {1.0f - f0, f0}, g1[2] = {1.0f - f1, f1}, g2[2] = {1.0f - f2, f2};
+#pragma unroll
+    for (int f = 0; f < F; ++f)
+        feat[f] = 0.0f;
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const float w = g0[b & 1] * g1[(b >> 1) & 1] * g2[(b >> 2) & 1];
+#pragma unroll
+        for (int f = 0; f < F; ++f)
+            feat[f] += w * v[b][f];
+        if (DEBUG) {
+            dbg.idx[b] = idx[b];
+            dbg.w[b] = w;
+        }
+    }
+    if (DEBUG) {
+        dbg.corner[0] = c0;
+        dbg.corner[1] = c1;
+        dbg.corner[2] = c2;
+    }
+}
+
+__device__ __forceinline__ const void *level_base(const GridParams &g, int l, int F, bool f16)
+{
+    const size_t esz = f16 ? 2 : 4;
+    return (const char *)g.table + (size_t)l * ((size_t)g.T_mask + 1) * (size_t)F * esz;
+}
+
+// --------------------------------------------------------------------------
+// Sec. 3.1: the small MLP on MFMA.  One call evaluates 16 samples (one
+// 16-wide N tile) of a wave: the layers are computed transposed,
+// Z^T[out][sample] = W^T[out][in] X^T[in][sample], so the fp32 accumulator
+// of one layer, after ReLU and conversion, is already the B operand of the
+// next layer in registers (the input neurons are permuted consistently in
+// the A operand instead of moving data across lanes).
+//
+// gfx950 lane layouts (wave64), lane l, c = l & 15, g = l >> 4:
+//   mfma_f32_16x16x32_f16  A: row c, k = 8g..8g+7;  B: column c, k = 8g..8g+7
+//   mfma_f32_16x16x16_f16  A: row c, k = 4g..4g+3;  B: column c, k = 4g..4g+3
+//   D (both):              column c, rows 4g..4g+3
+//
+// Every MFMA here starts from a zero accumulator and the partial products of
+// the K chunks are summed on the VALU: no MFMA reads another MFMA's result as
+// its C operand.  With this compiler, chains that fed a 16x16x32 result into
+// a 16x16x16 accumulate (with a different destination register) read a stale
+// accumulator on gfx950; the zero-C form has no such dependency.
+// --------------------------------------------------------------------------
+
+// Input slot -> neuron for a layer fed from the previous layer's registers.
+// 32-wide chunk ch, slot 8g + j: tile 2ch + (j >> 2), row 4g + (j & 3).
+__device__ __forceinline__ int perm32(int ch, int g, int j)
+{
+    return (2 * ch + (j >> 2)) * 16 + 4 * g + (j & 3);
+}
+
+template <int KIN, int MOUT, bool FROM_REGS>
+struct LayerA {
+    static constexpr int NC = KIN / 32;            // 32-deep chunks
+    static constexpr int R16 = (KIN % 32) / 16;    // one trailing 16-deep chunk
+    static constexpr int MT = (MOUT + 15) / 16;    // 16-row output tiles
+    static_assert(KIN % 16 == 0, "input width must be a multiple of 16");
+    static_assert(!FROM_REGS || KIN == 16 || KIN % 32 == 0, "hidden width 16, 32 or 64");
+    h8 a32[MT][NC > 0 ? NC : 1];
+    h4 a16[MT];
+
+    // W: fp16 [KIN][MOUT] row-major in global memory.
+    __device__ __forceinline__ void load(const _Float16 *W, int lane)
+    {
+        const int c = lane & 15, g = lane >> 4;
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) {
+            const int o = mt * 16 + c;
+            const bool ok = o < MOUT;
+#pragma unroll
+            for (int ch = 0; ch < NC; ++ch) {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const int k = FROM_REGS ? perm32(ch, g, j) : ch * 32 + 8 * g + j;
+                    a32[mt][ch][j] = ok ? W[k * MOUT + o] : (_Float16)0.0f;
+                }
+            }
+            if (R16) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int k = NC * 32 + 4 * g + j;
+                    a16[mt][j] = ok ? W[k * MOUT + o] : (_Float16)0.0f;
+                }
+            }
+        }
+    }
+};
+
+// Activations of one 16-sample tile held as MFMA D fragments: acc[t][j] is
+// neuron 16t + 4g + j of sample column c.
+template <int W>
+struct Act {
+    static constexpr int MT = (W + 15) / 16;
+    f4 acc[MT];
+};
+
+template <int KIN, int MOUT>
+__device__ __forceinline__ void layer_from_regs(const LayerA<KIN, MOUT, true> &A,
+                                                const Act<KIN> &in, Act<MOUT> &out)
+{
+    h8 b32[LayerA<KIN, MOUT, true>::NC > 0 ? LayerA<KIN, MOUT, true>::NC : 1];
+    h4 b16;
+#pragma unroll
+    for (int ch = 0; ch < LayerA<KIN, MOUT, true>::NC; ++ch) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            b32[ch][j] = (_Float16)fmaxf(in.acc[2 * ch][j], 0.0f);
+            b32[ch][j + 4] = (_Float16)fmaxf(in.acc[2 * ch + 1][j], 0.0f);
+        }
+    }
+    if (LayerA<KIN, MOUT, true>::R16) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            b16[j] = (_Float16)fmaxf(in.acc[0][j], 0.0f);
+    }
+#pragma unroll
+    for (int mt = 0; mt < Act<MOUT>::MT; ++mt) {
+        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+        f4 acc = zero;
+#pragma unroll
+        for (int ch = 0; ch < LayerA<KIN, MOUT, true>::NC; ++ch)
+            acc += __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], zero, 0, 0, 0);
+        if (LayerA<KIN, MOUT, true>::R16)
+            acc += __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
+        out.acc[mt] = acc;
+    }
+}
+
+// First layer: B operand read from a [16][ld] fp16 tile (row = sample) in
+// LDS or global memory.
+template <int KIN, int MOUT>
+__device__ __forceinline__ void layer_from_rows(const LayerA<KIN, MOUT, false> &A,
+                                                const _Float16 *rows, int ld, int lane,
+                                                Act<MOUT> &out)
+{
+    const int c = lane & 15, g = lane >> 4;
+    const _Float16 *row = rows + c * ld;
+    h8 b32[LayerA<KIN, MOUT, false>::NC > 0 ? LayerA<KIN, MOUT, false>::NC : 1];
+    h4 b16;
+#pragma unroll
+    for (int ch = 0; ch < LayerA<KIN, MOUT, false>::NC; ++ch)
+        b32[ch] = *(const h8 *)(row + ch * 32 + 8 * g);
+    if (LayerA<KIN, MOUT, false>::R16)
+        b16 = *(const h4 *)(row + LayerA<KIN, MOUT, false>::NC * 32 + 4 * g);
+#pragma unroll
+    for (int mt = 0; mt < Act<MOUT>::MT; ++mt) {
+        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+        f4 acc = zero;
+#pragma unroll
+        for (int ch = 0; ch < LayerA<KIN, MOUT, false>::NC; ++ch)
+            acc += __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], zero, 0, 0, 0);
+        if (LayerA<KIN, MOUT, false>::R16)
+            acc += __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
+        out.acc[mt] = acc;
+    }
+}
+
+// The whole MLP: IN -> HID (ReLU) -> [HID -> HID (ReLU)] x (NHID-1) -> 4.
+template <int IN, int HID, int NHID>
+struct MlpWeights {
+    static_assert(NHID >= 1 && NHID <= 3, "1..3 hidden layers");
+    LayerA<IN, HID, false> first;
+    LayerA<HID, HID, true> mid[NHID > 1 ? NHID - 1 : 1];
+    LayerA<HID, 4, true> head;
+
+    __device__ __forceinline__ void load(const _Float16 *W, int lane)
+    {
+        first.load(W, lane);
+        const _Float16 *p = W + IN * HID;
+#pragma unroll
+        for (int m = 0; m < NHID - 1; ++m) {
+            mid[m].load(p, lane);
+            p += HID * HID;
+        }
+        head.load(p, lane);
+    }
+};
+
+// Returns the raw head outputs: lanes 0..15 hold (sigma_raw, r, g, b) of
+// sample column (lane & 15) in elements 0..3; other lanes hold padding.
+template <int IN, int HID, int NHID>
+__device__ __forceinline__ f4 mlp_tile(const MlpWeights<IN, HID, NHID> &Wt,
+                                       const _Float16 *rows, int ld, int lane)
+{
+    Act<HID> a, b;
+    layer_from_rows<IN, HID>(Wt.first, rows, ld, lane, a);
+#pragma unroll
+    for (int m = 0; m < NHID - 1; ++m) {
+        layer_from_regs<HID, HID>(Wt.mid[m], a, b);
+        a = b;
+    }
+    Act<4> o;
+    layer_from_regs<HID, 4>(Wt.head, a, o);
+    return o.acc[0];
+}
+
+// Output activations (Sec. 3.1): density exp(.), colour sigmoid(.).
+__device__ __forceinline__ float4 mlp_activate(f4 o)
+{
+    return make_float4(expf(o[0]), 1.0f / (1.0f + expf(-o[1])), 1.0f / (1.0f + expf(-o[2])),
+                       1.0f / (1.0f + expf(-o[3])));
+}
+
+// --------------------------------------------------------------------------
+// Eq. 1 front to back: alpha_k = 1 - exp(-sigma_k delta), the running
+// transmittance excludes sample k, the remaining transmittance weights the
+// background, and a ray stops once its transmittance is below t_term.
+// --------------------------------------------------------------------------
+struct Composite {
+    float r = 0.0f, g = 0.0f, b = 0.0f, T = 1.0f;
+
+    __device__ __forceinline__ bool add(float4 s, float delta, float t_term)
+    {
+        const float alpha = 1.0f - expf(-s.x * delta);
+        const float w = T * alpha;
+        r += w * s.y;
+        g += w * s.z;
+        b += w * s.w;
+        T *= 1.0f - alpha;
+        return T >= t_term;
+    }
+
+    __device__ __forceinline__ float4 finish(float bgr, float bgg, float bgb) const
+    {
+        return make_float4(r + T * bgr, g + T * bgg, b + T * bgb, 1.0f - T);
+    }
+};
+
+}  // namespace mixrt

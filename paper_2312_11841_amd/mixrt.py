@@ -1,0 +1,310 @@
+"""Python binding of libmixrt.so (the C ABI in include/mixrt.h).
+
+Argument marshalling only: every step of the rendering path runs in the HIP
+kernels behind the C ABI.  PyTorch provides device memory and the stream.
+If the library is missing, importing works but every call raises
+MixrtUnavailable: there is no CPU fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmixrt.so")
+
+MIXRT_OK = 0
+MIXRT_EINVAL = -1
+MIXRT_ENOMEM = -2
+MIXRT_EDEVICE = -3
+MIXRT_EUNSUPPORTED = -4
+MIXRT_F32, MIXRT_F16, MIXRT_U8 = 0, 1, 2
+MIXRT_DISP_ALONG_RAY = 0
+MIXRT_FLAG_SYNC_CHECK = 1
+MAX_VIEWS, MAX_LEVELS, MAX_LAYERS = 16, 32, 8
+
+# Every symbol include/mixrt.h declares.
+EXPORTS = (
+    "mixrt_create", "mixrt_destroy", "mixrt_sync", "mixrt_validate",
+    "mixrt_level_resolutions", "mixrt_render", "mixrt_debug_ray_setup",
+    "mixrt_debug_hash_encode", "mixrt_debug_mlp", "mixrt_debug_composite",
+    "mixrt_status_string", "mixrt_last_error", "mixrt_thread_error",
+)
+
+
+class MixrtUnavailable(RuntimeError):
+    pass
+
+
+class MixrtError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{status_string(status)} ({status}): {msg}")
+        self.status = status
+
+
+# --- descriptor structs (field order and types as in mixrt.h) ------------------
+
+class CreateInfo(C.Structure):
+    _fields_ = [("device", C.c_int32), ("hip_stream", C.c_void_p), ("flags", C.c_uint32)]
+
+
+class GBuffer(C.Structure):
+    _fields_ = [("views", C.c_int32), ("W", C.c_int32), ("H", C.c_int32),
+                ("g0", C.c_void_p), ("g1", C.c_void_p)]
+
+
+class Camera(C.Structure):
+    _fields_ = [("c2w", C.c_float * 12), ("fov_y_deg", C.c_float), ("bg", C.c_float * 3)]
+
+
+class DispTex(C.Structure):
+    _fields_ = [("R", C.c_int32), ("V", C.c_int32), ("dtype", C.c_int32), ("mode", C.c_int32),
+                ("data", C.c_void_p)]
+
+
+class HashGrid(C.Structure):
+    _fields_ = [("L", C.c_int32), ("log2_T", C.c_int32), ("F", C.c_int32),
+                ("N_min", C.c_int32), ("N_max", C.c_int32), ("dtype", C.c_int32),
+                ("data", C.c_void_p)]
+
+
+class Mlp(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("width", C.c_int32 * (MAX_LAYERS + 1)),
+                ("view_sh_dim", C.c_int32), ("data", C.c_void_p)]
+
+
+class Sampling(C.Structure):
+    _fields_ = [("K", C.c_int32), ("delta", C.c_float), ("t_term", C.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libmixrt.so, or raise MixrtUnavailable (no fallback path exists)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise MixrtUnavailable(
+                f"{LIB_PATH} is missing: build it with `python __graft_entry__.py` "
+                "or `python paper_2312_11841_amd/build.py`")
+        L = C.CDLL(LIB_PATH)
+        P, I64 = C.c_void_p, C.c_int64
+        sig = {
+            "mixrt_create": (C.c_int, [C.POINTER(C.c_void_p), C.POINTER(CreateInfo)]),
+            "mixrt_destroy": (C.c_int, [P]),
+            "mixrt_sync": (C.c_int, [P]),
+            "mixrt_validate": (C.c_int, [C.POINTER(GBuffer), C.POINTER(Camera),
+                                         C.POINTER(DispTex), C.POINTER(HashGrid),
+                                         C.POINTER(Mlp), C.POINTER(Sampling),
+                                         C.c_char_p, C.c_size_t]),
+            "mixrt_level_resolutions": (C.c_int, [C.POINTER(HashGrid), P]),
+            "mixrt_render": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
+                                       C.POINTER(DispTex), C.POINTER(HashGrid), C.POINTER(Mlp),
+                                       C.POINTER(Sampling), P]),
+            "mixrt_debug_ray_setup": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
+                                                C.POINTER(DispTex), C.POINTER(Sampling), P, P]),
+            "mixrt_debug_hash_encode": (C.c_int, [P, C.POINTER(HashGrid), P, I64, P, P, P, P]),
+            "mixrt_debug_mlp": (C.c_int, [P, C.POINTER(Mlp), P, I64, P]),
+            "mixrt_debug_composite": (C.c_int, [P, P, I64, C.POINTER(Sampling), P, P]),
+            "mixrt_status_string": (C.c_char_p, [C.c_int]),
+            "mixrt_last_error": (C.c_char_p, [P]),
+            "mixrt_thread_error": (C.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().mixrt_status_string(status).decode()
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+# --- descriptors from scene data -------------------------------------------------
+
+_DT = {"float32": MIXRT_F32, "float16": MIXRT_F16}
+
+
+def _dtype_code(t) -> int:
+    return _DT[str(t.dtype).replace("torch.", "")]
+
+
+def make_cameras(cams: np.ndarray):
+    cams = np.asarray(cams, np.float32).reshape(-1, 16)
+    arr = (Camera * cams.shape[0])()
+    for v in range(cams.shape[0]):
+        arr[v].c2w[:] = [float(x) for x in cams[v, :12]]
+        arr[v].fov_y_deg = float(cams[v, 12])
+        arr[v].bg[:] = [float(x) for x in cams[v, 13:16]]
+    return arr
+
+
+def make_sampling(K: int, delta: float, t_term: float) -> Sampling:
+    return Sampling(int(K), float(delta), float(t_term))
+
+
+def make_grid(table, N_min: int, N_max: int) -> HashGrid:
+    L, T, F = table.shape
+    return HashGrid(L, int(T).bit_length() - 1, F, int(N_min), int(N_max),
+                    _dtype_code(table), _ptr(table))
+
+
+def make_mlp(weights, widths, view_sh_dim: int) -> Mlp:
+    m = Mlp()
+    m.n_layers = len(widths) - 1
+    for i, w in enumerate(widths):
+        m.width[i] = int(w)
+    m.view_sh_dim = int(view_sh_dim)
+    m.data = _ptr(weights)
+    return m
+
+
+@dataclass
+class DeviceScene:
+    """A scene's arrays in device memory plus the C descriptors that point at
+    them.  Keeps the tensors alive as long as the descriptors are used."""
+
+    g0: object
+    tex: object
+    table: object
+    weights: object
+    cams: object
+    gbuf: GBuffer
+    disp: DispTex
+    grid: HashGrid
+    mlp: Mlp
+    smp: Sampling
+    rays: int
+
+    @classmethod
+    def from_scene(cls, scene, device="cuda"):
+        import torch
+        cfg = scene.cfg
+        g0 = torch.from_numpy(np.ascontiguousarray(scene.g0)).to(device)
+        tex = torch.from_numpy(np.ascontiguousarray(scene.tex)).to(device)
+        table = torch.from_numpy(np.ascontiguousarray(scene.table)).to(device)
+        weights = torch.from_numpy(scene.weights_flat.view(np.uint16).astype(np.int16)).to(device)
+        gbuf = GBuffer(cfg.views, cfg.W, cfg.rows_kept, _ptr(g0), 0)
+        disp = DispTex(cfg.tex_R, cfg.tex_V, _dtype_code(tex), MIXRT_DISP_ALONG_RAY, _ptr(tex))
+        grid = make_grid(table, cfg.N_min, cfg.N_max)
+        mlp = make_mlp(weights, cfg.widths, cfg.view_sh_dim)
+        smp = make_sampling(cfg.K, cfg.delta, cfg.t_term)
+        return cls(g0, tex, table, weights, make_cameras(scene.cams), gbuf, disp, grid, mlp,
+                   smp, cfg.rays)
+
+
+# --- the library handle ------------------------------------------------------------
+
+class Renderer:
+    """One mixrt context bound to a device and a HIP stream."""
+
+    def __init__(self, device: int = 0, stream=None, sync_check: bool = False):
+        import torch
+        self.device = device
+        if stream is None:
+            stream = torch.cuda.current_stream(device)
+        self.stream = stream
+        ci = CreateInfo(device, C.c_void_p(int(stream.cuda_stream)),
+                        MIXRT_FLAG_SYNC_CHECK if sync_check else 0)
+        h = C.c_void_p()
+        rc = lib().mixrt_create(C.byref(h), C.byref(ci))
+        if rc != MIXRT_OK:
+            raise MixrtError(rc, lib().mixrt_thread_error().decode())
+        self._h = h
+
+    def _check(self, rc: int):
+        if rc != MIXRT_OK:
+            raise MixrtError(rc, lib().mixrt_last_error(self._h).decode())
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().mixrt_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def sync(self):
+        self._check(lib().mixrt_sync(self._h))
+
+    # -- the hot path
+    def render(self, ds: DeviceScene, out=None):
+        import torch
+        if out is None:
+            out = torch.empty((ds.rays, 4), dtype=torch.float32, device=ds.g0.device)
+        self._check(lib().mixrt_render(self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
+                                       C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp),
+                                       _ptr(out)))
+        return out
+
+    # -- stage entry points
+    def ray_setup(self, ds: DeviceScene):
+        import torch
+        K = ds.smp.K
+        x = torch.empty((ds.rays, K, 3), dtype=torch.float32, device=ds.g0.device)
+        hit = torch.empty((ds.rays,), dtype=torch.int32, device=ds.g0.device)
+        self._check(lib().mixrt_debug_ray_setup(self._h, C.byref(ds.gbuf), ds.cams,
+                                                C.byref(ds.disp), C.byref(ds.smp), _ptr(x),
+                                                _ptr(hit)))
+        return x, hit
+
+    def hash_encode(self, grid: HashGrid, x, want=("corner", "idx", "w", "feat")):
+        import torch
+        n = x.shape[0]
+        L, F = grid.L, grid.F
+        dev = x.device
+        out = {
+            "corner": torch.empty((n, L, 3), dtype=torch.int32, device=dev) if "corner" in want else None,
+            "idx": torch.empty((n, L, 8), dtype=torch.int32, device=dev) if "idx" in want else None,
+            "w": torch.empty((n, L, 8), dtype=torch.float32, device=dev) if "w" in want else None,
+            "feat": torch.empty((n, L * F), dtype=torch.float32, device=dev) if "feat" in want else None,
+        }
+        self._check(lib().mixrt_debug_hash_encode(
+            self._h, C.byref(grid), _ptr(x), n, _ptr(out["corner"]), _ptr(out["idx"]),
+            _ptr(out["w"]), _ptr(out["feat"])))
+        return out
+
+    def mlp(self, mlp: Mlp, x_f16):
+        import torch
+        n = x_f16.shape[0]
+        out = torch.empty((n, 4), dtype=torch.float32, device=x_f16.device)
+        self._check(lib().mixrt_debug_mlp(self._h, C.byref(mlp), _ptr(x_f16), n, _ptr(out)))
+        return out
+
+    def composite(self, srgb, smp: Sampling, bg):
+        import torch
+        rays = srgb.shape[0]
+        out = torch.empty((rays, 4), dtype=torch.float32, device=srgb.device)
+        bgc = (C.c_float * 3)(*[float(b) for b in bg])
+        self._check(lib().mixrt_debug_composite(self._h, _ptr(srgb), rays, C.byref(smp), bgc,
+                                                _ptr(out)))
+        return out
+
+
+def validate(gbuf, cams, disp, grid, mlp, smp):
+    """Pure-host descriptor check: returns (status, message)."""
+    buf = C.create_string_buffer(512)
+    ref = lambda s: None if s is None else C.byref(s)
+    rc = lib().mixrt_validate(ref(gbuf), cams, ref(disp), ref(grid), ref(mlp), ref(smp), buf, 512)
+    return rc, buf.value.decode()
+
+
+def level_resolutions(grid: HashGrid) -> np.ndarray:
+    out = np.zeros(grid.L, np.int32)
+    rc = lib().mixrt_level_resolutions(C.byref(grid), out.ctypes.data)
+    if rc != MIXRT_OK:
+        raise MixrtError(rc, lib().mixrt_thread_error().decode())
+    return out

@@ -1,0 +1,171 @@
+"""Host-only checks of the C ABI: the library loads without a GPU, exports
+every symbol the header declares, the binding's structs have the header's
+layout, and mixrt_validate (pure host code) rejects every bad descriptor."""
+import ctypes as C
+import os
+import re
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2312_11841_amd import mixrt, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mixrt.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mixrt_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    declared = _declared_functions()
+    assert set(declared) == set(mixrt.EXPORTS)
+    L = mixrt.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", mixrt.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (mixrt_\w+)", out))
+    assert set(declared) <= exported
+
+
+def test_struct_layout_matches_header():
+    structs = {"mixrt_create_info": mixrt.CreateInfo, "mixrt_gbuffer": mixrt.GBuffer,
+               "mixrt_camera": mixrt.Camera, "mixrt_disp_tex": mixrt.DispTex,
+               "mixrt_hash_grid": mixrt.HashGrid, "mixrt_mlp": mixrt.Mlp,
+               "mixrt_sampling": mixrt.Sampling}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "mixrt.h"', "int main(void){"]
+    for cname, py in structs.items():
+        lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
+        for fname, _ in py._fields_:
+            lines.append(f'printf("{cname} {fname} %zu\\n", offsetof({cname}, {fname}));')
+    lines.append("return 0;}")
+    with tempfile.TemporaryDirectory() as d:
+        src, exe = os.path.join(d, "l.c"), os.path.join(d, "l")
+        open(src, "w").write("\n".join(lines))
+        subprocess.run(["gcc", "-I", os.path.dirname(HEADER), src, "-o", exe], check=True)
+        rows = subprocess.run([exe], capture_output=True, text=True, check=True).stdout.split("\n")
+    got = {}
+    for r in rows:
+        if r:
+            a, b, c = r.split()
+            got[(a, b)] = int(c)
+    for cname, py in structs.items():
+        assert got[(cname, "size")] == C.sizeof(py), cname
+        for fname, _ in py._fields_:
+            assert got[(cname, fname)] == getattr(py, fname).offset, (cname, fname)
+
+
+def test_status_strings():
+    assert mixrt.status_string(0) == "ok"
+    for s in (-1, -2, -3, -4):
+        assert mixrt.status_string(s) not in ("ok", "unknown status")
+    assert mixrt.status_string(-99) == "unknown status"
+
+
+# --- validation -----------------------------------------------------------------
+
+FAKE = 0x10000  # an aligned address: validate never dereferences device pointers
+
+
+class _Desc:
+    def __init__(self, cfg=synth.VIEW720P):
+        self.cfg = cfg
+        self.gbuf = mixrt.GBuffer(cfg.views, cfg.W, cfg.H, FAKE, 0)
+        cams = np.zeros((cfg.views, 16), np.float32)
+        cams[:, [0, 5, 10]] = 1.0
+        cams[:, 12] = 60.0
+        self.cams = mixrt.make_cameras(cams)
+        self.disp = mixrt.DispTex(cfg.tex_R, cfg.tex_V, synth.dtype_code(cfg.tex_dtype),
+                                  0, FAKE)
+        self.grid = mixrt.HashGrid(cfg.L, cfg.log2_T, cfg.F, cfg.N_min, cfg.N_max,
+                                   synth.dtype_code(cfg.table_dtype), FAKE)
+        self.mlp = mixrt.Mlp()
+        self.mlp.n_layers = len(cfg.widths) - 1
+        for i, w in enumerate(cfg.widths):
+            self.mlp.width[i] = w
+        self.mlp.view_sh_dim = cfg.view_sh_dim
+        self.mlp.data = FAKE
+        self.smp = mixrt.Sampling(cfg.K, cfg.delta, cfg.t_term)
+
+    def validate(self):
+        return mixrt.validate(self.gbuf, self.cams, self.disp, self.grid, self.mlp, self.smp)
+
+
+@pytest.mark.parametrize("cfg", list(synth.CONFIGS.values()), ids=lambda c: c.name)
+def test_validate_accepts_every_workload(cfg):
+    rc, msg = _Desc(cfg).validate()
+    assert rc == mixrt.MIXRT_OK, msg
+
+
+BAD = [
+    ("gbuf.views", lambda d: setattr(d.gbuf, "views", 0), mixrt.MIXRT_EINVAL),
+    ("gbuf.views max", lambda d: setattr(d.gbuf, "views", 17), mixrt.MIXRT_EINVAL),
+    ("gbuf.W", lambda d: setattr(d.gbuf, "W", 0), mixrt.MIXRT_EINVAL),
+    ("gbuf.huge", lambda d: (setattr(d.gbuf, "W", 65536), setattr(d.gbuf, "H", 65536)),
+     mixrt.MIXRT_EUNSUPPORTED),
+    ("gbuf.g0 null", lambda d: setattr(d.gbuf, "g0", 0), mixrt.MIXRT_EINVAL),
+    ("gbuf.g0 misaligned", lambda d: setattr(d.gbuf, "g0", FAKE + 4), mixrt.MIXRT_EINVAL),
+    ("fov", lambda d: setattr(d.cams[0], "fov_y_deg", 180.0), mixrt.MIXRT_EINVAL),
+    ("c2w nan", lambda d: d.cams[0].c2w.__setitem__(3, float("nan")), mixrt.MIXRT_EINVAL),
+    ("disp.V", lambda d: setattr(d.disp, "V", 17), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.R", lambda d: setattr(d.disp, "R", 0), mixrt.MIXRT_EINVAL),
+    ("disp.dtype", lambda d: setattr(d.disp, "dtype", 2), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.mode", lambda d: setattr(d.disp, "mode", 1), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.data", lambda d: setattr(d.disp, "data", 0), mixrt.MIXRT_EINVAL),
+    ("grid.L", lambda d: setattr(d.grid, "L", 33), mixrt.MIXRT_EUNSUPPORTED),
+    ("grid.log2_T", lambda d: setattr(d.grid, "log2_T", 29), mixrt.MIXRT_EUNSUPPORTED),
+    ("grid.F", lambda d: setattr(d.grid, "F", 3), mixrt.MIXRT_EUNSUPPORTED),
+    ("grid.N", lambda d: setattr(d.grid, "N_max", 8), mixrt.MIXRT_EINVAL),
+    ("grid.dtype", lambda d: setattr(d.grid, "dtype", 2), mixrt.MIXRT_EUNSUPPORTED),
+    ("grid.data", lambda d: setattr(d.grid, "data", 0), mixrt.MIXRT_EINVAL),
+    ("mlp.in", lambda d: d.mlp.width.__setitem__(0, 64), mixrt.MIXRT_EINVAL),
+    ("mlp.out", lambda d: d.mlp.width.__setitem__(3, 3), mixrt.MIXRT_EINVAL),
+    ("mlp.hidden", lambda d: (d.mlp.width.__setitem__(1, 48), d.mlp.width.__setitem__(2, 48)),
+     mixrt.MIXRT_EUNSUPPORTED),
+    ("mlp.uneven", lambda d: d.mlp.width.__setitem__(2, 32), mixrt.MIXRT_EUNSUPPORTED),
+    ("mlp.view", lambda d: setattr(d.mlp, "view_sh_dim", 9), mixrt.MIXRT_EUNSUPPORTED),
+    ("mlp.layers", lambda d: setattr(d.mlp, "n_layers", 1), mixrt.MIXRT_EUNSUPPORTED),
+    ("mlp.data", lambda d: setattr(d.mlp, "data", 0), mixrt.MIXRT_EINVAL),
+    ("K=0", lambda d: setattr(d.smp, "K", 0), mixrt.MIXRT_EUNSUPPORTED),
+    ("K=65", lambda d: setattr(d.smp, "K", 65), mixrt.MIXRT_EUNSUPPORTED),
+    ("delta", lambda d: setattr(d.smp, "delta", -1.0), mixrt.MIXRT_EINVAL),
+    ("t_term", lambda d: setattr(d.smp, "t_term", 1.0), mixrt.MIXRT_EINVAL),
+    ("unbuilt variant", lambda d: setattr(d.disp, "dtype", 0), mixrt.MIXRT_EUNSUPPORTED),
+]
+
+
+@pytest.mark.parametrize("name,mutate,code", BAD, ids=[b[0] for b in BAD])
+def test_validate_rejects(name, mutate, code):
+    d = _Desc()
+    mutate(d)
+    rc, msg = d.validate()
+    assert rc == code, (rc, msg)
+    assert msg
+
+
+def test_validate_null_descriptors():
+    d = _Desc()
+    for field in ("gbuf", "disp", "grid", "mlp", "smp"):
+        args = dict(gbuf=d.gbuf, cams=d.cams, disp=d.disp, grid=d.grid, mlp=d.mlp, smp=d.smp)
+        args[field] = None
+        rc, msg = mixrt.validate(**args)
+        assert rc == mixrt.MIXRT_EINVAL and "NULL" in msg
+
+
+@pytest.mark.parametrize("L,nmin,nmax", [(8, 16, 256), (16, 16, 4096), (16, 16, 8192),
+                                         (4, 256, 4096), (1, 32, 32), (32, 2, 1 << 20)])
+def test_library_level_table_equals_oracle(L, nmin, nmax):
+    g = mixrt.HashGrid(L, 19, 2, nmin, nmax, 1, FAKE)
+    assert np.array_equal(mixrt.level_resolutions(g), oracle.level_resolutions(L, nmin, nmax))
+
+
+def test_level_table_rejects_bad_grid():
+    with pytest.raises(mixrt.MixrtError):
+        mixrt.level_resolutions(mixrt.HashGrid(0, 19, 2, 16, 256, 1, FAKE))

@@ -1,0 +1,324 @@
+"""GPU parity: every entry point of the C ABI against the CPU oracle on the same
+seeded inputs.
+
+Bars (see the tolerance derivations next to each check):
+  - voxel corners, table indices, hit flags: bit-exact;
+  - trilinear weights: 1e-6 absolute; features: 1e-5 x max|table|;
+  - sample positions: 2e-5 absolute (fp32 ray arithmetic vs double);
+  - MLP: a first-order bound on fp16 rounding of the hidden activations;
+  - frames: max |gpu - oracle| <= 2e-3 on rgb and alpha.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2312_11841_amd import mixrt, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+FRAME_TOL = 2e-3
+
+
+@pytest.fixture(scope="module")
+def R():
+    r = mixrt.Renderer(0, sync_check=True)
+    yield r
+    r.close()
+
+
+_scenes = {}
+
+
+def scene_of(cfg):
+    if cfg.name not in _scenes:
+        _scenes.clear() if len(_scenes) > 3 else None
+        sc = synth.make_scene(cfg)
+        _scenes[cfg.name] = (sc, mixrt.DeviceScene.from_scene(sc, "cuda:0"))
+    return _scenes[cfg.name]
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+# --------------------------------------------------------------------------
+# Hash encoding: corners and indices bit-exact (identical fp32 inputs)
+# --------------------------------------------------------------------------
+
+def _adversarial_x(N_levels, rng, n_rand):
+    xs = [rng.uniform(0, 1, (n_rand, 3)).astype(np.float32)]
+    edge = [0.0, 1.0, np.nextafter(np.float32(1), np.float32(0)), np.float32(1e-30)]
+    for n in N_levels:
+        n = int(n)
+        for k in (0, 1, n // 3, n // 2, n - 1, n):
+            v = np.float32(k) / np.float32(n)
+            edge += [v, np.nextafter(v, np.float32(0)), np.nextafter(v, np.float32(2))]
+    e = np.clip(np.array(edge, np.float32), 0, 1)
+    xs.append(np.stack([e, np.roll(e, 1), np.roll(e, 2)], 1))
+    return np.concatenate(xs)
+
+
+GRID_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.BATCH8X1080P,
+             synth.DEPLOYED720P]
+
+
+@pytest.mark.parametrize("cfg", GRID_CFGS, ids=lambda c: c.name)
+def test_hash_encode_bit_exact(R, cfg):
+    say("hash_encode", cfg.name)
+    rng = np.random.default_rng(100 + cfg.seed)
+    table = synth.make_scene(cfg.replace(H=8, W=8, rows=0, views=1)).table \
+        if cfg.views > 1 else scene_of(cfg)[0].table
+    N = oracle.level_resolutions(cfg.L, cfg.N_min, cfg.N_max)
+    x = _adversarial_x(N, rng, 5000 + 37)          # several blocks and a ragged tail
+    tt = torch.from_numpy(table).cuda()
+    grid = mixrt.make_grid(tt, cfg.N_min, cfg.N_max)
+    got = R.hash_encode(grid, torch.from_numpy(x).cuda())
+    R.sync()
+    corner, idx, w, feat = oracle.hash_encode(x, table, cfg.N_min, cfg.N_max)
+    assert np.array_equal(got["corner"].cpu().numpy(), corner)
+    assert np.array_equal(got["idx"].cpu().numpy().view(np.uint32), idx)
+    # fp32 products of three factors in [0,1] vs double: a few ulps
+    assert np.abs(got["w"].cpu().numpy() - w).max() <= 1e-6
+    # fp32 sum of 8 weighted entries: <= ~16 ulps of max|table|
+    scale = max(1.0, float(np.abs(table.astype(np.float32)).max()))
+    assert np.abs(got["feat"].cpu().numpy() - feat).max() <= 1e-5 * scale
+
+
+def test_hash_encode_empty_and_single(R):
+    cfg = synth.TINY64
+    tt = torch.from_numpy(scene_of(cfg)[0].table).cuda()
+    grid = mixrt.make_grid(tt, cfg.N_min, cfg.N_max)
+    got = R.hash_encode(grid, torch.zeros((0, 3), device="cuda"))
+    assert got["feat"].shape == (0, cfg.L * cfg.F)
+    x = np.array([[1.0, 1.0, 1.0]], np.float32)
+    got = R.hash_encode(grid, torch.from_numpy(x).cuda())
+    _, idx, _, feat = oracle.hash_encode(x, scene_of(cfg)[0].table, cfg.N_min, cfg.N_max)
+    assert np.array_equal(got["idx"].cpu().numpy().view(np.uint32), idx)
+
+
+# --------------------------------------------------------------------------
+# Ray setup: positions fed to the grid; their indices must equal the oracle's
+# --------------------------------------------------------------------------
+
+RAY_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.DEPLOYED720P]
+
+
+@pytest.mark.parametrize("cfg", RAY_CFGS, ids=lambda c: c.name)
+def test_ray_setup_and_indices_from_gpu_positions(R, cfg):
+    say("ray_setup", cfg.name)
+    sc, ds = scene_of(cfg)
+    x, hit = R.ray_setup(ds)
+    R.sync()
+    rng = np.random.default_rng(7)
+    pix = np.unique(np.concatenate([rng.choice(cfg.rays, min(cfg.rays, 3000), replace=False),
+                                    [0, cfg.rays - 1], np.arange(min(cfg.W, cfg.rays))]))
+    xo, xd, hito = oracle.OracleScene(sc).pixel_samples(pix)
+    xg = x.cpu().numpy()[pix]
+    assert np.array_equal(hit.cpu().numpy()[pix], hito)
+    # fp32 ray arithmetic (|q| <= ~25) against double: positions agree to a
+    # few ulps of the world coordinates, divided by 4 by the cube map
+    assert np.abs(xg - xd).max() <= 2e-5
+    # the grid decision itself: the oracle's encoding of the GPU's positions
+    flat = xg.reshape(-1, 3)
+    tt = ds.table
+    grid = ds.grid
+    got = R.hash_encode(grid, torch.from_numpy(flat).cuda(), want=("corner", "idx"))
+    R.sync()
+    corner, idx, _, _ = oracle.hash_encode(flat, sc.table, cfg.N_min, cfg.N_max)
+    assert np.array_equal(got["corner"].cpu().numpy(), corner)
+    assert np.array_equal(got["idx"].cpu().numpy().view(np.uint32), idx)
+    del tt
+
+
+# --------------------------------------------------------------------------
+# MLP on MFMA
+# --------------------------------------------------------------------------
+
+def _mlp_bound(x, weights):
+    """First-order bound of the GPU's error on the head outputs: every hidden
+    activation is rounded to fp16 (relative 2^-11) before the next layer;
+    fp32 accumulation adds far less.  Returns per-sample bounds on o."""
+    eps = 2.0 ** -11
+    z = x
+    err = np.zeros_like(x)
+    for m, w in enumerate(weights):
+        wa = np.abs(w.astype(np.float64))
+        zn = z @ w.astype(np.float64)
+        err = err @ wa
+        if m < len(weights) - 1:
+            zn = np.maximum(zn, 0)
+            err = err + np.abs(zn) * eps
+        z = zn
+    return 2.0 * err + 1e-6
+
+
+MLP_SHAPES = [(16, 32, 1), (32, 32, 1), (48, 64, 2), (32, 64, 2), (16, 64, 2)]
+
+
+@pytest.mark.parametrize("shape", MLP_SHAPES, ids=lambda s: f"{s[0]}-{s[1]}x{s[2]}")
+@pytest.mark.parametrize("n", [1, 63, 64, 1000 + 17])
+def test_mlp_parity(R, shape, n):
+    say("mlp", shape, n)
+    IN, HID, NH = shape
+    widths = [IN] + [HID] * NH + [4]
+    rng = np.random.default_rng(IN * 100 + HID + n)
+    ws = [rng.normal(0, 0.2, (widths[m], widths[m + 1])).astype(np.float16)
+          for m in range(len(widths) - 1)]
+    x = rng.uniform(-1, 1, (n, IN)).astype(np.float16)
+    flat = np.concatenate([w.reshape(-1) for w in ws])
+    wt = torch.from_numpy(flat.view(np.int16).copy()).cuda()
+    m = mixrt.make_mlp(wt, widths, 0)
+    got = R.mlp(m, torch.from_numpy(x.view(np.int16).copy()).cuda()).cpu().numpy()
+    R.sync()
+    ref = oracle.mlp(x.astype(np.float64), ws)
+    b = _mlp_bound(x.astype(np.float64), ws)
+    # sigma = exp(o0): relative error ~ |d o0|; rgb = sigmoid: slope <= 1/4
+    assert np.all(np.abs(got[:, 0] / ref[:, 0] - 1) <= b[:, 0] * 1.01 + 1e-6)
+    assert np.all(np.abs(got[:, 1:] - ref[:, 1:]) <= 0.25 * b[:, 1:] + 1e-6)
+
+
+# --------------------------------------------------------------------------
+# Compositing
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("K", [1, 3, 8, 64])
+def test_composite_parity(R, K):
+    say("composite", K)
+    rng = np.random.default_rng(K)
+    rays = 1000 + 13
+    s = rng.uniform(0, 1, (rays, K, 4)).astype(np.float32)
+    s[..., 0] = rng.exponential(2.0, (rays, K))
+    s[:10, :, 0] = 0.0                      # transparent rays
+    s[10:20, 0, 0] = 1e30                   # opaque first sample
+    bg = [0.25, 0.5, 0.75]
+    for t_term in (0.0, 1e-4):
+        smp = mixrt.make_sampling(K, 0.3, t_term)
+        got = R.composite(torch.from_numpy(s).cuda(), smp, bg).cpu().numpy()
+        ref = oracle.composite(s.astype(np.float64), 0.3, bg)
+        # fp32 exp and products over K <= 64 samples; early termination moves
+        # the result by at most t_term
+        assert np.abs(got - ref).max() <= 1e-5 + t_term
+    assert np.array_equal(got[:10], np.tile([0.25, 0.5, 0.75, 0.0], (10, 1)).astype(np.float32))
+    assert np.allclose(got[10:20, :3], s[10:20, 0, 1:], atol=1e-6)
+
+
+# --------------------------------------------------------------------------
+# Whole frames through mixrt_render
+# --------------------------------------------------------------------------
+
+def _frame_pixels(cfg, rng, n):
+    if cfg.rays <= 20000:
+        return np.arange(cfg.rays)
+    pix = rng.choice(cfg.rays, n, replace=False)
+    first_row = np.arange(cfg.W)
+    return np.unique(np.concatenate([pix, first_row, [cfg.rays - 1]]))
+
+
+FRAME_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.VIEW720P_DENSE,
+              synth.DEPLOYED720P]
+
+
+@pytest.mark.parametrize("cfg", FRAME_CFGS, ids=lambda c: c.name)
+def test_frame_parity(R, cfg):
+    say("frame", cfg.name, cfg.rays)
+    sc, ds = scene_of(cfg)
+    out = R.render(ds)
+    R.sync()
+    got = out.cpu().numpy()
+    pix = _frame_pixels(cfg, np.random.default_rng(3), 3000)
+    ref = oracle.OracleScene(sc).render_pixels(pix, threads=oracle.max_threads())
+    err = np.abs(got[pix] - ref).max()
+    say(f"  max |gpu - oracle| = {err:.3e} over {pix.size} px")
+    assert err <= FRAME_TOL
+    assert np.all(np.isfinite(got))
+
+
+def test_frame_is_deterministic(R):
+    sc, ds = scene_of(synth.VIEW720P_DENSE)
+    a = R.render(ds).clone()
+    b = R.render(ds)
+    R.sync()
+    assert torch.equal(a, b)
+
+
+def test_large_batch_one_view_sampled(R):
+    cfg = synth.BATCH8X1080P
+    say("frame", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    out = R.render(ds)
+    R.sync()
+    got = out.cpu().numpy()
+    rng = np.random.default_rng(5)
+    view = 5
+    hw = cfg.H * cfg.W
+    pix = view * hw + rng.choice(hw, 1500, replace=False)
+    pix = np.concatenate([pix, [0, cfg.rays - 1, hw - 1, hw]])   # view boundaries
+    ref = oracle.OracleScene(sc).render_pixels(pix, threads=oracle.max_threads())
+    err = np.abs(got[pix] - ref).max()
+    say(f"  max |gpu - oracle| = {err:.3e}")
+    assert err <= FRAME_TOL
+    del ds
+
+
+@pytest.mark.parametrize("K", [1, 2, 4, 8, 16, 32])
+def test_sweep_rays_by_samples(R, K):
+    cfg = synth.sweep_config(1 << 16, K, dense=True)
+    say("sweep", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got = R.render(ds).cpu().numpy()
+    pix = _frame_pixels(cfg, np.random.default_rng(K), 1200)
+    ref = oracle.OracleScene(sc).render_pixels(pix, threads=oracle.max_threads())
+    assert np.abs(got[pix] - ref).max() <= FRAME_TOL
+
+
+# --------------------------------------------------------------------------
+# Edge cases of the frame path
+# --------------------------------------------------------------------------
+
+@pytest.mark.parametrize("H,W,K,views", [(1, 1, 8, 1), (23, 37, 3, 1), (17, 5, 64, 1),
+                                         (9, 11, 5, 3), (33, 31, 1, 2), (8, 8, 7, 16)])
+def test_ragged_shapes(R, H, W, K, views):
+    cfg = synth.TINY64_DENSE.replace(name=f"rag{H}x{W}k{K}v{views}", H=H, W=W, K=K,
+                                     views=views, gbuf="iid")
+    say("ragged", cfg.name)
+    sc = synth.make_scene(cfg)
+    if views > 1:   # distinct cameras and backgrounds per view
+        for v in range(views):
+            sc.cams[v, 3] = 0.1 * v
+            sc.cams[v, 13:16] = [0.1 * v, 0.5, 1.0 - 0.05 * v]
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got = R.render(ds).cpu().numpy()
+    ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays))
+    assert np.abs(got - ref).max() <= FRAME_TOL
+
+
+def test_miss_pixels_are_background(R):
+    cfg = synth.TINY64_DENSE
+    sc = synth.make_scene(cfg)
+    sc.g0[0, 0, :5, 0] = [0.0, -1.0, np.nan, np.inf, -np.inf]
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got = R.render(ds).cpu().numpy()
+    bg = np.array(list(cfg.bg) + [0.0], np.float32)
+    assert np.array_equal(got[:5], np.tile(bg, (5, 1)))
+    ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays))
+    assert np.abs(got - ref).max() <= FRAME_TOL
+
+
+def test_render_rejects_bad_calls(R):
+    sc, ds = scene_of(synth.TINY64)
+    bad = mixrt.make_sampling(65, 0.01, 1e-4)
+    saved = ds.smp
+    ds.smp = bad
+    with pytest.raises(mixrt.MixrtError) as e:
+        R.render(ds)
+    assert e.value.status == mixrt.MIXRT_EUNSUPPORTED
+    ds.smp = saved
+    with pytest.raises(mixrt.MixrtError):
+        import ctypes as C
+        mixrt.lib()  # the binding passes a NULL output through to the library
+        rc = mixrt.lib().mixrt_render(R._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
+                                      C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp), None)
+        R._check(rc)
