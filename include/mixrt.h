@@ -114,7 +114,7 @@ typedef struct {
  * the spatial hash (v0 * 1 ^ v1 * 2654435761 ^ v2 * 805459861) mod T. */
 typedef struct {
     int32_t L;           /* levels, 1..32 */
-    int32_t log2_T;      /* T = 2^log2_T entries per level, 4..28 */
+    int32_t log2_T;      /* T = 2^log2_T entries per level, 4..26 */
     int32_t F;           /* features per entry: 2 or 4 */
     int32_t N_min, N_max;/* 1 <= N_min <= N_max <= 2^20 */
     int32_t dtype;       /* MIXRT_F32 or MIXRT_F16 */

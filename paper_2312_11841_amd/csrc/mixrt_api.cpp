@@ -122,8 +122,8 @@ int check_grid(const mixrt_hash_grid *g, Msg m)
     if (!g) return vfail(m, MIXRT_EINVAL, "grid is NULL");
     if (g->L < 1 || g->L > MIXRT_MAX_LEVELS)
         return vfail(m, MIXRT_EUNSUPPORTED, "grid.L=%d outside 1..%d", g->L, MIXRT_MAX_LEVELS);
-    if (g->log2_T < 4 || g->log2_T > 28)
-        return vfail(m, MIXRT_EUNSUPPORTED, "grid.log2_T=%d outside 4..28", g->log2_T);
+    if (g->log2_T < 4 || g->log2_T > 26)
+        return vfail(m, MIXRT_EUNSUPPORTED, "grid.log2_T=%d outside 4..26", g->log2_T);
     if (g->F != 2 && g->F != 4) return vfail(m, MIXRT_EUNSUPPORTED, "grid.F=%d (2 or 4)", g->F);
     if (g->N_min < 1 || g->N_max < g->N_min || g->N_max > (1 << 20))
         return vfail(m, MIXRT_EINVAL, "grid N_min=%d N_max=%d", g->N_min, g->N_max);
@@ -238,7 +238,10 @@ void fill_grid_params(mixrt::GridParams &gp, const mixrt_hash_grid *g)
     for (int l = 0; l < g->L; ++l) {
         gp.N[l] = (uint32_t)N[l];
         const uint64_t side = (uint64_t)N[l] + 1;
-        if (side * side * side <= T) gp.dense_mask |= 1u << l;
+        if (side * side * side <= T) {
+            gp.dense_mask |= 1u << l;
+            gp.n_dense = l + 1;  // resolutions increase, so dense levels are a prefix
+        }
     }
 }
 

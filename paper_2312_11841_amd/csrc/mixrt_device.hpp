@@ -14,6 +14,14 @@ typedef _Float16 h2 __attribute__((ext_vector_type(2)));
 typedef _Float16 h4 __attribute__((ext_vector_type(4)));
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
+// Under-aligned integers for loads of two neighbouring table entries, split
+// into 32-bit words with shifts.  (An under-aligned ext_vector_type typedef
+// had its second element read back as the first by this compiler, and
+// structs get split into single-dword loads.)
+typedef uint64_t u64a4 __attribute__((aligned(4)));
+typedef unsigned __int128 u128a8 __attribute__((aligned(8)));
+
+__device__ __forceinline__ h2 word_h2(uint32_t w) { return __builtin_bit_cast(h2, w); }
 
 constexpr int kMaxViews = 16;
 constexpr int kMaxLevels = 32;
@@ -45,6 +53,7 @@ struct GridParams {
     uint32_t log2_T;
     int32_t L;
     uint32_t dense_mask;    // bit l: level l indexes its vertices densely
+    int32_t n_dense;        // dense levels form the prefix 0..n_dense-1
     uint32_t N[kMaxLevels];
 };
 
@@ -220,15 +229,17 @@ __device__ __forceinline__ bool sample_position(const RayParams &p, const Ray &r
 // The voxel is chosen from the fp32 product x * N_l (one rounding, no
 // contraction into an FMA) so corners and indices are reproducible.
 // --------------------------------------------------------------------------
+// Table reads use a uniform (scalar) level base plus a 32-bit byte offset,
+// which maps onto the scalar-base + vector-offset form of global loads.
 template <int F, bool F16>
 struct TableEntry;
 
 template <>
 struct TableEntry<2, true> {
-    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    static constexpr uint32_t kBytes = 4;
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
     {
-        const uint32_t raw = ((const uint32_t *)t)[idx];
-        const h2 h = __builtin_bit_cast(h2, raw);
+        const h2 h = __builtin_bit_cast(h2, *(const uint32_t *)(t + off));
         v[0] = (float)h.x;
         v[1] = (float)h.y;
     }
@@ -236,9 +247,10 @@ struct TableEntry<2, true> {
 
 template <>
 struct TableEntry<2, false> {
-    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    static constexpr uint32_t kBytes = 8;
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
     {
-        const float2 f = ((const float2 *)t)[idx];
+        const float2 f = *(const float2 *)(t + off);
         v[0] = f.x;
         v[1] = f.y;
     }
@@ -246,9 +258,10 @@ struct TableEntry<2, false> {
 
 template <>
 struct TableEntry<4, true> {
-    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    static constexpr uint32_t kBytes = 8;
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
     {
-        const uint2 raw = ((const uint2 *)t)[idx];
+        const uint2 raw = *(const uint2 *)(t + off);
         const h2 a = __builtin_bit_cast(h2, raw.x), b = __builtin_bit_cast(h2, raw.y);
         v[0] = (float)a.x;
         v[1] = (float)a.y;
@@ -259,9 +272,10 @@ struct TableEntry<4, true> {
 
 template <>
 struct TableEntry<4, false> {
-    static __device__ __forceinline__ void load(const void *t, uint32_t idx, float *v)
+    static constexpr uint32_t kBytes = 16;
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
     {
-        const float4 f = ((const float4 *)t)[idx];
+        const float4 f = *(const float4 *)(t + off);
         v[0] = f.x;
         v[1] = f.y;
         v[2] = f.z;
@@ -269,65 +283,142 @@ struct TableEntry<4, false> {
     }
 };
 
+// Two neighbouring entries (idx, idx + 1) in one load: along x, the dense
+// index of corner (c0 + 1) is the dense index of c0 plus one.  Entries are
+// at least 4-byte aligned, which multi-dword global loads accept.
+template <int F, bool F16>
+struct TablePair;
+
+template <>
+struct TablePair<2, true> {
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v0, float *v1)
+    {
+        const uint64_t raw = *(const u64a4 *)(t + off);
+        const h2 a = word_h2((uint32_t)raw), b = word_h2((uint32_t)(raw >> 32));
+        v0[0] = (float)a.x;
+        v0[1] = (float)a.y;
+        v1[0] = (float)b.x;
+        v1[1] = (float)b.y;
+    }
+};
+
+template <>
+struct TablePair<2, false> {
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v0, float *v1)
+    {
+        const unsigned __int128 raw = *(const u128a8 *)(t + off);
+        v0[0] = __builtin_bit_cast(float, (uint32_t)raw);
+        v0[1] = __builtin_bit_cast(float, (uint32_t)(raw >> 32));
+        v1[0] = __builtin_bit_cast(float, (uint32_t)(raw >> 64));
+        v1[1] = __builtin_bit_cast(float, (uint32_t)(raw >> 96));
+    }
+};
+
+template <>
+struct TablePair<4, true> {
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v0, float *v1)
+    {
+        const unsigned __int128 raw = *(const u128a8 *)(t + off);
+        const h2 a = word_h2((uint32_t)raw), b = word_h2((uint32_t)(raw >> 32));
+        const h2 c = word_h2((uint32_t)(raw >> 64)), d = word_h2((uint32_t)(raw >> 96));
+        v0[0] = (float)a.x;
+        v0[1] = (float)a.y;
+        v0[2] = (float)b.x;
+        v0[3] = (float)b.y;
+        v1[0] = (float)c.x;
+        v1[1] = (float)c.y;
+        v1[2] = (float)d.x;
+        v1[3] = (float)d.y;
+    }
+};
+
+template <>
+struct TablePair<4, false> {
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v0, float *v1)
+    {
+        TableEntry<4, false>::load(t, off, v0);
+        TableEntry<4, false>::load(t, off + 16u, v1);
+    }
+};
+
 constexpr uint32_t kPrimeY = 2654435761u;
 constexpr uint32_t kPrimeZ = 805459861u;
 
-struct LevelDebug {
-    int32_t *corner;  // [3]
-    uint32_t *idx;    // [8]
-    float *w;         // [8]
+// Voxel, fractional position and the 8 corner indices of one query at one
+// level.  Corner b has offset (b & 1, b >> 1 & 1, b >> 2 & 1).
+struct LevelSetup {
+    int32_t c[3];
+    float fr[3];
+    uint32_t idx[8];
 };
 
-template <int F, bool F16, bool DEBUG>
-__device__ __forceinline__ void hash_level(const void *table_l, uint32_t N, bool dense,
-                                           uint32_t T_mask, float x0, float x1, float x2,
-                                           float *feat, LevelDebug dbg)
+__device__ __forceinline__ void level_setup(uint32_t N, bool dense, uint32_t T_mask, float x0,
+                                            float x1, float x2, LevelSetup &s)
 {
     const float Nf = (float)N;
-    const float p0 = __fmul_rn(x0, Nf), p1 = __fmul_rn(x1, Nf), p2 = __fmul_rn(x2, Nf);
+    const float p[3] = {__fmul_rn(x0, Nf), __fmul_rn(x1, Nf), __fmul_rn(x2, Nf)};
     const int32_t top = (int32_t)N - 1;
-    const int32_t c0 = min(max((int32_t)floorf(p0), 0), top);
-    const int32_t c1 = min(max((int32_t)floorf(p1), 0), top);
-    const int32_t c2 = min(max((int32_t)floorf(p2), 0), top);
-    const float f0 = p0 - (float)c0, f1 = p1 - (float)c1, f2 = p2 - (float)c2;
-    uint32_t idx[8];
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        s.c[a] = min(max((int32_t)floorf(p[a]), 0), top);
+        s.fr[a] = p[a] - (float)s.c[a];
+    }
     if (dense) {
         const uint32_t s1 = N + 1u, s2 = s1 * s1;
-        const uint32_t base = (uint32_t)c0 + (uint32_t)c1 * s1 + (uint32_t)c2 * s2;
+        const uint32_t base = (uint32_t)s.c[0] + (uint32_t)s.c[1] * s1 + (uint32_t)s.c[2] * s2;
 #pragma unroll
         for (int b = 0; b < 8; ++b)
-            idx[b] = base + (uint32_t)(b & 1) + ((b & 2) ? s1 : 0u) + ((b & 4) ? s2 : 0u);
+            s.idx[b] = base + (uint32_t)(b & 1) + ((b & 2) ? s1 : 0u) + ((b & 4) ? s2 : 0u);
     } else {
-        const uint32_t hy0 = (uint32_t)c1 * kPrimeY, hy1 = hy0 + kPrimeY;
-        const uint32_t hz0 = (uint32_t)c2 * kPrimeZ, hz1 = hz0 + kPrimeZ;
+        const uint32_t hy0 = (uint32_t)s.c[1] * kPrimeY, hy1 = hy0 + kPrimeY;
+        const uint32_t hz0 = (uint32_t)s.c[2] * kPrimeZ, hz1 = hz0 + kPrimeZ;
 #pragma unroll
         for (int b = 0; b < 8; ++b)
-            idx[b] = (((uint32_t)c0 + (uint32_t)(b & 1)) ^ ((b & 2) ? hy1 : hy0) ^
-                      ((b & 4) ? hz1 : hz0)) & T_mask;
+            s.idx[b] = (((uint32_t)s.c[0] + (uint32_t)(b & 1)) ^ ((b & 2) ? hy1 : hy0) ^
+                        ((b & 4) ? hz1 : hz0)) & T_mask;
     }
-    float v[8][F];
+}
+
+__device__ __forceinline__ float corner_weight(const LevelSetup &s, int b)
+{
+    const float w0 = (b & 1) ? s.fr[0] : 1.0f - s.fr[0];
+    const float w1 = (b & 2) ? s.fr[1] : 1.0f - s.fr[1];
+    const float w2 = (b & 4) ? s.fr[2] : 1.0f - s.fr[2];
+    return w0 * w1 * w2;
+}
+
+// The 8 corner entries of a level: 4 pair loads on a dense level, 8 single
+// loads on a hashed one.
+template <int F, bool F16, bool DENSE>
+__device__ __forceinline__ void level_fetch(const void *table_l, const LevelSetup &s,
+                                            float (*v)[F])
+{
+    const char *t = (const char *)table_l;
+    constexpr uint32_t eb = TableEntry<F, F16>::kBytes;
+    if (DENSE) {
 #pragma unroll
-    for (int b = 0; b < 8; ++b)
-        TableEntry<F, F16>::load(table_l, idx[b], v[b]);
-    const float g0[2] = {1.0f - f0, f0}, g1[2] = {1.0f - f1, f1}, g2[2] = {1.0f - f2, f2};
+        for (int q = 0; q < 4; ++q)
+            TablePair<F, F16>::load(t, s.idx[2 * q] * eb, v[2 * q], v[2 * q + 1]);
+    } else {
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            TableEntry<F, F16>::load(t, s.idx[b] * eb, v[b]);
+    }
+}
+
+template <int F>
+__device__ __forceinline__ void level_accumulate(const LevelSetup &s, const float (*v)[F],
+                                                 float *feat)
+{
 #pragma unroll
     for (int f = 0; f < F; ++f)
         feat[f] = 0.0f;
 #pragma unroll
     for (int b = 0; b < 8; ++b) {
-        const float w = g0[b & 1] * g1[(b >> 1) & 1] * g2[(b >> 2) & 1];
+        const float w = corner_weight(s, b);
 #pragma unroll
         for (int f = 0; f < F; ++f)
             feat[f] += w * v[b][f];
-        if (DEBUG) {
-            dbg.idx[b] = idx[b];
-            dbg.w[b] = w;
-        }
-    }
-    if (DEBUG) {
-        dbg.corner[0] = c0;
-        dbg.corner[1] = c1;
-        dbg.corner[2] = c2;
     }
 }
 
@@ -335,6 +426,26 @@ __device__ __forceinline__ const void *level_base(const GridParams &g, int l, in
 {
     const size_t esz = f16 ? 2 : 4;
     return (const char *)g.table + (size_t)l * ((size_t)g.T_mask + 1) * (size_t)F * esz;
+}
+
+// G consecutive levels starting at l0, all of one kind (dense or hashed):
+// every corner load of the group is issued before any interpolation, so a
+// wave keeps 4G (dense) or 8G (hashed) gathers in flight.
+template <int F, bool F16, int G, bool DENSE>
+__device__ __forceinline__ void hash_group(const GridParams &gp, int l0, float x0, float x1,
+                                           float x2, float (*feat)[F])
+{
+    LevelSetup s[G];
+    float v[G][8][F];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        level_setup(gp.N[l0 + g], DENSE, gp.T_mask, x0, x1, x2, s[g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        level_fetch<F, F16, DENSE>(level_base(gp, l0 + g, F, F16), s[g], v[g]);
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        level_accumulate<F>(s[g], v[g], feat[g]);
 }
 
 // --------------------------------------------------------------------------
@@ -409,36 +520,53 @@ struct Act {
     f4 acc[MT];
 };
 
+// ReLU of two fp32 activations, packed to fp16 (max commutes with rounding).
+__device__ __forceinline__ h2 relu_pack(float a, float b)
+{
+    const h2 v = {(_Float16)a, (_Float16)b};
+    const h2 z = {(_Float16)0.0f, (_Float16)0.0f};
+    return __builtin_elementwise_max(v, z);
+}
+
+template <int NC, int R16, typename AL>
+__device__ __forceinline__ f4 mfma_tile(const AL &A, int mt, const h8 *b32, h4 b16)
+{
+    const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+    f4 acc;
+    if (NC > 0)
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][0], b32[0], zero, 0, 0, 0);
+    else
+        acc = __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
+#pragma unroll
+    for (int ch = 1; ch < NC; ++ch)
+        acc += __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], zero, 0, 0, 0);
+    if (NC > 0 && R16)
+        acc += __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
+    return acc;
+}
+
 template <int KIN, int MOUT>
 __device__ __forceinline__ void layer_from_regs(const LayerA<KIN, MOUT, true> &A,
                                                 const Act<KIN> &in, Act<MOUT> &out)
 {
-    h8 b32[LayerA<KIN, MOUT, true>::NC > 0 ? LayerA<KIN, MOUT, true>::NC : 1];
-    h4 b16;
+    constexpr int NC = LayerA<KIN, MOUT, true>::NC, R16 = LayerA<KIN, MOUT, true>::R16;
+    h8 b32[NC > 0 ? NC : 1];
+    h4 b16 = {};
 #pragma unroll
-    for (int ch = 0; ch < LayerA<KIN, MOUT, true>::NC; ++ch) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            b32[ch][j] = (_Float16)fmaxf(in.acc[2 * ch][j], 0.0f);
-            b32[ch][j + 4] = (_Float16)fmaxf(in.acc[2 * ch + 1][j], 0.0f);
-        }
+    for (int ch = 0; ch < NC; ++ch) {
+        const f4 lo = in.acc[2 * ch], hi = in.acc[2 * ch + 1];
+        const h2 p0 = relu_pack(lo[0], lo[1]), p1 = relu_pack(lo[2], lo[3]);
+        const h2 p2 = relu_pack(hi[0], hi[1]), p3 = relu_pack(hi[2], hi[3]);
+        b32[ch] = h8{p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
     }
-    if (LayerA<KIN, MOUT, true>::R16) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            b16[j] = (_Float16)fmaxf(in.acc[0][j], 0.0f);
+    if (R16) {
+        const h2 p0 = relu_pack(in.acc[0][0], in.acc[0][1]);
+        const h2 p1 = relu_pack(in.acc[0][2], in.acc[0][3]);
+        b16 = h4{p0.x, p0.y, p1.x, p1.y};
     }
 #pragma unroll
-    for (int mt = 0; mt < Act<MOUT>::MT; ++mt) {
-        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-        f4 acc = zero;
-#pragma unroll
-        for (int ch = 0; ch < LayerA<KIN, MOUT, true>::NC; ++ch)
-            acc += __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], zero, 0, 0, 0);
-        if (LayerA<KIN, MOUT, true>::R16)
-            acc += __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
-        out.acc[mt] = acc;
-    }
+    for (int mt = 0; mt < Act<MOUT>::MT; ++mt)
+        out.acc[mt] = mfma_tile<NC, R16>(A, mt, b32, b16);
 }
 
 // First layer: B operand read from a [16][ld] fp16 tile (row = sample) in
@@ -448,26 +576,19 @@ __device__ __forceinline__ void layer_from_rows(const LayerA<KIN, MOUT, false> &
                                                 const _Float16 *rows, int ld, int lane,
                                                 Act<MOUT> &out)
 {
+    constexpr int NC = LayerA<KIN, MOUT, false>::NC, R16 = LayerA<KIN, MOUT, false>::R16;
     const int c = lane & 15, g = lane >> 4;
     const _Float16 *row = rows + c * ld;
-    h8 b32[LayerA<KIN, MOUT, false>::NC > 0 ? LayerA<KIN, MOUT, false>::NC : 1];
-    h4 b16;
+    h8 b32[NC > 0 ? NC : 1];
+    h4 b16 = {};
 #pragma unroll
-    for (int ch = 0; ch < LayerA<KIN, MOUT, false>::NC; ++ch)
+    for (int ch = 0; ch < NC; ++ch)
         b32[ch] = *(const h8 *)(row + ch * 32 + 8 * g);
-    if (LayerA<KIN, MOUT, false>::R16)
-        b16 = *(const h4 *)(row + LayerA<KIN, MOUT, false>::NC * 32 + 4 * g);
+    if (R16)
+        b16 = *(const h4 *)(row + NC * 32 + 4 * g);
 #pragma unroll
-    for (int mt = 0; mt < Act<MOUT>::MT; ++mt) {
-        const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-        f4 acc = zero;
-#pragma unroll
-        for (int ch = 0; ch < LayerA<KIN, MOUT, false>::NC; ++ch)
-            acc += __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], zero, 0, 0, 0);
-        if (LayerA<KIN, MOUT, false>::R16)
-            acc += __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
-        out.acc[mt] = acc;
-    }
+    for (int mt = 0; mt < Act<MOUT>::MT; ++mt)
+        out.acc[mt] = mfma_tile<NC, R16>(A, mt, b32, b16);
 }
 
 // The whole MLP: IN -> HID (ReLU) -> [HID -> HID (ReLU)] x (NHID-1) -> 4.
@@ -509,11 +630,17 @@ __device__ __forceinline__ f4 mlp_tile(const MlpWeights<IN, HID, NHID> &Wt,
     return o.acc[0];
 }
 
-// Output activations (Sec. 3.1): density exp(.), colour sigmoid(.).
+// Output activations (Sec. 3.1): density exp(.), colour sigmoid(.), with the
+// hardware exp2 and reciprocal (about 1 ulp).
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+__device__ __forceinline__ float fast_sigmoid(float x)
+{
+    return __builtin_amdgcn_rcpf(1.0f + fast_exp(-x));
+}
+
 __device__ __forceinline__ float4 mlp_activate(f4 o)
 {
-    return make_float4(expf(o[0]), 1.0f / (1.0f + expf(-o[1])), 1.0f / (1.0f + expf(-o[2])),
-                       1.0f / (1.0f + expf(-o[3])));
+    return make_float4(fast_exp(o[0]), fast_sigmoid(o[1]), fast_sigmoid(o[2]), fast_sigmoid(o[3]));
 }
 
 // --------------------------------------------------------------------------
@@ -526,7 +653,7 @@ struct Composite {
 
     __device__ __forceinline__ bool add(float4 s, float delta, float t_term)
     {
-        const float alpha = 1.0f - expf(-s.x * delta);
+        const float alpha = 1.0f - fast_exp(-s.x * delta);
         const float w = T * alpha;
         r += w * s.y;
         g += w * s.z;

@@ -29,6 +29,24 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
+// Levels per batch of corner loads in the render kernel.
+constexpr int kLevelGroup = 2;
+
+// G levels of one query into its fp16 row of MLP inputs.
+template <int F, bool TF16, int G, bool DENSE>
+__device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, float x0, float x1,
+                                              float x2, _Float16 *row)
+{
+    float f[G][F];
+    hash_group<F, TF16, G, DENSE>(gp, l0, x0, x1, x2, f);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int i = 0; i < F; i += 2)
+            *(h2 *)(row + (l0 + g) * F + i) = h2{(_Float16)f[g][i], (_Float16)f[g][i + 1]};
+    }
+}
+
 template <bool XF16, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
                                                         const _Float16 *__restrict__ weights,
@@ -56,6 +74,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     const int r_loc = lane / K;
     const int k = lane - r_loc * K;
     const int L = gp.L;
+    const int n_dense = gp.n_dense;
     const uint32_t hw = (uint32_t)rp.H * (uint32_t)rp.W;
 
     for (int tile = gw; tile < n_tiles; tile += total) {
@@ -69,25 +88,22 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
             ry = pixel_ray(rp, ray);
             hit = sample_position<XT>(rp, ry, rp.g0[ray], k, x0, x1, x2);
         }
-        // --- hash encoding: one level at a time, features to LDS as fp16
+        // --- hash encoding, features to LDS as fp16: dense levels first (pair
+        // loads), then hashed levels, kLevelGroup levels per batch of loads
         _Float16 *row = rows + lane * LD;
-        for (int l = 0; l < L; ++l) {
-            float f[F];
-            if (hit) {
-                hash_level<F, TF16, false>(level_base(gp, l, F, TF16), gp.N[l],
-                                           (gp.dense_mask >> l) & 1u, gp.T_mask, x0, x1, x2,
-                                           f, LevelDebug{});
-            } else {
-#pragma unroll
-                for (int i = 0; i < F; ++i) f[i] = 0.0f;
-            }
-            if (F == 2) {
-                h2 hv = {(_Float16)f[0], (_Float16)f[1]};
-                *(h2 *)(row + l * F) = hv;
-            } else {
-                h4 hv = {(_Float16)f[0], (_Float16)f[1], (_Float16)f[2], (_Float16)f[3]};
-                *(h4 *)(row + l * F) = hv;
-            }
+        if (hit) {
+            int l = 0;
+            for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
+                encode_levels<F, TF16, kLevelGroup, true>(gp, l, x0, x1, x2, row);
+            for (; l < n_dense; ++l)
+                encode_levels<F, TF16, 1, true>(gp, l, x0, x1, x2, row);
+            for (; l + kLevelGroup <= L; l += kLevelGroup)
+                encode_levels<F, TF16, kLevelGroup, false>(gp, l, x0, x1, x2, row);
+            for (; l < L; ++l)
+                encode_levels<F, TF16, 1, false>(gp, l, x0, x1, x2, row);
+        } else {
+            for (int e = 0; e < L * F; e += 2)
+                *(h2 *)(row + e) = h2{(_Float16)0.0f, (_Float16)0.0f};
         }
         if (view_sh) {
             float Y[16];
@@ -161,18 +177,24 @@ __global__ __launch_bounds__(kBlock) void hash_encode_kernel(GridParams gp, cons
     if (s >= n) return;
     const float x0 = x[3 * s], x1 = x[3 * s + 1], x2 = x[3 * s + 2];
     for (int l = 0; l < gp.L; ++l) {
-        int32_t corner[3];
-        uint32_t idx[8];
-        float w[8], f[F];
-        hash_level<F, TF16, true>(level_base(gp, l, F, TF16), gp.N[l], (gp.dense_mask >> l) & 1u,
-                                  gp.T_mask, x0, x1, x2, f, LevelDebug{corner, idx, w});
+        // the render kernel's arithmetic, one level at a time
+        LevelSetup st;
+        float v[8][F], f[F];
+        const bool dense = l < gp.n_dense;
+        level_setup(gp.N[l], dense, gp.T_mask, x0, x1, x2, st);
+        const void *base = level_base(gp, l, F, TF16);
+        if (dense)
+            level_fetch<F, TF16, true>(base, st, v);
+        else
+            level_fetch<F, TF16, false>(base, st, v);
+        level_accumulate<F>(st, v, f);
         const int64_t sl = s * gp.L + l;
         if (out_corner)
-            for (int a = 0; a < 3; ++a) out_corner[sl * 3 + a] = corner[a];
+            for (int a = 0; a < 3; ++a) out_corner[sl * 3 + a] = st.c[a];
         if (out_idx)
-            for (int b = 0; b < 8; ++b) out_idx[sl * 8 + b] = idx[b];
+            for (int b = 0; b < 8; ++b) out_idx[sl * 8 + b] = st.idx[b];
         if (out_w)
-            for (int b = 0; b < 8; ++b) out_w[sl * 8 + b] = w[b];
+            for (int b = 0; b < 8; ++b) out_w[sl * 8 + b] = corner_weight(st, b);
         if (out_feat)
             for (int i = 0; i < F; ++i) out_feat[s * gp.L * F + l * F + i] = f[i];
     }

@@ -120,7 +120,7 @@ BAD = [
     ("disp.mode", lambda d: setattr(d.disp, "mode", 1), mixrt.MIXRT_EUNSUPPORTED),
     ("disp.data", lambda d: setattr(d.disp, "data", 0), mixrt.MIXRT_EINVAL),
     ("grid.L", lambda d: setattr(d.grid, "L", 33), mixrt.MIXRT_EUNSUPPORTED),
-    ("grid.log2_T", lambda d: setattr(d.grid, "log2_T", 29), mixrt.MIXRT_EUNSUPPORTED),
+    ("grid.log2_T", lambda d: setattr(d.grid, "log2_T", 27), mixrt.MIXRT_EUNSUPPORTED),
     ("grid.F", lambda d: setattr(d.grid, "F", 3), mixrt.MIXRT_EUNSUPPORTED),
     ("grid.N", lambda d: setattr(d.grid, "N_max", 8), mixrt.MIXRT_EINVAL),
     ("grid.dtype", lambda d: setattr(d.grid, "dtype", 2), mixrt.MIXRT_EUNSUPPORTED),
