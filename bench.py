@@ -18,6 +18,75 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
 MFMA_F16_PEAK_TFLOPS = 2500.0   # MI355X dense fp16 MFMA
+PROFILE_COUNTERS = os.path.join(ROOT, "profiles", "render_kernel_view720p.counters.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2312_11841_amd", "csrc", f)
+                  for f in ("mixrt_render.hip", "mixrt_device.hpp", "mixrt_common.hpp")]
+
+
+def kernel_source_digest() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    passes, each scaled by the same counter's reading for a plain copy of known
+    size; None when no such record exists for this workload or the kernel
+    sources changed since the counters were taken."""
+    try:
+        rec = json.load(open(PROFILE_COUNTERS))
+    except (OSError, ValueError):
+        return None, "no counter record"
+    if rec.get("workload") != workload:
+        return None, "counters taken on another workload"
+    if rec.get("kernel_source_digest") != kernel_source_digest():
+        return None, "kernel changed since the counters were taken"
+    fetch = rec["FETCH_SIZE_KiB"] * 1024 * rec["fetch_scale"]
+    write = rec["WRITE_SIZE_KiB"] * 1024 * rec["write_scale"]
+    return int(fetch + write), "rocprofv3 FETCH_SIZE+WRITE_SIZE, copy-calibrated"
+
+
+def measured_rooflines(cfg):
+    """Achievable rates on this GPU from libmixrt_microbench.so: random
+    gathers at the working sets of one hash level and of the whole table,
+    streaming copy, fp16 MFMA."""
+    from paper_2312_11841_amd import microbench as mb
+    eb = 2 if cfg.table_dtype == "f16" else 4
+    entry = cfg.F * eb
+    level_bytes = cfg.T * entry
+    out = {"gather_random_lane_loads_per_s": {}, "gather_entry_bytes": entry}
+    for name, size in (("one_level", level_bytes), ("whole_table", level_bytes * cfg.L)):
+        size = 1 << (int(size) - 1).bit_length()
+        r = mb.gather(size, 4 if entry <= 4 else (8 if entry <= 8 else 16), 0, iters=128)
+        out["gather_random_lane_loads_per_s"][name] = {"bytes": size,
+                                                       "value": round(r["lane_loads_per_s"])}
+    out["copy_GBps"] = round(mb.copy(1 << 30)["GBps"], 1)
+    out["mfma_f16_TFLOPs"] = round(mb.mfma()["TFLOPs"], 1)
+    return out
+
+
+def standalone_mlp(cfg, ds, renderer, samples):
+    """The MLP stage alone (mixrt_debug_mlp) on `samples` fp16 input rows."""
+    import torch
+    x = torch.randn((samples, cfg.widths[0]), device="cuda:0").to(torch.float16)
+    xi = x.view(torch.int16)
+    renderer.mlp(ds.mlp, xi)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    s = torch.cuda.current_stream()
+    a.record(s)
+    for _ in range(5):
+        renderer.mlp(ds.mlp, xi)
+    b.record(s)
+    torch.cuda.synchronize()
+    sec = a.elapsed_time(b) / 5 * 1e-3
+    flops = samples * 2 * sum(p * q for p, q in zip(cfg.widths[:-1], cfg.widths[1:]))
+    return {"samples": samples, "ms": round(sec * 1e3, 4), "TFLOPs": round(flops / sec / 1e12, 1),
+            "util_of_peak": round(flops / sec / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+            "hbm_bytes": samples * (cfg.widths[0] * 2 + 16)}
 
 
 def algorithmic_work(cfg):
@@ -70,6 +139,8 @@ def main():
     ap.add_argument("--workload", default="view720p")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle work for the CPU baseline (0: skip)")
+    ap.add_argument("--no-rooflines", action="store_true",
+                    help="skip the microbenchmark rooflines and the standalone MLP leg")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes per step (the "
                          "reference kernel that scales the FETCH_SIZE / WRITE_SIZE counters)")
@@ -121,9 +192,14 @@ def main():
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall
     ms = start.elapsed_time(end) / args.steps
+    extra = {}
+    if not args.no_rooflines:
+        extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
+        extra["rooflines_measured"] = measured_rooflines(cfg)
     r.close()
 
     work = algorithmic_work(cfg)
+    traffic, traffic_src = measured_traffic(cfg.name)
     sec = ms * 1e-3
     total_bytes = work["hash_bytes"] + work["ray_bytes"]
     achieved = total_bytes / sec / 1e9
@@ -158,14 +234,20 @@ def main():
             "peak": HBM_PEAK_GBPS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": None,
+            "traffic": traffic,
+            "traffic_source": traffic_src,
             "algorithmic_bytes_per_launch": total_bytes,
+            "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
+                                           "ray": work["per_ray_bytes"]},
         },
         "hash_encode_GBps": round(work["hash_bytes"] / sec / 1e9, 1),
+        "hash_lane_loads_per_s": round(cfg.samples * cfg.L * 8 / sec),
         "mlp_mfma_util": round(work["mlp_flops"] / sec / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
         "mlp_tflops": round(work["mlp_flops"] / sec / 1e12, 2),
         "wall_s_timed": round(t_wall, 3),
+        "kernel_source_digest": kernel_source_digest(),
     }
+    line.update(extra)
     if args.cpu_budget > 0:
         line["cpu_baseline"] = cpu_baseline(scene, args.cpu_budget)
     print(json.dumps(line), flush=True)

@@ -201,8 +201,9 @@ int mixrt_debug_hash_encode(mixrt_ctx *ctx, const mixrt_hash_grid *grid, const f
                             int64_t n, int32_t *out_corner, uint32_t *out_idx,
                             float *out_w, float *out_feat);
 
-/* The MLP on n fp16 inputs (device [n][width[0]]); out4: device float
- * [n][4] = (sigma, r, g, b) after exp / sigmoid. */
+/* The MLP on n fp16 inputs (device [n][width[0]], 16-byte aligned); out4:
+ * device float [n][4] = (sigma, r, g, b) after exp / sigmoid, 16-byte
+ * aligned. */
 int mixrt_debug_mlp(mixrt_ctx *ctx, const mixrt_mlp *mlp, const uint16_t *in_f16, int64_t n,
                     float *out4);
 

@@ -8,7 +8,9 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmixrt.so")
-SOURCES = ["mixrt_api.cpp", "mixrt_kernels.hip"]
+SOURCES = ["mixrt_api.cpp", "mixrt_render.hip", "mixrt_stages.hip"]
+MB_LIB = os.path.join(PKG, "libmixrt_microbench.so")
+MB_SOURCES = ["microbench.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -23,8 +25,14 @@ FLAGS = [
 
 
 def build(verbose: bool = False, extra=()) -> str:
-    tmp = LIB + ".tmp"
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    _build_one(LIB, SOURCES, verbose, extra)
+    _build_one(MB_LIB, MB_SOURCES, verbose, extra)
+    return LIB
+
+
+def _build_one(lib, sources, verbose, extra):
+    tmp = lib + ".tmp"
+    srcs = [os.path.join(CSRC, s) for s in sources]
     cmd = [HIPCC, *FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, "-x", "hip", *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -35,8 +43,7 @@ def build(verbose: bool = False, extra=()) -> str:
         raise RuntimeError(f"hipcc failed ({r.returncode}):\n{err}")
     if verbose and err.strip():
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
 
 
 if __name__ == "__main__":

@@ -1,0 +1,155 @@
+// Roofline microbenchmarks for gfx950, used to calibrate the rendering
+// kernel's measured bounds (not part of the rendering path):
+//   - gather: random or coalesced loads of 4/8/16 bytes per lane from a
+//     table of a given size (the access pattern of hash-grid lookups), which
+//     measures the achievable gather rate by working set (L1/L2/MALL/HBM);
+//   - copy:   a streaming copy (HBM bandwidth);
+//   - mfma:   a dependent-free fp16 16x16x32 MFMA loop (matrix-core peak).
+// Entry points launch on the given stream and return hipError_t codes; the
+// caller times them with events on that stream.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mixrt_microbench.h"
+
+namespace {
+
+constexpr int kBlock = 256;
+
+template <int W>
+struct Vec;
+template <>
+struct Vec<4> {
+    typedef uint32_t T;
+    static __device__ __forceinline__ uint32_t fold(T v) { return v; }
+};
+template <>
+struct Vec<8> {
+    typedef uint2 T;
+    static __device__ __forceinline__ uint32_t fold(T v) { return v.x ^ v.y; }
+};
+template <>
+struct Vec<16> {
+    typedef uint4 T;
+    static __device__ __forceinline__ uint32_t fold(T v) { return v.x ^ v.y ^ v.z ^ v.w; }
+};
+
+// Each lane walks its own xorshift stream; per iteration it issues NL
+// independent loads (all issued before any is consumed).  pattern 0: a
+// random W-byte element per load; pattern 1: every lane of the wave loads
+// the same element (one cache line per instruction).
+template <int W, int NL>
+__global__ __launch_bounds__(kBlock) void gather_kernel(const char *__restrict__ table,
+                                                        uint32_t n_elems_mask, int iters,
+                                                        int pattern, uint32_t *__restrict__ sink)
+{
+    typedef typename Vec<W>::T T;
+    const uint32_t gid = blockIdx.x * kBlock + threadIdx.x;
+    uint32_t x = gid * 2654435761u + 12345u;
+    const uint32_t wave_seed = (gid / 64u) * 2246822519u + 777u;
+    uint32_t acc = 0;
+    for (int it = 0; it < iters; ++it) {
+        uint32_t off[NL];
+#pragma unroll
+        for (int q = 0; q < NL; ++q) {
+            x ^= x << 13;
+            x ^= x >> 17;
+            x ^= x << 5;
+            const uint32_t r = pattern ? (wave_seed + (uint32_t)(it * NL + q) * 40503u) : x;
+            off[q] = (r & n_elems_mask) * (uint32_t)W;
+        }
+        T v[NL];
+#pragma unroll
+        for (int q = 0; q < NL; ++q)
+            v[q] = *(const T *)(table + off[q]);
+#pragma unroll
+        for (int q = 0; q < NL; ++q)
+            acc ^= Vec<W>::fold(v[q]);
+    }
+    sink[gid] = acc;
+}
+
+__global__ __launch_bounds__(kBlock) void copy_kernel(const uint4 *__restrict__ src,
+                                                      uint4 *__restrict__ dst, uint64_t n)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    for (uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x; i < n; i += stride)
+        dst[i] = src[i];
+}
+
+typedef _Float16 h8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+
+// 8 independent accumulators per wave, so consecutive MFMAs do not depend on
+// each other.
+__global__ __launch_bounds__(kBlock) void mfma_kernel(int iters, float *__restrict__ out)
+{
+    const int lane = threadIdx.x & 63;
+    h8 a, b;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        a[j] = (_Float16)(0.001f * (lane + j));
+        b[j] = (_Float16)(0.002f * (lane - j));
+    }
+    f4 acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, acc[u], 0, 0, 0);
+    }
+    f4 s = acc[0];
+#pragma unroll
+    for (int u = 1; u < 8; ++u) s += acc[u];
+    out[blockIdx.x * kBlock + threadIdx.x] = s[0] + s[1] + s[2] + s[3];
+}
+
+}  // namespace
+
+extern "C" {
+
+int mixrt_mb_gather(const void *table, uint64_t table_bytes, int width, int loads_per_iter,
+                    int iters, int pattern, int blocks, uint32_t *sink, void *stream)
+{
+    if (!table || !sink || blocks < 1 || iters < 1) return hipErrorInvalidValue;
+    if (width != 4 && width != 8 && width != 16) return hipErrorInvalidValue;
+    if (loads_per_iter != 1 && loads_per_iter != 8) return hipErrorInvalidValue;
+    const uint64_t n = table_bytes / (uint64_t)width;
+    if (n == 0 || (n & (n - 1)) || n > (1ull << 32)) return hipErrorInvalidValue;
+    const uint32_t mask = (uint32_t)(n - 1);
+    hipStream_t s = (hipStream_t)stream;
+    const char *t = (const char *)table;
+#define G(W, NL)                                                                              \
+    hipLaunchKernelGGL((gather_kernel<W, NL>), dim3(blocks), dim3(kBlock), 0, s, t, mask, iters, \
+                       pattern, sink)
+    if (loads_per_iter == 8) {
+        if (width == 4) G(4, 8);
+        else if (width == 8) G(8, 8);
+        else G(16, 8);
+    } else {
+        if (width == 4) G(4, 1);
+        else if (width == 8) G(8, 1);
+        else G(16, 1);
+    }
+#undef G
+    return hipGetLastError();
+}
+
+int mixrt_mb_copy(const void *src, void *dst, uint64_t bytes, int blocks, void *stream)
+{
+    if (!src || !dst || (bytes & 15) || blocks < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream,
+                       (const uint4 *)src, (uint4 *)dst, bytes / 16);
+    return hipGetLastError();
+}
+
+int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream)
+{
+    if (!out || blocks < 1 || iters < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(mfma_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream, iters,
+                       out);
+    return hipGetLastError();
+}
+
+}  // extern "C"

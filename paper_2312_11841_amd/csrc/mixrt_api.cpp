@@ -2,7 +2,7 @@
 //
 // Host side: descriptor validation (pure host code, no HIP call), the level
 // resolution table, camera constants, and the launches of the kernels in
-// mixrt_kernels.hip on the context's stream.
+// mixrt_render.hip and mixrt_stages.hip on the context's stream.
 #include "mixrt.h"
 
 #include <hip/hip_runtime.h>
@@ -438,11 +438,13 @@ int mixrt_debug_mlp(mixrt_ctx *ctx, const mixrt_mlp *mlp, const uint16_t *in_f16
     if (rc) return fail(ctx, rc, "%s", msg);
     if (n < 0 || n >= ((int64_t)1 << 40)) return fail(ctx, MIXRT_EINVAL, "n=%lld", (long long)n);
     if (n > 0 && (!in_f16 || !out4)) return fail(ctx, MIXRT_EINVAL, "in or out is NULL");
+    if (n > 0 && (!aligned16(in_f16) || !aligned16(out4)))
+        return fail(ctx, MIXRT_EINVAL, "in_f16/out4 not 16-byte aligned");
     if ((rc = bind_device(ctx))) return rc;
     return finish_launch(ctx,
                          mixrt::launch_mlp(mlp->width[0], hid, nhid, (const _Float16 *)mlp->data,
                                            (const _Float16 *)in_f16, n, (float4 *)out4,
-                                           ctx->stream),
+                                           ctx->cus, ctx->stream),
                          "mlp");
 }
 

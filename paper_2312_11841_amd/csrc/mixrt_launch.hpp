@@ -1,4 +1,5 @@
-// Internal interface between the C ABI (mixrt_api.cpp) and the kernels.
+// Internal interface between the C ABI (mixrt_api.cpp) and the kernels
+// (mixrt_render.hip, mixrt_stages.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -29,7 +30,7 @@ hipError_t launch_ray_setup(const RayParams &rp, bool xf16, float *out_x, int32_
 hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const float *x, int64_t n,
                               int32_t *oc, uint32_t *oi, float *ow, float *of, hipStream_t stream);
 hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const _Float16 *x,
-                      int64_t n, float4 *out4, hipStream_t stream);
+                      int64_t n, float4 *out4, int cus, hipStream_t stream);
 hipError_t launch_composite(const float4 *srgb, int64_t rays, int K, float delta, float t_term,
                             const float *bg, float4 *out, hipStream_t stream);
 

@@ -1,0 +1,171 @@
+// The hot path: the fused per-pixel render kernel of the MixRT path for
+// gfx950, and its launcher.
+//
+// render_kernel is one persistent kernel in which each wave repeatedly takes
+// a tile of 64 sample slots (64/K rays x K samples), runs ray setup, Eq. 2
+// calibration, contraction and the hash encoding with one sample per lane,
+// stages the fp16 MLP inputs in its own slice of LDS, runs the MLP on MFMA
+// with register-resident weights, and composites each ray's samples.  Nothing
+// is written to HBM except the RGBA result.
+#include "mixrt_common.hpp"
+#include "mixrt_launch.hpp"
+
+namespace mixrt {
+
+// Levels per batch of corner loads in the render kernel.
+constexpr int kLevelGroup = 2;
+
+// G levels of one query into its fp16 row of MLP inputs.
+template <int F, bool TF16, int G, bool DENSE>
+__device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, float x0, float x1,
+                                              float x2, _Float16 *row)
+{
+    float f[G][F];
+    hash_group<F, TF16, G, DENSE>(gp, l0, x0, x1, x2, f);
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+#pragma unroll
+        for (int i = 0; i < F; i += 2)
+            *(h2 *)(row + (l0 + g) * F + i) = h2{(_Float16)f[g][i], (_Float16)f[g][i + 1]};
+    }
+}
+
+template <bool XF16, int F, bool TF16, int IN, int HID, int NHID>
+__global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
+                                                        const _Float16 *__restrict__ weights,
+                                                        int view_sh, float4 *__restrict__ out)
+{
+    typedef typename std::conditional<XF16, _Float16, float>::type XT;
+    constexpr int LD = IN + 8;  // padded row of MLP inputs (halves), 16-byte multiple
+    __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][kWave * LD];
+    __shared__ float4 s_out[kWavesPerBlock][kWave];
+    __shared__ int s_hit[kWavesPerBlock][kWave];
+
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x / kWave;
+    _Float16 *rows = s_rows[wv];
+
+    MlpWeights<IN, HID, NHID> Wt;
+    Wt.load(weights, lane);
+
+    const int K = rp.K;
+    const int R = kWave / K;                 // rays per tile
+    const int spt = R * K;                   // sample slots used per tile
+    const int n_tiles = (rp.rays + R - 1) / R;
+    const int gw = xcd_logical_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wv;
+    const int total = gridDim.x * kWavesPerBlock;
+    const int r_loc = lane / K;
+    const int k = lane - r_loc * K;
+    const int L = gp.L;
+    const int n_dense = gp.n_dense;
+    const uint32_t hw = (uint32_t)rp.H * (uint32_t)rp.W;
+
+    for (int tile = gw; tile < n_tiles; tile += total) {
+        const int ray0 = tile * R;
+        const int ray = ray0 + r_loc;
+        const bool valid = lane < spt && ray < rp.rays;
+        float x0 = 0.0f, x1 = 0.0f, x2 = 0.0f;
+        bool hit = false;
+        Ray ry = {};
+        if (valid) {
+            ry = pixel_ray(rp, ray);
+            hit = sample_position<XT>(rp, ry, rp.g0[ray], k, x0, x1, x2);
+        }
+        // --- hash encoding, features to LDS as fp16: dense levels first (pair
+        // loads), then hashed levels, kLevelGroup levels per batch of loads
+        _Float16 *row = rows + lane * LD;
+        if (hit) {
+            int l = 0;
+            for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
+                encode_levels<F, TF16, kLevelGroup, true>(gp, l, x0, x1, x2, row);
+            for (; l < n_dense; ++l)
+                encode_levels<F, TF16, 1, true>(gp, l, x0, x1, x2, row);
+            for (; l + kLevelGroup <= L; l += kLevelGroup)
+                encode_levels<F, TF16, kLevelGroup, false>(gp, l, x0, x1, x2, row);
+            for (; l < L; ++l)
+                encode_levels<F, TF16, 1, false>(gp, l, x0, x1, x2, row);
+        } else {
+            for (int e = 0; e < L * F; e += 2)
+                *(h2 *)(row + e) = h2{(_Float16)0.0f, (_Float16)0.0f};
+        }
+        if (view_sh) {
+            float Y[16];
+            sh_basis<16>(ry.dx, ry.dy, ry.dz, Y);
+#pragma unroll
+            for (int e = 0; e < 16; e += 2) {
+                h2 hv = {(_Float16)(valid ? Y[e] : 0.0f), (_Float16)(valid ? Y[e + 1] : 0.0f)};
+                *(h2 *)(row + L * F + e) = hv;
+            }
+        }
+        s_hit[wv][lane] = hit ? 1 : 0;
+        wave_lds_sync();
+        // --- MLP on MFMA, 16 samples per step
+        const int c = lane & 15, g = lane >> 4;
+        const int n_nt = (spt + 15) >> 4;
+        for (int nt = 0; nt < n_nt; ++nt) {
+            const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
+            if (g == 0) {
+                const int s = nt * 16 + c;
+                float4 a = mlp_activate(o);
+                if (!s_hit[wv][s]) a.x = 0.0f;   // no density on a missed ray
+                s_out[wv][s] = a;
+            }
+        }
+        wave_lds_sync();
+        // --- compositing, one lane per ray
+        if (lane < R) {
+            const int ray_c = ray0 + lane;
+            if (ray_c < rp.rays) {
+                Composite cp;
+                for (int kk = 0; kk < K; ++kk)
+                    if (!cp.add(s_out[wv][lane * K + kk], rp.delta, rp.t_term)) break;
+                const CamK &cam = rp.cams[(uint32_t)ray_c / hw];
+                out[ray_c] = cp.finish(cam.bg[0], cam.bg[1], cam.bg[2]);
+            }
+        }
+        wave_lds_sync();
+    }
+}
+
+
+#define MIXRT_RENDER_VARIANTS(X)      \
+    X(false, 2, false, 16, 32, 1)     \
+    X(false, 2, false, 32, 32, 1)     \
+    X(true, 2, true, 48, 64, 2)       \
+    X(true, 2, true, 32, 64, 2)       \
+    X(true, 4, true, 32, 64, 2)       \
+    X(true, 4, true, 16, 64, 2)
+
+bool render_variant_supported(bool xf16, int F, bool tf16, int in, int hid, int nhid)
+{
+#define X(a, b, c, d, e, f) \
+    if (xf16 == a && F == b && tf16 == c && in == d && hid == e && nhid == f) return true;
+    MIXRT_RENDER_VARIANTS(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
+{
+    const int R = kWave / L.rp.K;
+    const int64_t n_tiles = ((int64_t)L.rp.rays + R - 1) / R;
+    const int64_t want = (n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+#define X(a, b, c, d, e, f)                                                                    \
+    if (L.xf16 == a && L.F == b && L.tf16 == c && L.in == d && L.hid == e && L.nhid == f) {     \
+        auto fn = render_kernel<a, b, c, d, e, f>;                                             \
+        static int resident = 0; /* blocks resident on the whole device */                    \
+        if (!resident) resident = resident_blocks((const void *)fn, L.cus);                    \
+        int64_t blocks = resident;                                                             \
+        if (want < blocks) blocks = want;                                                      \
+        if (blocks > 8) blocks -= blocks % 8;                                                  \
+        if (blocks < 1) blocks = 1;                                                            \
+        hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, L.rp, L.gp,    \
+                           L.weights, L.view_sh, L.out);                                       \
+        return hipGetLastError();                                                              \
+    }
+    MIXRT_RENDER_VARIANTS(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+}  // namespace mixrt

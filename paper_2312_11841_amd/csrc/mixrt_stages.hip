@@ -1,0 +1,183 @@
+// Stage kernels of the MixRT path (the entry points that expose one stage's
+// intermediates): they call the same device functions as render_kernel.
+#include "mixrt_common.hpp"
+#include "mixrt_launch.hpp"
+
+namespace mixrt {
+
+template <bool XF16>
+__global__ __launch_bounds__(kBlock) void ray_setup_kernel(RayParams rp, float *__restrict__ out_x,
+                                                           int32_t *__restrict__ out_hit)
+{
+    typedef typename std::conditional<XF16, _Float16, float>::type XT;
+    const int64_t idx = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    const int64_t n = (int64_t)rp.rays * rp.K;
+    if (idx >= n) return;
+    const int ray = (int)(idx / rp.K);
+    const int k = (int)(idx - (int64_t)ray * rp.K);
+    const Ray ry = pixel_ray(rp, ray);
+    float x0, x1, x2;
+    const bool hit = sample_position<XT>(rp, ry, rp.g0[ray], k, x0, x1, x2);
+    out_x[idx * 3 + 0] = x0;
+    out_x[idx * 3 + 1] = x1;
+    out_x[idx * 3 + 2] = x2;
+    if (out_hit && k == 0) out_hit[ray] = hit ? 1 : 0;
+}
+
+template <int F, bool TF16>
+__global__ __launch_bounds__(kBlock) void hash_encode_kernel(GridParams gp, const float *__restrict__ x,
+                                                             int64_t n, int32_t *out_corner,
+                                                             uint32_t *out_idx, float *out_w,
+                                                             float *out_feat)
+{
+    const int64_t s = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (s >= n) return;
+    const float x0 = x[3 * s], x1 = x[3 * s + 1], x2 = x[3 * s + 2];
+    for (int l = 0; l < gp.L; ++l) {
+        // the render kernel's arithmetic, one level at a time
+        LevelSetup st;
+        float v[8][F], f[F];
+        const bool dense = l < gp.n_dense;
+        level_setup(gp.N[l], dense, gp.T_mask, x0, x1, x2, st);
+        const void *base = level_base(gp, l, F, TF16);
+        if (dense)
+            level_fetch<F, TF16, true>(base, st, v);
+        else
+            level_fetch<F, TF16, false>(base, st, v);
+        level_accumulate<F>(st, v, f);
+        const int64_t sl = s * gp.L + l;
+        if (out_corner)
+            for (int a = 0; a < 3; ++a) out_corner[sl * 3 + a] = st.c[a];
+        if (out_idx)
+            for (int b = 0; b < 8; ++b) out_idx[sl * 8 + b] = st.idx[b];
+        if (out_w)
+            for (int b = 0; b < 8; ++b) out_w[sl * 8 + b] = corner_weight(st, b);
+        if (out_feat)
+            for (int i = 0; i < F; ++i) out_feat[s * gp.L * F + l * F + i] = f[i];
+    }
+}
+
+template <int IN, int HID, int NHID>
+__global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict__ weights,
+                                                     const _Float16 *__restrict__ in, int64_t n,
+                                                     float4 *__restrict__ out4)
+{
+    constexpr int LD = IN + 8;
+    __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][kWave * LD];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x / kWave;
+    _Float16 *rows = s_rows[wv];
+    MlpWeights<IN, HID, NHID> Wt;
+    Wt.load(weights, lane);
+    // persistent: weights are loaded once per wave, then 64-row tiles
+    const int64_t n_tiles = (n + kWave - 1) / kWave;
+    const int64_t total = (int64_t)gridDim.x * kWavesPerBlock;
+    const int c = lane & 15, g = lane >> 4;
+    for (int64_t tile = (int64_t)blockIdx.x * kWavesPerBlock + wv; tile < n_tiles; tile += total) {
+        const int64_t base = tile * kWave;
+        // stage 64 rows (zeros past n), 16 bytes at a time
+        const int64_t r = base + lane;
+#pragma unroll
+        for (int e = 0; e < IN; e += 8)
+            *(h8 *)(rows + lane * LD + e) = r < n ? *(const h8 *)(in + r * IN + e) : h8{};
+        wave_lds_sync();
+        for (int nt = 0; nt < 4; ++nt) {
+            const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
+            const int64_t s = base + nt * 16 + c;
+            if (g == 0 && s < n) out4[s] = mlp_activate(o);
+        }
+        wave_lds_sync();
+    }
+}
+
+__global__ __launch_bounds__(kBlock) void composite_kernel(const float4 *__restrict__ srgb,
+                                                           int64_t rays, int K, float delta,
+                                                           float t_term, float bg0, float bg1,
+                                                           float bg2, float4 *__restrict__ out)
+{
+    const int64_t r = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (r >= rays) return;
+    Composite cp;
+    for (int k = 0; k < K; ++k)
+        if (!cp.add(srgb[r * K + k], delta, t_term)) break;
+    out[r] = cp.finish(bg0, bg1, bg2);
+}
+
+#define MIXRT_MLP_VARIANTS(X) \
+    X(16, 32, 1)              \
+    X(32, 32, 1)              \
+    X(48, 64, 2)              \
+    X(32, 64, 2)              \
+    X(16, 64, 2)
+
+bool mlp_variant_supported(int in, int hid, int nhid)
+{
+#define X(d, e, f) \
+    if (in == d && hid == e && nhid == f) return true;
+    MIXRT_MLP_VARIANTS(X)
+#undef X
+    return false;
+}
+
+hipError_t launch_ray_setup(const RayParams &rp, bool xf16, float *out_x, int32_t *out_hit,
+                            hipStream_t stream)
+{
+    const int64_t n = (int64_t)rp.rays * rp.K;
+    if (n == 0) return hipSuccess;
+    const dim3 grid((unsigned)((n + kBlock - 1) / kBlock));
+    if (xf16)
+        hipLaunchKernelGGL(ray_setup_kernel<true>, grid, dim3(kBlock), 0, stream, rp, out_x, out_hit);
+    else
+        hipLaunchKernelGGL(ray_setup_kernel<false>, grid, dim3(kBlock), 0, stream, rp, out_x,
+                           out_hit);
+    return hipGetLastError();
+}
+
+hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const float *x, int64_t n,
+                              int32_t *oc, uint32_t *oi, float *ow, float *of, hipStream_t stream)
+{
+    if (n == 0) return hipSuccess;
+    const dim3 grid((unsigned)((n + kBlock - 1) / kBlock));
+#define LAUNCH(FF, TT)                                                                         \
+    hipLaunchKernelGGL((hash_encode_kernel<FF, TT>), grid, dim3(kBlock), 0, stream, gp, x, n, oc, \
+                       oi, ow, of)
+    if (F == 2 && tf16) LAUNCH(2, true);
+    else if (F == 2) LAUNCH(2, false);
+    else if (F == 4 && tf16) LAUNCH(4, true);
+    else if (F == 4) LAUNCH(4, false);
+    else return hipErrorInvalidValue;
+#undef LAUNCH
+    return hipGetLastError();
+}
+
+hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const _Float16 *x,
+                      int64_t n, float4 *out4, int cus, hipStream_t stream)
+{
+    if (n == 0) return hipSuccess;
+    const int64_t want = ((n + kWave - 1) / kWave + kWavesPerBlock - 1) / kWavesPerBlock;
+#define X(d, e, f)                                                                           \
+    if (in == d && hid == e && nhid == f) {                                                  \
+        auto fn = mlp_kernel<d, e, f>;                                                       \
+        static int resident = 0;                                                             \
+        if (!resident) resident = resident_blocks((const void *)fn, cus);                    \
+        const int64_t blocks = want < resident ? want : resident;                            \
+        hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, weights, x, n, \
+                           out4);                                                            \
+        return hipGetLastError();                                                            \
+    }
+    MIXRT_MLP_VARIANTS(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t launch_composite(const float4 *srgb, int64_t rays, int K, float delta, float t_term,
+                            const float *bg, float4 *out, hipStream_t stream)
+{
+    if (rays == 0) return hipSuccess;
+    const dim3 grid((unsigned)((rays + kBlock - 1) / kBlock));
+    hipLaunchKernelGGL(composite_kernel, grid, dim3(kBlock), 0, stream, srgb, rays, K, delta,
+                       t_term, bg[0], bg[1], bg[2], out);
+    return hipGetLastError();
+}
+
+}  // namespace mixrt

@@ -1,0 +1,100 @@
+"""Roofline microbenchmarks (libmixrt_microbench.so): achievable gather rate by
+working-set size, streaming-copy bandwidth and fp16 MFMA throughput on the
+current GPU.  These calibrate the rendering kernel's measured bounds; they
+are not part of the rendering path."""
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libmixrt_microbench.so")
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build with paper_2312_11841_amd/build.py")
+        L = C.CDLL(LIB_PATH)
+        P = C.c_void_p
+        L.mixrt_mb_gather.argtypes = [P, C.c_uint64, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
+                                      P, P]
+        L.mixrt_mb_copy.argtypes = [P, P, C.c_uint64, C.c_int, P]
+        L.mixrt_mb_mfma.argtypes = [C.c_int, C.c_int, P, P]
+        for f in (L.mixrt_mb_gather, L.mixrt_mb_copy, L.mixrt_mb_mfma):
+            f.restype = C.c_int
+        _lib = L
+    return _lib
+
+
+def _timed(launch, reps=5):
+    import torch
+    s = torch.cuda.current_stream()
+    launch(s)  # warm
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(s)
+    for _ in range(reps):
+        launch(s)
+    b.record(s)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / reps * 1e-3
+
+
+def _check(rc):
+    if rc != 0:
+        raise RuntimeError(f"microbenchmark launch failed: hipError {rc}")
+
+
+def gather(table_bytes: int, width: int = 4, pattern: int = 0, iters: int = 64,
+           blocks: int | None = None):
+    """Random (pattern 0) or coalesced (pattern 1) gathers; returns rates."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = blocks or cus * 8
+    table = torch.randint(0, 2 ** 31, (table_bytes // 4,), dtype=torch.int32, device="cuda")
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    nl = 8
+
+    def launch(s):
+        _check(lib().mixrt_mb_gather(table.data_ptr(), table_bytes, width, nl, iters, pattern,
+                                     blocks, sink.data_ptr(), s.cuda_stream))
+
+    t = _timed(launch)
+    lane_loads = blocks * 256 * iters * nl
+    wave_instr = lane_loads / 64
+    return {"table_bytes": table_bytes, "width": width, "pattern": pattern,
+            "seconds": t, "lane_loads_per_s": lane_loads / t,
+            "useful_GBps": lane_loads * width / t / 1e9,
+            "wave_instr_per_s": wave_instr / t,
+            "ns_per_wave_instr_per_cu": t * 1e9 * cus / wave_instr}
+
+
+def copy(bytes_: int = 1 << 30, blocks: int | None = None):
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = blocks or cus * 8
+    src = torch.empty(bytes_, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+
+    def launch(s):
+        _check(lib().mixrt_mb_copy(src.data_ptr(), dst.data_ptr(), bytes_, blocks, s.cuda_stream))
+
+    t = _timed(launch)
+    return {"bytes": bytes_, "seconds": t, "GBps": 2 * bytes_ / t / 1e9}
+
+
+def mfma(iters: int = 4096, blocks: int | None = None):
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = blocks or cus * 8
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+
+    def launch(s):
+        _check(lib().mixrt_mb_mfma(iters, blocks, out.data_ptr(), s.cuda_stream))
+
+    t = _timed(launch)
+    flops = blocks * 4 * iters * 8 * (2 * 16 * 16 * 32)
+    return {"seconds": t, "TFLOPs": flops / t / 1e12}
