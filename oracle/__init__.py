@@ -13,7 +13,9 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+# MIXRT_ORACLE_LIB: load another build of mixrt_oracle.c (the mutation test
+# uses it to check that the pins reject planted mistakes).
+_LIB_PATH = os.environ.get("MIXRT_ORACLE_LIB", os.path.join(_HERE, "liboracle.so"))
 _lib = None
 
 _DT = {np.dtype(np.float32): 0, np.dtype(np.float16): 1}

@@ -1,0 +1,54 @@
+"""The pins must reject plausible mistakes: each case plants one mistake in a
+copy of the oracle's C source (on the CPU), builds it, and requires the pin
+suite to fail against that build."""
+import os
+import subprocess
+import sys
+import tempfile
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "mixrt_oracle.c")
+
+MUTATIONS = {
+    "prime_swap": ("(uint32_t)v[1] * 2654435761u) ^ ((uint32_t)v[2] * 805459861u)",
+                   "(uint32_t)v[1] * 805459861u) ^ ((uint32_t)v[2] * 2654435761u)"),
+    "xor_to_plus": ("((uint32_t)v[0] * 1u) ^ ((uint32_t)v[1]", "((uint32_t)v[0] * 1u) + ((uint32_t)v[1]"),
+    "dense_strides": ("side * (uint64_t)v[1] + side * side * (uint64_t)v[2]",
+                      "side * (uint64_t)v[2] + side * side * (uint64_t)v[1]"),
+    "uv_swap": ("double a = u * R - 0.5, b = v * R - 0.5;", "double a = v * R - 0.5, b = u * R - 0.5;"),
+    "no_half_texel": ("double a = u * R - 0.5, b = v * R - 0.5;", "double a = u * R, b = v * R;"),
+    "inclusive_T": ("double T = exp(-optical);\n            double alpha",
+                    "double T = exp(-optical - s[4 * k] * delta);\n            double alpha"),
+    "weight_flip": ("wt *= bit ? fr[a] : 1.0 - fr[a];", "wt *= bit ? 1.0 - fr[a] : fr[a];"),
+    "sh_sign": ("return sqrt(2.0) * k * p * sin((double)am * phi);",
+                "return -sqrt(2.0) * k * p * sin((double)am * phi);"),
+    "contract_norm": ("(2.0 - 1.0 / r) * (q[a] / r)", "(2.0 - 1.0 / r) * q[a]"),
+    "fov_full": ("tan(0.5 * (double)cam[12]", "tan((double)cam[12]"),
+    "row_up": ("-((double)j + 0.5 - 0.5 * H) / f", "((double)j + 0.5 - 0.5 * H) / f"),
+    "sample_offset": ("((double)k - 0.5 * (double)(sc->K - 1)) * sc->delta", "((double)k) * sc->delta"),
+    "relu_on_head": ("b[o] = (m < n_layers - 1 && acc < 0.0) ? 0.0 : acc;", "b[o] = (acc < 0.0) ? 0.0 : acc;"),
+    "no_level_guard": ("pow(b, (double)l) + 1e-6)", "pow(b, (double)l))"),
+    "calibration_sign": ("p_cali[r] = p[r] + s * d[r];", "p_cali[r] = p[r] - s * d[r];"),
+    "corner_clamp": ("c0[a] = c < 0 ? 0 : (c > N - 1 ? N - 1 : c);", "c0[a] = c < 0 ? 0 : (c > N ? N : c);"),
+    "subnormal_exp": ("v = ldexp((double)mant, -24);", "v = ldexp((double)mant, -25);"),
+    "no_background": ("out[4 * r + ch] = c[ch] + Tend * bg[3 * r + ch];", "out[4 * r + ch] = c[ch];"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTATIONS))
+def test_pins_reject_planted_mistake(name, tmp_path):
+    a, b = MUTATIONS[name]
+    src = open(SRC).read()
+    assert src.count(a) == 1, f"mutation anchor for {name} not found once"
+    mut = tmp_path / "mut.c"
+    mut.write_text(src.replace(a, b))
+    lib = tmp_path / "liboracle_mut.so"
+    subprocess.run(["gcc", "-O2", "-fno-fast-math", "-ffp-contract=off", "-fopenmp", "-shared",
+                    "-fPIC", str(mut), "-o", str(lib), "-lm"], check=True)
+    env = dict(os.environ, MIXRT_ORACLE_LIB=str(lib))
+    r = subprocess.run([sys.executable, "-m", "pytest", os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        "-x", "-q", "-p", "no:cacheprovider"], cwd=ROOT, env=env,
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0, f"pins did not catch {name}:\n{r.stdout[-2000:]}"
