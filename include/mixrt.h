@@ -51,7 +51,13 @@ enum mixrt_disp_mode {
     /* The V channels at p_t are coefficients of the first V real spherical
      * harmonics of the view direction d (bands by degree, m = -l..l); their
      * weighted sum s is a signed length and p_cali = p + s d. */
-    MIXRT_DISP_ALONG_RAY = 0
+    MIXRT_DISP_ALONG_RAY = 0,
+    /* Eq. 2 as printed: channel a*nb + v (nb = (sh_degree+1)^2, a = x, y, z)
+     * is the coefficient of harmonic v for axis a; S = (sum_v Y_v(d) m[a*nb+v])_a
+     * and p_cali = p + m_s(p_t) S with the scale map m_s. */
+    MIXRT_DISP_SH_VEC3 = 1,
+    /* No displacement map: p_cali = p. */
+    MIXRT_DISP_NONE = 2
 };
 
 /* Context creation flags. */
@@ -101,10 +107,18 @@ typedef struct {
 typedef struct {
     int32_t R;           /* texture is R x R texels, addressed with texel
                             centres at (i + 0.5) / R, clamp to edge, row from v */
-    int32_t V;           /* channels per texel, 1..16 */
-    int32_t dtype;       /* MIXRT_F32 or MIXRT_F16 */
+    int32_t V;           /* ALONG_RAY: channels used, 1..16 (ignored otherwise) */
+    int32_t dtype;       /* MIXRT_F32, MIXRT_F16 or MIXRT_U8 */
     int32_t mode;        /* mixrt_disp_mode */
-    const void *data;    /* device [R][R][V]; 16-byte aligned */
+    const void *data;    /* device [R][R][C]; 16-byte aligned; NULL for NONE */
+    int32_t C;           /* stored channels per texel, >= channels used; 0
+                            means exactly the channels used.  Texels of a
+                            multiple of 16 bytes are read with vector loads */
+    int32_t sh_degree;   /* SH_VEC3: degree 0..3, 3 (sh_degree+1)^2 channels */
+    const void *scale;   /* SH_VEC3: device [R][R] scale map m_s of dtype */
+    float q_scale[2];    /* MIXRT_U8: value = q_offset + q_scale * q, for */
+    float q_offset[2];   /* [0] the coefficient map and [1] the scale map
+                            (the maps are quantised to 8 bits, Sec. 4.3.2) */
 } mixrt_disp_tex;
 
 /* Multiresolution hash grid (Sec. 3.1, 4.3.3, 5.1.2).  Level l has

@@ -18,7 +18,8 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _LIB_PATH = os.environ.get("MIXRT_ORACLE_LIB", os.path.join(_HERE, "liboracle.so"))
 _lib = None
 
-_DT = {np.dtype(np.float32): 0, np.dtype(np.float16): 1}
+_DT = {np.dtype(np.float32): 0, np.dtype(np.float16): 1, np.dtype(np.uint8): 2}
+_DISP = {"ray": 0, "vec3": 1, "none": 2}
 
 
 def lib():
@@ -48,6 +49,11 @@ def _declare(L):
     L.orc_tex_bilinear.argtypes = [P, C.c_int, C.c_int, C.c_int, C.c_double, C.c_double, P]
     L.orc_calibrate.restype = None
     L.orc_calibrate.argtypes = [P, P, P, C.c_int, P]
+    L.orc_calibrate_vec3.restype = None
+    L.orc_calibrate_vec3.argtypes = [P, P, P, C.c_int, C.c_double, P]
+    L.orc_map_bilinear.restype = None
+    L.orc_map_bilinear.argtypes = [P, C.c_int, C.c_int, C.c_int, C.c_int, C.c_double,
+                                   C.c_double, C.c_double, C.c_double, P]
     L.orc_contract.restype = None
     L.orc_contract.argtypes = [P, P]
     L.orc_hash_level.restype = None
@@ -84,6 +90,8 @@ class _OrcScene(C.Structure):
         ("n_max", C.c_int), ("table_dtype", C.c_int), ("table", C.c_void_p),
         ("n_layers", C.c_int), ("widths", C.c_void_p), ("view_sh_dim", C.c_int),
         ("weights", C.c_void_p), ("K", C.c_int), ("delta", C.c_double),
+        ("disp_mode", C.c_int), ("tex_C", C.c_int), ("sh_degree", C.c_int),
+        ("scale", C.c_void_p), ("q_scale", C.c_double * 2), ("q_offset", C.c_double * 2),
     ]
 
 
@@ -130,6 +138,26 @@ def tex_bilinear(tex: np.ndarray, u: float, v: float) -> np.ndarray:
     assert R == R2
     out = np.zeros(V)
     lib().orc_tex_bilinear(_p(tex), _DT[tex.dtype], R, V, float(u), float(v), _p(out))
+    return out
+
+
+def map_bilinear(data: np.ndarray, nch: int, u: float, v: float, q_scale=0.0,
+                 q_offset=0.0) -> np.ndarray:
+    """Bilinear fetch of the first nch of C stored channels ([R][R][C] map)."""
+    data = np.ascontiguousarray(data)
+    if data.ndim == 2:
+        data = data[..., None]
+    R, _, Cst = data.shape
+    out = np.zeros(nch)
+    lib().orc_map_bilinear(_p(data), _DT[data.dtype], R, Cst, nch, float(q_scale),
+                           float(q_offset), float(u), float(v), _p(out))
+    return out
+
+
+def calibrate_vec3(p, d, m, nb: int, ms: float) -> np.ndarray:
+    p, d, m = _c(p, np.float64), _c(d, np.float64), _c(m, np.float64)
+    out = np.zeros(3)
+    lib().orc_calibrate_vec3(_p(p), _p(d), _p(m), nb, float(ms), _p(out))
     return out
 
 
@@ -219,6 +247,14 @@ class OracleScene:
         s.view_sh_dim = cfg.view_sh_dim
         s.weights = wbits.ctypes.data
         s.K, s.delta = cfg.K, float(cfg.delta)
+        s.disp_mode = _DISP[cfg.disp]
+        s.tex_C = scene.tex.shape[2]
+        s.sh_degree = cfg.sh_degree
+        if scene.scale is not None:
+            self._keep.append(scene.scale)
+            s.scale = scene.scale.ctypes.data
+        s.q_scale[:] = [float(q) for q in scene.q_scale]
+        s.q_offset[:] = [float(q) for q in scene.q_offset]
         self.desc = s
 
     def render_pixels(self, pix, threads: int = 1) -> np.ndarray:

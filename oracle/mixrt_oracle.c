@@ -28,8 +28,10 @@
  * Readings where the paper is silent or inconsistent:
  *   - Eq. 1 transmittance is exclusive of sample k; delta_k = delta for all k;
  *     the final transmittance blends a background colour.
- *   - Eq. 2 scalar form: the V channels are coefficients of the first V real
- *     spherical harmonics of d, their sum is a length along d (scale map 1).
+ *   - Eq. 2, scalar form: the V channels are coefficients of the first V
+ *     real spherical harmonics of d, their sum is a length along d (scale
+ *     map 1).  Eq. 2 as printed (a 3-vector of SH sums times the scale map)
+ *     and no displacement are the other two forms.
  *   - texels are addressed GL-style: centres at (i+0.5)/R, clamp to edge.
  *   - level resolutions N_l = floor(N_min b^l + 1e-6), b the geometric growth
  *     factor from N_min to N_max; dense indexing when (N_l+1)^3 <= T, else the
@@ -51,6 +53,8 @@
 #define ORC_PI 3.14159265358979323846
 
 enum { ORC_F32 = 0, ORC_F16 = 1, ORC_U8 = 2 };
+
+static int clampi(int v, int lo, int hi);
 
 /* ------------------------------------------------------------------------ */
 /* Stored values                                                              */
@@ -191,9 +195,26 @@ void orc_camera_ray(const float *cam, int W, int H, int i, int j, double *o, dou
 
 static int clampi(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 
-/* Bilinear fetch of the V channels of an [R][R][V] texture at (u, v). */
-void orc_tex_bilinear(const void *tex, int dtype, int R, int V, double u, double v, double *out)
+/* A displacement-map texture: [R][R][C] values of one dtype; 8-bit values
+ * stand for q_offset + q_scale * q (the maps are quantised to 8 bits after
+ * training, Sec. 4.3.2). */
+typedef struct {
+    int R, C, dtype;
+    const void *data;
+    double q_scale, q_offset;
+} orc_map;
+
+static double map_value(const orc_map *m, int64_t i)
 {
+    if (m->dtype == ORC_U8)
+        return m->q_offset + m->q_scale * (double)((const uint8_t *)m->data)[i];
+    return load_value(m->data, m->dtype, i);
+}
+
+/* Bilinear fetch of the first nch channels of a map at (u, v). */
+static void map_bilinear(const orc_map *m, int nch, double u, double v, double *out)
+{
+    const int R = m->R;
     double a = u * R - 0.5, b = v * R - 0.5;
     double fa = floor(a), fb = floor(b);
     double wa = a - fa, wb = b - fb;
@@ -201,13 +222,28 @@ void orc_tex_bilinear(const void *tex, int dtype, int R, int V, double u, double
     int ia[2] = {clampi(i0, 0, R - 1), clampi(i0 + 1, 0, R - 1)};
     int jb[2] = {clampi(j0, 0, R - 1), clampi(j0 + 1, 0, R - 1)};
     double w[2][2] = {{(1 - wa) * (1 - wb), wa * (1 - wb)}, {(1 - wa) * wb, wa * wb}};
-    for (int c = 0; c < V; ++c) {
+    for (int c = 0; c < nch; ++c) {
         double s = 0.0;
         for (int y = 0; y < 2; ++y)
             for (int x = 0; x < 2; ++x)
-                s += w[y][x] * load_value(tex, dtype, ((int64_t)jb[y] * R + ia[x]) * V + c);
+                s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * m->C + c);
         out[c] = s;
     }
+}
+
+/* Bilinear fetch of the V channels of an [R][R][V] texture at (u, v). */
+void orc_tex_bilinear(const void *tex, int dtype, int R, int V, double u, double v, double *out)
+{
+    orc_map m = {R, V, dtype, tex, 0.0, 0.0};
+    map_bilinear(&m, V, u, v, out);
+}
+
+/* The same for a map with C stored channels and 8-bit dequantisation. */
+void orc_map_bilinear(const void *data, int dtype, int R, int C, int nch, double q_scale,
+                      double q_offset, double u, double v, double *out)
+{
+    orc_map m = {R, C, dtype, data, q_scale, q_offset};
+    map_bilinear(&m, nch, u, v, out);
 }
 
 /* p_cali = p + S(m(p_t), d) d : the SH-weighted sum of the texture channels
@@ -221,6 +257,22 @@ void orc_calibrate(const double *p, const double *d, const double *m, int V, dou
         s += y[c] * m[c];
     for (int r = 0; r < 3; ++r)
         p_cali[r] = p[r] + s * d[r];
+}
+
+/* Eq. 2 as printed: p_cali = p + S(m_SH(p_t), d) * m_s(p_t), where the SH map
+ * holds, for each of the 3 axes, the coefficients of the first nb real
+ * harmonics of d (channel a*nb + v), and m_s is the scalar scale map. */
+void orc_calibrate_vec3(const double *p, const double *d, const double *m, int nb, double ms,
+                        double *p_cali)
+{
+    double y[64];
+    orc_sh_basis(nb, d, y);
+    for (int a = 0; a < 3; ++a) {
+        double s = 0.0;
+        for (int v = 0; v < nb; ++v)
+            s += y[v] * m[a * nb + v];
+        p_cali[a] = p[a] + s * ms;
+    }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -406,6 +458,13 @@ typedef struct {
     const uint16_t *weights; /* concatenated [in][out] fp16 */
     int K;
     double delta;
+    /* displacement form: 0 scalar along the ray (tex_V channels), 1 Eq. 2's
+     * vector times scale (3 (sh_degree+1)^2 channels + the scale map), 2 none */
+    int disp_mode;
+    int tex_C;               /* stored channels per texel (>= used) */
+    int sh_degree;
+    const void *scale;       /* [R][R] scale map (mode 1) */
+    double q_scale[2], q_offset[2]; /* 8-bit maps: [0] coefficients, [1] scale */
 } orc_scene;
 
 /* Steps 1-4 for one pixel.  Returns 0 for a miss (no samples).  x receives K
@@ -430,8 +489,21 @@ static int pixel_samples(const orc_scene *sc, int64_t pix, float *x, double *xd,
     double p[3], m[64], pc[3];
     for (int r = 0; r < 3; ++r)
         p[r] = o[r] + t * d[r];
-    orc_tex_bilinear(sc->tex, sc->tex_dtype, sc->tex_R, sc->tex_V, g[1], g[2], m);
-    orc_calibrate(p, d, m, sc->tex_V, pc);
+    orc_map coef = {sc->tex_R, sc->tex_C, sc->tex_dtype, sc->tex, sc->q_scale[0], sc->q_offset[0]};
+    if (sc->disp_mode == 0) {
+        map_bilinear(&coef, sc->tex_V, g[1], g[2], m);
+        orc_calibrate(p, d, m, sc->tex_V, pc);
+    } else if (sc->disp_mode == 1) {
+        int nb = (sc->sh_degree + 1) * (sc->sh_degree + 1);
+        orc_map sm = {sc->tex_R, 1, sc->tex_dtype, sc->scale, sc->q_scale[1], sc->q_offset[1]};
+        double ms;
+        map_bilinear(&coef, 3 * nb, g[1], g[2], m);
+        map_bilinear(&sm, 1, g[1], g[2], &ms);
+        orc_calibrate_vec3(p, d, m, nb, ms, pc);
+    } else {
+        for (int r = 0; r < 3; ++r)
+            pc[r] = p[r];
+    }
     for (int k = 0; k < sc->K; ++k) {
         double off = ((double)k - 0.5 * (double)(sc->K - 1)) * sc->delta;
         double q[3], xc[3];
@@ -482,7 +554,9 @@ int orc_render_pixels(const orc_scene *sc, int64_t n_pix, const int64_t *pix, do
                       int n_threads)
 {
     if (sc->widths[0] != sc->L * sc->F + sc->view_sh_dim || sc->tex_V > 64 ||
-        sc->view_sh_dim > 16 || sc->F > 16)
+        sc->view_sh_dim > 16 || sc->F > 16 || sc->sh_degree > 3 ||
+        (sc->disp_mode == 0 && sc->tex_C < sc->tex_V) ||
+        (sc->disp_mode == 1 && sc->tex_C < 3 * (sc->sh_degree + 1) * (sc->sh_degree + 1)))
         return -1;
 #ifdef _OPENMP
     if (n_threads < 1)

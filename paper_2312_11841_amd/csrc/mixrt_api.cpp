@@ -102,18 +102,42 @@ int check_gbuf(const mixrt_gbuffer *g, const mixrt_camera *cams, Msg m)
     return MIXRT_OK;
 }
 
+int disp_channels(const mixrt_disp_tex *d)
+{
+    if (d->mode == MIXRT_DISP_ALONG_RAY) return d->V;
+    if (d->mode == MIXRT_DISP_SH_VEC3) return 3 * (d->sh_degree + 1) * (d->sh_degree + 1);
+    return 0;
+}
+
+int stored_channels(const mixrt_disp_tex *d) { return d->C > 0 ? d->C : disp_channels(d); }
+
 int check_disp(const mixrt_disp_tex *d, Msg m)
 {
     if (!d) return vfail(m, MIXRT_EINVAL, "disp is NULL");
-    if (d->R < 1 || d->R > (1 << 15)) return vfail(m, MIXRT_EINVAL, "disp.R=%d", d->R);
-    if (d->V < 1 || d->V > MIXRT_MAX_TEX_CHANNELS)
-        return vfail(m, MIXRT_EUNSUPPORTED, "disp.V=%d outside 1..%d", d->V, MIXRT_MAX_TEX_CHANNELS);
-    if (d->dtype != MIXRT_F32 && d->dtype != MIXRT_F16)
-        return vfail(m, MIXRT_EUNSUPPORTED, "disp.dtype=%d (F32 or F16)", d->dtype);
-    if (d->mode != MIXRT_DISP_ALONG_RAY)
+    if (d->mode != MIXRT_DISP_ALONG_RAY && d->mode != MIXRT_DISP_SH_VEC3 &&
+        d->mode != MIXRT_DISP_NONE)
         return vfail(m, MIXRT_EUNSUPPORTED, "disp.mode=%d", d->mode);
+    if (d->mode == MIXRT_DISP_NONE) return MIXRT_OK;
+    if (d->R < 1 || d->R > (1 << 15)) return vfail(m, MIXRT_EINVAL, "disp.R=%d", d->R);
+    if (d->mode == MIXRT_DISP_ALONG_RAY && (d->V < 1 || d->V > MIXRT_MAX_TEX_CHANNELS))
+        return vfail(m, MIXRT_EUNSUPPORTED, "disp.V=%d outside 1..%d", d->V, MIXRT_MAX_TEX_CHANNELS);
+    if (d->mode == MIXRT_DISP_SH_VEC3 && (d->sh_degree < 0 || d->sh_degree > 3))
+        return vfail(m, MIXRT_EUNSUPPORTED, "disp.sh_degree=%d outside 0..3", d->sh_degree);
+    if (d->dtype != MIXRT_F32 && d->dtype != MIXRT_F16 && d->dtype != MIXRT_U8)
+        return vfail(m, MIXRT_EUNSUPPORTED, "disp.dtype=%d (F32, F16 or U8)", d->dtype);
+    if (d->C < 0 || stored_channels(d) < disp_channels(d) || stored_channels(d) > 256)
+        return vfail(m, MIXRT_EINVAL, "disp.C=%d for %d channels used", d->C, disp_channels(d));
+    if (mixrt::tex_id(d->dtype, d->mode, d->sh_degree) < 0)
+        return vfail(m, MIXRT_EUNSUPPORTED, "no kernel for disp dtype %d, mode %d, degree %d",
+                     d->dtype, d->mode, d->sh_degree);
     if (!d->data) return vfail(m, MIXRT_EINVAL, "disp.data is NULL");
     if (!aligned16(d->data)) return vfail(m, MIXRT_EINVAL, "disp.data not 16-byte aligned");
+    if (d->mode == MIXRT_DISP_SH_VEC3 && !d->scale)
+        return vfail(m, MIXRT_EINVAL, "disp.scale is NULL");
+    if (d->dtype == MIXRT_U8)
+        for (int i = 0; i < 2; ++i)
+            if (!std::isfinite(d->q_scale[i]) || !std::isfinite(d->q_offset[i]))
+                return vfail(m, MIXRT_EINVAL, "disp 8-bit dequantisation not finite");
     return MIXRT_OK;
 }
 
@@ -188,11 +212,13 @@ int validate_all(const mixrt_gbuffer *gbuf, const mixrt_camera *cams, const mixr
     if ((rc = check_sampling(smp, m))) return rc;
     if (!mlp) return vfail(m, MIXRT_EINVAL, "mlp is NULL");
     if ((rc = check_mlp(mlp, grid->L * grid->F + mlp->view_sh_dim, m, hid, nhid))) return rc;
-    if (!mixrt::render_variant_supported(disp->dtype == MIXRT_F16, grid->F,
-                                         grid->dtype == MIXRT_F16, mlp->width[0], *hid, *nhid))
+    const int tex = mixrt::tex_id(disp->dtype, disp->mode, disp->sh_degree);
+    if (!mixrt::render_variant_supported(tex, grid->F, grid->dtype == MIXRT_F16, mlp->width[0],
+                                         *hid, *nhid))
         return vfail(m, MIXRT_EUNSUPPORTED,
-                     "no render kernel for tex %s, grid F=%d %s, mlp %d->%dx%d->4",
-                     disp->dtype == MIXRT_F16 ? "f16" : "f32", grid->F,
+                     "no render kernel for disp (dtype %d, mode %d, degree %d), grid F=%d %s, "
+                     "mlp %d->%dx%d->4",
+                     disp->dtype, disp->mode, disp->sh_degree, grid->F,
                      grid->dtype == MIXRT_F16 ? "f16" : "f32", mlp->width[0], *hid, *nhid);
     return MIXRT_OK;
 }
@@ -206,9 +232,16 @@ void fill_ray_params(mixrt::RayParams &rp, const mixrt_gbuffer *g, const mixrt_c
     rp.W = g->W;
     rp.H = g->H;
     rp.rays = g->views * g->H * g->W;
-    rp.tex = d ? d->data : nullptr;
-    rp.tex_R = d ? d->R : 1;
-    rp.tex_V = d ? d->V : 0;
+    const bool none = d->mode == MIXRT_DISP_NONE;
+    rp.tex = none ? nullptr : d->data;
+    rp.tex_scale = none ? nullptr : d->scale;
+    rp.tex_R = none ? 1 : d->R;
+    rp.tex_V = d->mode == MIXRT_DISP_ALONG_RAY ? d->V : 0;
+    rp.tex_C = none ? 1 : stored_channels(d);
+    for (int i = 0; i < 2; ++i) {
+        rp.q_scale[i] = d->q_scale[i];
+        rp.q_offset[i] = d->q_offset[i];
+    }
     rp.K = s->K;
     rp.delta = s->delta;
     rp.t_term = s->t_term;
@@ -375,7 +408,7 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
     L.weights = (const _Float16 *)mlp->data;
     L.out = (float4 *)out_rgba;
     L.view_sh = mlp->view_sh_dim;
-    L.xf16 = disp->dtype == MIXRT_F16;
+    L.tex = mixrt::tex_id(disp->dtype, disp->mode, disp->sh_degree);
     L.tf16 = grid->dtype == MIXRT_F16;
     L.F = grid->F;
     L.in = mlp->width[0];
@@ -402,8 +435,9 @@ int mixrt_debug_ray_setup(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt
     mixrt::RayParams rp;
     fill_ray_params(rp, gbuf, cams, disp, smp);
     return finish_launch(ctx,
-                         mixrt::launch_ray_setup(rp, disp->dtype == MIXRT_F16, out_x, out_hit,
-                                                 ctx->stream),
+                         mixrt::launch_ray_setup(
+                             rp, mixrt::tex_id(disp->dtype, disp->mode, disp->sh_degree), out_x,
+                             out_hit, ctx->stream),
                          "ray_setup");
 }
 

@@ -39,8 +39,10 @@ struct RayParams {
     const float4 *g0;
     int32_t views, W, H;
     int32_t rays;           // views * H * W (< 2^31)
-    const void *tex;
-    int32_t tex_R, tex_V;
+    const void *tex;        // displacement coefficients [R][R][C]
+    const void *tex_scale;  // Eq. 2 scale map [R][R] (SH_VEC3)
+    int32_t tex_R, tex_V, tex_C;
+    float q_scale[2], q_offset[2];  // 8-bit dequantisation: coefficients, scale
     int32_t K;
     float delta;
     float t_term;
@@ -122,15 +124,38 @@ __device__ __forceinline__ void sh_basis(float x, float y, float z, float *Y)
 }
 
 // --------------------------------------------------------------------------
-// Eq. 2: bilinear fetch of the V texture channels at p_t (texel centres at
-// (i + 0.5)/R, clamp to edge), dotted with the SH basis of d: the signed
-// displacement length along the ray.
+// Eq. 2: the view-dependent displacement of the hit point.
+//
+// Texture kinds: element type (fp32, fp16 or 8-bit with an affine
+// dequantisation) and displacement form.  A texel's channels are read in
+// 16-byte chunks when texels are whole 16-byte lines, else element by
+// element.  Bilinear filtering (texel centres at (i + 0.5)/R, clamp to edge)
+// is done in fp32 on dequantised values.
 // --------------------------------------------------------------------------
-template <typename XT>
-__device__ __forceinline__ float displacement(const void *tex_, int R, int V, float u, float v,
-                                              float dx, float dy, float dz)
+enum DispMode { kDispAlongRay = 0, kDispShVec3 = 1, kDispNone = 2 };
+
+template <typename XT, int MODE, int DEG = 0>
+struct TexKind {
+    typedef XT T;
+    static constexpr int mode = MODE;
+    static constexpr int degree = DEG;
+    static constexpr int nb = (DEG + 1) * (DEG + 1);
+};
+
+__device__ __forceinline__ float tex_elem(float e, float, float) { return e; }
+__device__ __forceinline__ float tex_elem(_Float16 e, float, float) { return (float)e; }
+__device__ __forceinline__ float tex_elem(uint8_t e, float qs, float qo)
 {
-    const XT *tex = (const XT *)tex_;
+    return qo + qs * (float)e;
+}
+
+struct Bilinear {
+    int64_t t[4];   // element offsets of the 4 taps' texels (times C)
+    float w[4];
+};
+
+__device__ __forceinline__ Bilinear bilinear_taps(int R, int C, float u, float v)
+{
     float a = u * (float)R - 0.5f;
     float b = v * (float)R - 0.5f;
     // keep non-finite or far-out coordinates on the edge texels
@@ -143,45 +168,106 @@ __device__ __forceinline__ float displacement(const void *tex_, int R, int V, fl
     const int i0 = (int)fa, j0 = (int)fb;
     const int ia0 = min(max(i0, 0), R - 1), ia1 = min(max(i0 + 1, 0), R - 1);
     const int jb0 = min(max(j0, 0), R - 1), jb1 = min(max(j0 + 1, 0), R - 1);
-    const float w00 = (1.0f - wa) * (1.0f - wb), w01 = wa * (1.0f - wb);
-    const float w10 = (1.0f - wa) * wb, w11 = wa * wb;
-    const XT *t00 = tex + ((int64_t)jb0 * R + ia0) * V;
-    const XT *t01 = tex + ((int64_t)jb0 * R + ia1) * V;
-    const XT *t10 = tex + ((int64_t)jb1 * R + ia0) * V;
-    const XT *t11 = tex + ((int64_t)jb1 * R + ia1) * V;
+    Bilinear B;
+    B.t[0] = ((int64_t)jb0 * R + ia0) * C;
+    B.t[1] = ((int64_t)jb0 * R + ia1) * C;
+    B.t[2] = ((int64_t)jb1 * R + ia0) * C;
+    B.t[3] = ((int64_t)jb1 * R + ia1) * C;
+    B.w[0] = (1.0f - wa) * (1.0f - wb);
+    B.w[1] = wa * (1.0f - wb);
+    B.w[2] = (1.0f - wa) * wb;
+    B.w[3] = wa * wb;
+    return B;
+}
+
+// Filtered channels [c0, c0 + EPV) of one 16-byte chunk of every texel.
+template <typename XT>
+__device__ __forceinline__ void bilinear_chunk(const XT *tex, const Bilinear &B, int c0,
+                                               float qs, float qo, float *m)
+{
+    constexpr int EPV = 16 / (int)sizeof(XT);
+#pragma unroll
+    for (int e = 0; e < EPV; ++e) m[e] = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        XT e[EPV];
+        *(uint4 *)e = *(const uint4 *)(tex + B.t[k] + c0);
+#pragma unroll
+        for (int i = 0; i < EPV; ++i) m[i] += B.w[k] * tex_elem(e[i], qs, qo);
+    }
+}
+
+template <typename XT>
+__device__ __forceinline__ float bilinear_elem(const XT *tex, const Bilinear &B, int c, float qs,
+                                               float qo)
+{
+    float m = 0.0f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) m += B.w[k] * tex_elem(tex[B.t[k] + c], qs, qo);
+    return m;
+}
+
+// Offset p_cali - p for the ray direction d at texture coordinate (u, v).
+template <typename TK>
+__device__ __forceinline__ void displacement(const RayParams &p, float u, float v, float dx,
+                                             float dy, float dz, float &ox, float &oy, float &oz)
+{
+    typedef typename TK::T XT;
+    ox = oy = oz = 0.0f;
+    if (TK::mode == kDispNone) return;
+    constexpr int EPV = 16 / (int)sizeof(XT);
+    const XT *tex = (const XT *)p.tex;
+    const Bilinear B = bilinear_taps(p.tex_R, p.tex_C, u, v);
+    const float qs = p.q_scale[0], qo = p.q_offset[0];
+    const bool vec = ((p.tex_C * (int)sizeof(XT)) & 15) == 0;
     float Y[16];
     sh_basis<16>(dx, dy, dz, Y);
-    float s = 0.0f;
-    constexpr int EPV = 16 / (int)sizeof(XT);  // elements per 16-byte load
-    if (V % EPV == 0) {
-        // texels are whole 16-byte lines: one vector load per texel and chunk
+    if (TK::mode == kDispAlongRay) {
+        // s = sum_v Y_v(d) m_v over the first V channels; p_cali = p + s d
+        float s = 0.0f;
+        if (vec) {
 #pragma unroll
-        for (int c0 = 0; c0 < 16; c0 += EPV) {
-            if (c0 < V) {
-                XT e00[EPV], e01[EPV], e10[EPV], e11[EPV];
-                *(uint4 *)e00 = *(const uint4 *)(t00 + c0);
-                *(uint4 *)e01 = *(const uint4 *)(t01 + c0);
-                *(uint4 *)e10 = *(const uint4 *)(t10 + c0);
-                *(uint4 *)e11 = *(const uint4 *)(t11 + c0);
+            for (int c0 = 0; c0 < 16; c0 += EPV) {
+                if (c0 < p.tex_V) {
+                    float m[EPV];
+                    bilinear_chunk<XT>(tex, B, c0, qs, qo, m);
 #pragma unroll
-                for (int e = 0; e < EPV; ++e) {
-                    const float m = w00 * (float)e00[e] + w01 * (float)e01[e] +
-                                    w10 * (float)e10[e] + w11 * (float)e11[e];
-                    s += Y[c0 + e] * m;
+                    for (int e = 0; e < EPV && c0 + e < 16; ++e)
+                        if (c0 + e < p.tex_V) s += Y[c0 + e] * m[e];
                 }
             }
-        }
-    } else {
+        } else {
 #pragma unroll
-        for (int c = 0; c < 16; ++c) {
-            if (c < V) {
-                const float m = w00 * (float)t00[c] + w01 * (float)t01[c] + w10 * (float)t10[c] +
-                                w11 * (float)t11[c];
-                s += Y[c] * m;
-            }
+            for (int c = 0; c < 16; ++c)
+                if (c < p.tex_V) s += Y[c] * bilinear_elem<XT>(tex, B, c, qs, qo);
         }
+        ox = s * dx;
+        oy = s * dy;
+        oz = s * dz;
+    } else {
+        // Eq. 2 as printed: S_a = sum_v Y_v(d) m[a nb + v]; p_cali = p + m_s S
+        constexpr int NB = TK::nb, NCH = 3 * NB;
+        constexpr int NCHUNK = (NCH + EPV - 1) / EPV;
+        float m[NCHUNK * EPV];
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < NCHUNK; ++q) bilinear_chunk<XT>(tex, B, q * EPV, qs, qo, m + q * EPV);
+        } else {
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) m[c] = bilinear_elem<XT>(tex, B, c, qs, qo);
+        }
+        const Bilinear Bs = bilinear_taps(p.tex_R, 1, u, v);
+        const float ms =
+            bilinear_elem<XT>((const XT *)p.tex_scale, Bs, 0, p.q_scale[1], p.q_offset[1]);
+        float S[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int a = 0; a < 3; ++a)
+#pragma unroll
+            for (int vv = 0; vv < NB; ++vv) S[a] += Y[vv] * m[a * NB + vv];
+        ox = ms * S[0];
+        oy = ms * S[1];
+        oz = ms * S[2];
     }
-    return s;
 }
 
 // --------------------------------------------------------------------------
@@ -208,7 +294,7 @@ __device__ __forceinline__ void contract_to_cube(float qx, float qy, float qz, f
 
 // Steps before the grid for sample k of a ray: hit test, Eq. 2 calibration,
 // sample placement, contraction.  Returns false for a miss.
-template <typename XT>
+template <typename TK>
 __device__ __forceinline__ bool sample_position(const RayParams &p, const Ray &r, float4 g, int k,
                                                 float &x0, float &x1, float &x2)
 {
@@ -218,9 +304,11 @@ __device__ __forceinline__ bool sample_position(const RayParams &p, const Ray &r
         x0 = x1 = x2 = 0.0f;
         return false;
     }
-    const float s = displacement<XT>(p.tex, p.tex_R, p.tex_V, g.y, g.z, r.dx, r.dy, r.dz);
-    const float off = t + s + ((float)k - 0.5f * (float)(p.K - 1)) * p.delta;
-    contract_to_cube(r.ox + off * r.dx, r.oy + off * r.dy, r.oz + off * r.dz, x0, x1, x2);
+    float ox, oy, oz;
+    displacement<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, ox, oy, oz);
+    const float off = t + ((float)k - 0.5f * (float)(p.K - 1)) * p.delta;
+    contract_to_cube(r.ox + ox + off * r.dx, r.oy + oy + off * r.dy, r.oz + oz + off * r.dz, x0,
+                     x1, x2);
     return true;
 }
 

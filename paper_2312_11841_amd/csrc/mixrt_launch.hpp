@@ -10,22 +10,59 @@
 
 namespace mixrt {
 
+// Texture kinds the kernels are built for: (element type, displacement form,
+// SH degree of Eq. 2's vector form).
+enum TexId {
+    kTexF32Ray,
+    kTexF16Ray,
+    kTexU8Ray,
+    kTexF32Vec3D1,
+    kTexF16Vec3D2,
+    kTexU8Vec3D2,
+    kTexNone,
+};
+
+template <int ID>
+struct TexOf;
+template <> struct TexOf<kTexF32Ray> { typedef TexKind<float, kDispAlongRay> type; };
+template <> struct TexOf<kTexF16Ray> { typedef TexKind<_Float16, kDispAlongRay> type; };
+template <> struct TexOf<kTexU8Ray> { typedef TexKind<uint8_t, kDispAlongRay> type; };
+template <> struct TexOf<kTexF32Vec3D1> { typedef TexKind<float, kDispShVec3, 1> type; };
+template <> struct TexOf<kTexF16Vec3D2> { typedef TexKind<_Float16, kDispShVec3, 2> type; };
+template <> struct TexOf<kTexU8Vec3D2> { typedef TexKind<uint8_t, kDispShVec3, 2> type; };
+template <> struct TexOf<kTexNone> { typedef TexKind<float, kDispNone> type; };
+
+// dtype: 0 f32, 1 f16, 2 u8 (mixrt_dtype); mode: mixrt_disp_mode.  -1 when
+// no kernel is built for the combination.
+inline int tex_id(int dtype, int mode, int degree)
+{
+    if (mode == kDispNone) return kTexNone;
+    if (mode == kDispAlongRay) return dtype == 0 ? kTexF32Ray : dtype == 1 ? kTexF16Ray : kTexU8Ray;
+    if (mode == kDispShVec3) {
+        if (dtype == 0 && degree == 1) return kTexF32Vec3D1;
+        if (dtype == 1 && degree == 2) return kTexF16Vec3D2;
+        if (dtype == 2 && degree == 2) return kTexU8Vec3D2;
+    }
+    return -1;
+}
+
 struct RenderLaunch {
     RayParams rp;
     GridParams gp;
     const _Float16 *weights;
     float4 *out;
     int view_sh;
-    bool xf16, tf16;
+    int tex;          // TexId
+    bool tf16;
     int F, in, hid, nhid;
     int cus;
 };
 
-bool render_variant_supported(bool xf16, int F, bool tf16, int in, int hid, int nhid);
+bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid);
 bool mlp_variant_supported(int in, int hid, int nhid);
 
 hipError_t launch_render(const RenderLaunch &L, hipStream_t stream);
-hipError_t launch_ray_setup(const RayParams &rp, bool xf16, float *out_x, int32_t *out_hit,
+hipError_t launch_ray_setup(const RayParams &rp, int tex, float *out_x, int32_t *out_hit,
                             hipStream_t stream);
 hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const float *x, int64_t n,
                               int32_t *oc, uint32_t *oi, float *ow, float *of, hipStream_t stream);

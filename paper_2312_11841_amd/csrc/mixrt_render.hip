@@ -30,12 +30,12 @@ __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, floa
     }
 }
 
-template <bool XF16, int F, bool TF16, int IN, int HID, int NHID>
+template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
                                                         const _Float16 *__restrict__ weights,
                                                         int view_sh, float4 *__restrict__ out)
 {
-    typedef typename std::conditional<XF16, _Float16, float>::type XT;
+    typedef typename TexOf<TEX>::type TK;
     constexpr int LD = IN + 8;  // padded row of MLP inputs (halves), 16-byte multiple
     __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][kWave * LD];
     __shared__ float4 s_out[kWavesPerBlock][kWave];
@@ -69,7 +69,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         Ray ry = {};
         if (valid) {
             ry = pixel_ray(rp, ray);
-            hit = sample_position<XT>(rp, ry, rp.g0[ray], k, x0, x1, x2);
+            hit = sample_position<TK>(rp, ry, rp.g0[ray], k, x0, x1, x2);
         }
         // --- hash encoding, features to LDS as fp16: dense levels first (pair
         // loads), then hashed levels, kLevelGroup levels per batch of loads
@@ -128,18 +128,26 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
 }
 
 
-#define MIXRT_RENDER_VARIANTS(X)      \
-    X(false, 2, false, 16, 32, 1)     \
-    X(false, 2, false, 32, 32, 1)     \
-    X(true, 2, true, 48, 64, 2)       \
-    X(true, 2, true, 32, 64, 2)       \
-    X(true, 4, true, 32, 64, 2)       \
-    X(true, 4, true, 16, 64, 2)
+// Built render kernels: (texture kind, F, fp16 table, MLP in, hidden, hidden layers).
+#define MIXRT_RENDER_VARIANTS(X)                \
+    X(kTexF32Ray, 2, false, 16, 32, 1)          \
+    X(kTexF32Ray, 2, false, 32, 32, 1)          \
+    X(kTexF16Ray, 2, true, 48, 64, 2)           \
+    X(kTexF16Ray, 2, true, 32, 64, 2)           \
+    X(kTexF16Ray, 4, true, 32, 64, 2)           \
+    X(kTexF16Ray, 4, true, 16, 64, 2)           \
+    X(kTexU8Vec3D2, 4, true, 32, 64, 2)         \
+    X(kTexF16Vec3D2, 4, true, 32, 64, 2)        \
+    X(kTexF32Vec3D1, 2, false, 16, 32, 1)       \
+    X(kTexU8Ray, 2, false, 16, 32, 1)           \
+    X(kTexNone, 2, false, 16, 32, 1)            \
+    X(kTexNone, 2, true, 48, 64, 2)             \
+    X(kTexNone, 4, true, 32, 64, 2)
 
-bool render_variant_supported(bool xf16, int F, bool tf16, int in, int hid, int nhid)
+bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid)
 {
 #define X(a, b, c, d, e, f) \
-    if (xf16 == a && F == b && tf16 == c && in == d && hid == e && nhid == f) return true;
+    if (tex == a && F == b && tf16 == c && in == d && hid == e && nhid == f) return true;
     MIXRT_RENDER_VARIANTS(X)
 #undef X
     return false;
@@ -151,7 +159,7 @@ hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
     const int64_t n_tiles = ((int64_t)L.rp.rays + R - 1) / R;
     const int64_t want = (n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
 #define X(a, b, c, d, e, f)                                                                    \
-    if (L.xf16 == a && L.F == b && L.tf16 == c && L.in == d && L.hid == e && L.nhid == f) {     \
+    if (L.tex == a && L.F == b && L.tf16 == c && L.in == d && L.hid == e && L.nhid == f) {      \
         auto fn = render_kernel<a, b, c, d, e, f>;                                             \
         static int resident = 0; /* blocks resident on the whole device */                    \
         if (!resident) resident = resident_blocks((const void *)fn, L.cus);                    \

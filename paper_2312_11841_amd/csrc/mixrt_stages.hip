@@ -5,11 +5,11 @@
 
 namespace mixrt {
 
-template <bool XF16>
+template <int TEX>
 __global__ __launch_bounds__(kBlock) void ray_setup_kernel(RayParams rp, float *__restrict__ out_x,
                                                            int32_t *__restrict__ out_hit)
 {
-    typedef typename std::conditional<XF16, _Float16, float>::type XT;
+    typedef typename TexOf<TEX>::type TK;
     const int64_t idx = (int64_t)blockIdx.x * kBlock + threadIdx.x;
     const int64_t n = (int64_t)rp.rays * rp.K;
     if (idx >= n) return;
@@ -17,7 +17,7 @@ __global__ __launch_bounds__(kBlock) void ray_setup_kernel(RayParams rp, float *
     const int k = (int)(idx - (int64_t)ray * rp.K);
     const Ray ry = pixel_ray(rp, ray);
     float x0, x1, x2;
-    const bool hit = sample_position<XT>(rp, ry, rp.g0[ray], k, x0, x1, x2);
+    const bool hit = sample_position<TK>(rp, ry, rp.g0[ray], k, x0, x1, x2);
     out_x[idx * 3 + 0] = x0;
     out_x[idx * 3 + 1] = x1;
     out_x[idx * 3 + 2] = x2;
@@ -119,17 +119,22 @@ bool mlp_variant_supported(int in, int hid, int nhid)
     return false;
 }
 
-hipError_t launch_ray_setup(const RayParams &rp, bool xf16, float *out_x, int32_t *out_hit,
+hipError_t launch_ray_setup(const RayParams &rp, int tex, float *out_x, int32_t *out_hit,
                             hipStream_t stream)
 {
     const int64_t n = (int64_t)rp.rays * rp.K;
     if (n == 0) return hipSuccess;
     const dim3 grid((unsigned)((n + kBlock - 1) / kBlock));
-    if (xf16)
-        hipLaunchKernelGGL(ray_setup_kernel<true>, grid, dim3(kBlock), 0, stream, rp, out_x, out_hit);
-    else
-        hipLaunchKernelGGL(ray_setup_kernel<false>, grid, dim3(kBlock), 0, stream, rp, out_x,
-                           out_hit);
+#define T(ID)                                                                                  \
+    case ID:                                                                                   \
+        hipLaunchKernelGGL(ray_setup_kernel<ID>, grid, dim3(kBlock), 0, stream, rp, out_x, out_hit); \
+        break;
+    switch (tex) {
+        T(kTexF32Ray) T(kTexF16Ray) T(kTexU8Ray) T(kTexF32Vec3D1) T(kTexF16Vec3D2) T(kTexU8Vec3D2)
+        T(kTexNone)
+    default: return hipErrorInvalidValue;
+    }
+#undef T
     return hipGetLastError();
 }
 

@@ -22,7 +22,8 @@ MIXRT_ENOMEM = -2
 MIXRT_EDEVICE = -3
 MIXRT_EUNSUPPORTED = -4
 MIXRT_F32, MIXRT_F16, MIXRT_U8 = 0, 1, 2
-MIXRT_DISP_ALONG_RAY = 0
+MIXRT_DISP_ALONG_RAY, MIXRT_DISP_SH_VEC3, MIXRT_DISP_NONE = 0, 1, 2
+_DISP = {"ray": MIXRT_DISP_ALONG_RAY, "vec3": MIXRT_DISP_SH_VEC3, "none": MIXRT_DISP_NONE}
 MIXRT_FLAG_SYNC_CHECK = 1
 MAX_VIEWS, MAX_LEVELS, MAX_LAYERS = 16, 32, 8
 
@@ -62,7 +63,8 @@ class Camera(C.Structure):
 
 class DispTex(C.Structure):
     _fields_ = [("R", C.c_int32), ("V", C.c_int32), ("dtype", C.c_int32), ("mode", C.c_int32),
-                ("data", C.c_void_p)]
+                ("data", C.c_void_p), ("C", C.c_int32), ("sh_degree", C.c_int32),
+                ("scale", C.c_void_p), ("q_scale", C.c_float * 2), ("q_offset", C.c_float * 2)]
 
 
 class HashGrid(C.Structure):
@@ -132,7 +134,7 @@ def _ptr(t) -> int:
 
 # --- descriptors from scene data -------------------------------------------------
 
-_DT = {"float32": MIXRT_F32, "float16": MIXRT_F16}
+_DT = {"float32": MIXRT_F32, "float16": MIXRT_F16, "uint8": MIXRT_U8}
 
 
 def _dtype_code(t) -> int:
@@ -176,6 +178,7 @@ class DeviceScene:
 
     g0: object
     tex: object
+    scale: object
     table: object
     weights: object
     cams: object
@@ -192,15 +195,25 @@ class DeviceScene:
         cfg = scene.cfg
         g0 = torch.from_numpy(np.ascontiguousarray(scene.g0)).to(device)
         tex = torch.from_numpy(np.ascontiguousarray(scene.tex)).to(device)
+        scale = (None if scene.scale is None
+                 else torch.from_numpy(np.ascontiguousarray(scene.scale)).to(device))
         table = torch.from_numpy(np.ascontiguousarray(scene.table)).to(device)
         weights = torch.from_numpy(scene.weights_flat.view(np.uint16).astype(np.int16)).to(device)
         gbuf = GBuffer(cfg.views, cfg.W, cfg.rows_kept, _ptr(g0), 0)
-        disp = DispTex(cfg.tex_R, cfg.tex_V, _dtype_code(tex), MIXRT_DISP_ALONG_RAY, _ptr(tex))
+        disp = DispTex()
+        disp.R, disp.V, disp.dtype = cfg.tex_R, cfg.tex_V, _dtype_code(tex)
+        disp.mode = _DISP[cfg.disp]
+        disp.data = _ptr(tex)
+        disp.C = scene.tex.shape[2]
+        disp.sh_degree = cfg.sh_degree
+        disp.scale = _ptr(scale)
+        disp.q_scale[:] = [float(q) for q in scene.q_scale]
+        disp.q_offset[:] = [float(q) for q in scene.q_offset]
         grid = make_grid(table, cfg.N_min, cfg.N_max)
         mlp = make_mlp(weights, cfg.widths, cfg.view_sh_dim)
         smp = make_sampling(cfg.K, cfg.delta, cfg.t_term)
-        return cls(g0, tex, table, weights, make_cameras(scene.cams), gbuf, disp, grid, mlp,
-                   smp, cfg.rays)
+        return cls(g0, tex, scale, table, weights, make_cameras(scene.cams), gbuf, disp, grid,
+                   mlp, smp, cfg.rays)
 
 
 # --- the library handle ------------------------------------------------------------

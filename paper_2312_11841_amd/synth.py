@@ -68,6 +68,10 @@ class SceneConfig:
     head_scale: float = 1.0   # multiplies the output-layer weights
     bg: tuple = (0.0, 0.0, 0.0)
     rows: int = 0             # >0: keep only the first `rows` image rows
+    disp: str = "ray"         # "ray": scalar along the ray; "vec3": Eq. 2 as
+                              # printed (SH vector x scale map); "none"
+    sh_degree: int = 0        # "vec3": SH degree D, 3 (D+1)^2 channels
+    scale_range: tuple = (0.0, 1.0)  # "vec3": scale map values
 
     @property
     def T(self) -> int:
@@ -84,6 +88,21 @@ class SceneConfig:
     @property
     def samples(self) -> int:
         return self.rays * self.K
+
+    @property
+    def tex_channels(self) -> int:
+        """Channels the displacement form reads."""
+        if self.disp == "vec3":
+            return 3 * (self.sh_degree + 1) ** 2
+        return self.tex_V if self.disp == "ray" else 0
+
+    @property
+    def tex_C(self) -> int:
+        """Stored channels per texel: the used ones padded to 16-byte texels."""
+        eb = {"f32": 4, "f16": 2, "u8": 1}[self.tex_dtype]
+        per = 16 // eb
+        n = max(self.tex_channels, 1)
+        return n if self.disp == "ray" else -(-n // per) * per
 
     def replace(self, **kw) -> "SceneConfig":
         return dataclasses.replace(self, **kw)
@@ -127,12 +146,32 @@ def sweep_config(rays: int, K: int, dense: bool = False) -> SceneConfig:
 
 # The deployed grid of the paper's implementation details: four levels,
 # resolution 256 to 4096, 2^21 entries of four features, one query per pixel.
-DEPLOYED720P = VIEW720P.replace(name="deployed720p", K=1, L=4, log2_T=21, F=4,
+# With one query per pixel the density saturates (delta = 10), so the pixel
+# is the MLP's colour, as in the paper's pipeline.
+DEPLOYED720P = VIEW720P.replace(name="deployed720p", K=1, delta=10.0, L=4, log2_T=21, F=4,
                                 N_min=256, N_max=4096, widths=(32, 64, 64, 4),
                                 seed=5)
 
+# The paper's deployed configuration with Eq. 2 as printed: SH degree 2
+# displacement vectors (27 channels, stored in 32-byte texels) times a scale
+# map, both 8-bit at R_m = 1536 (Sec. 4.3.2, Sec. 5.1.2), the deployed grid,
+# one query per pixel.  Features and weights large enough for a structured
+# frame (rgb over ~[0.3, 0.6]) while the fp16 MLP inputs stay well inside the
+# frame tolerance.
+PAPER720P = DEPLOYED720P.replace(name="paper720p", tex_R=1536, tex_dtype="u8", disp="vec3",
+                                 sh_degree=2, tex_range=0.05, scale_range=(0.0, 1.0),
+                                 table_range=0.5, w_std=0.2, head_scale=1.0,
+                                 bg=(0.2, 0.4, 0.6), seed=6)
+
+# Tiny workloads for the other displacement forms (CPU-checkable).
+TINY64_VEC3 = TINY64_DENSE.replace(name="tiny64_vec3", disp="vec3", sh_degree=1,
+                                   tex_range=0.2, seed=13)
+TINY64_U8 = TINY64_DENSE.replace(name="tiny64_u8", tex_dtype="u8", tex_range=0.3, seed=14)
+TINY64_NODISP = TINY64_DENSE.replace(name="tiny64_nodisp", disp="none", seed=15)
+
 CONFIGS = {c.name: c for c in (TINY64, TINY64_DENSE, VIEW720P, VIEW720P_DENSE,
-                               BATCH8X1080P, DEPLOYED720P)}
+                               BATCH8X1080P, DEPLOYED720P, PAPER720P, TINY64_VEC3,
+                               TINY64_U8, TINY64_NODISP)}
 
 
 # --- scene container ----------------------------------------------------------
@@ -143,9 +182,12 @@ class Scene:
     g0: np.ndarray            # [views, rows, W, 4] f32: (t, u, v, 0)
     g1: np.ndarray            # [views, rows, W, 4] f32: (nx, ny, nz, 0)
     cams: np.ndarray          # [views, 16] f32: c2w row-major 3x4, fov_y_deg, bg rgb
-    tex: np.ndarray           # [R, R, V] f32/f16
+    tex: np.ndarray           # [R, R, C] f32/f16/u8 (C stored channels)
     table: np.ndarray         # [L, T, F] f32/f16
     weights: list             # per layer [in, out] f16
+    scale: np.ndarray = None  # [R, R] scale map ("vec3"), same dtype as tex
+    q_scale: tuple = (0.0, 0.0)   # 8-bit maps: value = q_offset + q_scale * q
+    q_offset: tuple = (0.0, 0.0)  # ([0] coefficient map, [1] scale map)
     extra: dict = field(default_factory=dict)
 
     @property
@@ -154,7 +196,8 @@ class Scene:
 
     def digest(self) -> str:
         h = hashlib.sha256()
-        for a in (self.g0, self.g1, self.cams, self.tex, self.table, self.weights_flat):
+        for a in (self.g0, self.g1, self.cams, self.tex, self.table, self.weights_flat,
+                  self.scale if self.scale is not None else np.zeros(0)):
             h.update(np.ascontiguousarray(a).tobytes())
         return h.hexdigest()
 
@@ -294,8 +337,20 @@ def make_scene(cfg: SceneConfig) -> Scene:
     else:
         g0, g1 = _room_gbuffer(cfg, rng)
     cams = _camera_rows(cfg, rng)
-    tex = rng.uniform(-cfg.tex_range, cfg.tex_range,
-                      (cfg.tex_R, cfg.tex_R, cfg.tex_V)).astype(_NP_DT[cfg.tex_dtype])
+    shape = (cfg.tex_R, cfg.tex_R, cfg.tex_C)
+    q_scale, q_offset = (0.0, 0.0), (0.0, 0.0)
+    scale = None
+    if cfg.tex_dtype == "u8":
+        lo, hi = cfg.scale_range
+        q_scale = (2.0 * cfg.tex_range / 255.0, (hi - lo) / 255.0)
+        q_offset = (-cfg.tex_range, lo)
+        tex = rng.integers(0, 256, shape, dtype=np.uint8)
+        if cfg.disp == "vec3":
+            scale = rng.integers(0, 256, shape[:2], dtype=np.uint8)
+    else:
+        tex = rng.uniform(-cfg.tex_range, cfg.tex_range, shape).astype(_NP_DT[cfg.tex_dtype])
+        if cfg.disp == "vec3":
+            scale = rng.uniform(*cfg.scale_range, shape[:2]).astype(_NP_DT[cfg.tex_dtype])
     table = rng.uniform(-cfg.table_range, cfg.table_range,
                         (cfg.L, cfg.T, cfg.F)).astype(np.float32)
     table = table.astype(_NP_DT[cfg.table_dtype])
@@ -309,7 +364,9 @@ def make_scene(cfg: SceneConfig) -> Scene:
         weights.append(w.astype(np.float16))
     return Scene(cfg=cfg, g0=np.ascontiguousarray(g0), g1=np.ascontiguousarray(g1),
                  cams=cams, tex=np.ascontiguousarray(tex),
-                 table=np.ascontiguousarray(table), weights=weights)
+                 table=np.ascontiguousarray(table), weights=weights,
+                 scale=None if scale is None else np.ascontiguousarray(scale),
+                 q_scale=q_scale, q_offset=q_offset)
 
 
 def dtype_code(name: str) -> int:

@@ -82,8 +82,15 @@ class _Desc:
         cams[:, [0, 5, 10]] = 1.0
         cams[:, 12] = 60.0
         self.cams = mixrt.make_cameras(cams)
-        self.disp = mixrt.DispTex(cfg.tex_R, cfg.tex_V, synth.dtype_code(cfg.tex_dtype),
-                                  0, FAKE)
+        self.disp = mixrt.DispTex()
+        self.disp.R, self.disp.V = cfg.tex_R, cfg.tex_V
+        self.disp.dtype = synth.dtype_code(cfg.tex_dtype)
+        self.disp.mode = {"ray": 0, "vec3": 1, "none": 2}[cfg.disp]
+        self.disp.data = FAKE
+        self.disp.C = cfg.tex_C
+        self.disp.sh_degree = cfg.sh_degree
+        self.disp.scale = FAKE if cfg.disp == "vec3" else 0
+        self.disp.q_scale[:] = [0.01, 0.01]
         self.grid = mixrt.HashGrid(cfg.L, cfg.log2_T, cfg.F, cfg.N_min, cfg.N_max,
                                    synth.dtype_code(cfg.table_dtype), FAKE)
         self.mlp = mixrt.Mlp()
@@ -116,8 +123,16 @@ BAD = [
     ("c2w nan", lambda d: d.cams[0].c2w.__setitem__(3, float("nan")), mixrt.MIXRT_EINVAL),
     ("disp.V", lambda d: setattr(d.disp, "V", 17), mixrt.MIXRT_EUNSUPPORTED),
     ("disp.R", lambda d: setattr(d.disp, "R", 0), mixrt.MIXRT_EINVAL),
-    ("disp.dtype", lambda d: setattr(d.disp, "dtype", 2), mixrt.MIXRT_EUNSUPPORTED),
-    ("disp.mode", lambda d: setattr(d.disp, "mode", 1), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.dtype", lambda d: setattr(d.disp, "dtype", 3), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.mode", lambda d: setattr(d.disp, "mode", 3), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.vec3 degree unbuilt", lambda d: setattr(d.disp, "mode", 1), mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.vec3 degree 4", lambda d: (setattr(d.disp, "mode", 1), setattr(d.disp, "sh_degree", 4)),
+     mixrt.MIXRT_EUNSUPPORTED),
+    ("disp.vec3 no scale", lambda d: (setattr(d.disp, "mode", 1), setattr(d.disp, "sh_degree", 2),
+                                      setattr(d.disp, "C", 32)), mixrt.MIXRT_EINVAL),
+    ("disp.C too small", lambda d: setattr(d.disp, "C", 4), mixrt.MIXRT_EINVAL),
+    ("disp.u8 nan", lambda d: (setattr(d.disp, "dtype", 2), d.disp.q_scale.__setitem__(0, float("nan"))),
+     mixrt.MIXRT_EINVAL),
     ("disp.data", lambda d: setattr(d.disp, "data", 0), mixrt.MIXRT_EINVAL),
     ("grid.L", lambda d: setattr(d.grid, "L", 33), mixrt.MIXRT_EUNSUPPORTED),
     ("grid.log2_T", lambda d: setattr(d.grid, "log2_T", 27), mixrt.MIXRT_EUNSUPPORTED),
@@ -138,6 +153,8 @@ BAD = [
     ("delta", lambda d: setattr(d.smp, "delta", -1.0), mixrt.MIXRT_EINVAL),
     ("t_term", lambda d: setattr(d.smp, "t_term", 1.0), mixrt.MIXRT_EINVAL),
     ("unbuilt variant", lambda d: setattr(d.disp, "dtype", 0), mixrt.MIXRT_EUNSUPPORTED),
+    ("no map needs no data", lambda d: (setattr(d.disp, "mode", 2), setattr(d.disp, "data", 0),
+                                        setattr(d.disp, "R", 0)), mixrt.MIXRT_OK),
 ]
 
 
@@ -147,7 +164,7 @@ def test_validate_rejects(name, mutate, code):
     mutate(d)
     rc, msg = d.validate()
     assert rc == code, (rc, msg)
-    assert msg
+    assert bool(msg) == (code != mixrt.MIXRT_OK)
 
 
 def test_validate_null_descriptors():

@@ -101,7 +101,8 @@ def test_hash_encode_empty_and_single(R):
 # Ray setup: positions fed to the grid; their indices must equal the oracle's
 # --------------------------------------------------------------------------
 
-RAY_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.DEPLOYED720P]
+RAY_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.DEPLOYED720P,
+            synth.PAPER720P, synth.TINY64_VEC3, synth.TINY64_U8, synth.TINY64_NODISP]
 
 
 @pytest.mark.parametrize("cfg", RAY_CFGS, ids=lambda c: c.name)
@@ -216,7 +217,8 @@ def _frame_pixels(cfg, rng, n):
 
 
 FRAME_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.VIEW720P_DENSE,
-              synth.DEPLOYED720P]
+              synth.DEPLOYED720P, synth.PAPER720P, synth.TINY64_VEC3, synth.TINY64_U8,
+              synth.TINY64_NODISP]
 
 
 @pytest.mark.parametrize("cfg", FRAME_CFGS, ids=lambda c: c.name)

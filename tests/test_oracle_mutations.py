@@ -33,6 +33,11 @@ MUTATIONS = {
     "calibration_sign": ("p_cali[r] = p[r] + s * d[r];", "p_cali[r] = p[r] - s * d[r];"),
     "corner_clamp": ("c0[a] = c < 0 ? 0 : (c > N - 1 ? N - 1 : c);", "c0[a] = c < 0 ? 0 : (c > N ? N : c);"),
     "subnormal_exp": ("v = ldexp((double)mant, -24);", "v = ldexp((double)mant, -25);"),
+    "vec3_axis_stride": ("s += y[v] * m[a * nb + v];", "s += y[v] * m[v * 3 + a];"),
+    "u8_offset": ("return m->q_offset + m->q_scale * (double)((const uint8_t *)m->data)[i];",
+                  "return m->q_scale * (double)((const uint8_t *)m->data)[i];"),
+    "stored_channels": ("s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * m->C + c);",
+                        "s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * nch + c);"),
     "no_background": ("out[4 * r + ch] = c[ch] + Tend * bg[3 * r + ch];", "out[4 * r + ch] = c[ch];"),
 }
 

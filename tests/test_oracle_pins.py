@@ -522,3 +522,92 @@ def test_constant_field_reduces_to_one_mlp_query():
     out = oracle.OracleScene(sc).render_pixels(np.arange(0, cfg.rays, 97))
     assert np.allclose(out[:, :3], scipy.special.expit(o[1:]), atol=1e-12)
     assert np.allclose(out[:, 3], 1.0)
+
+
+# --------------------------------------------------------------------------
+# Eq. 2 as printed (SH vector x scale map), 8-bit maps, no displacement
+# --------------------------------------------------------------------------
+
+def test_u8_map_is_dequantised_affinely():
+    R = 8
+    jj, ii = np.mgrid[0:R, 0:R]
+    q = (3 + 2 * ii + 5 * jj + ii * jj).astype(np.uint8)[..., None]   # bilinear in (i, j)
+    qs, qo = 0.01, -0.7
+    rng = np.random.default_rng(20)
+    for _ in range(50):
+        u, v = rng.uniform(0.5 / R, 1 - 0.5 / R, 2)
+        a, b = u * R - 0.5, v * R - 0.5
+        ref = qo + qs * (3 + 2 * a + 5 * b + a * b)
+        assert oracle.map_bilinear(q, 1, u, v, qs, qo)[0] == pytest.approx(ref, abs=1e-12)
+    # texel centre: exactly q_offset + q_scale * q
+    assert oracle.map_bilinear(q, 1, 2.5 / R, 5.5 / R, qs, qo)[0] == pytest.approx(
+        qo + qs * float(q[5, 2, 0]), abs=1e-15)
+
+
+def test_padding_channels_are_ignored():
+    rng = np.random.default_rng(21)
+    used = rng.uniform(-1, 1, (6, 6, 12)).astype(np.float32)
+    padded = np.concatenate([used, rng.uniform(-9, 9, (6, 6, 4)).astype(np.float32)], -1)
+    for _ in range(20):
+        u, v = rng.uniform(-0.1, 1.1, 2)
+        assert np.array_equal(oracle.map_bilinear(used, 12, u, v),
+                              oracle.map_bilinear(padded, 12, u, v))
+
+
+def test_vector_calibration_axis_by_axis():
+    p = np.array([0.5, -0.25, 1.0])
+    d = np.array([0.6, 0.0, -0.8])
+    for D in range(4):
+        nb = (D + 1) ** 2
+        Y = oracle.sh_basis(nb, d)[0]
+        assert np.array_equal(oracle.calibrate_vec3(p, d, np.zeros(3 * nb), nb, 0.7), p)
+        for a in range(3):
+            for v in range(nb):
+                m = np.zeros(3 * nb)
+                m[a * nb + v] = 0.4
+                step = np.zeros(3)
+                step[a] = 0.7 * 0.4 * Y[v]
+                assert np.allclose(oracle.calibrate_vec3(p, d, m, nb, 0.7) - p, step, atol=1e-15)
+        # the scale map scales the whole vector
+        m = np.random.default_rng(D).uniform(-1, 1, 3 * nb)
+        a1 = oracle.calibrate_vec3(p, d, m, nb, 1.0) - p
+        assert np.allclose(oracle.calibrate_vec3(p, d, m, nb, 0.25) - p, 0.25 * a1, atol=1e-15)
+        # constant band only: a view-independent offset Y_00 * m_s * c
+        m = np.zeros(3 * nb)
+        m[[0, nb, 2 * nb]] = [0.3, -0.2, 0.1]
+        off = oracle.calibrate_vec3(p, d, m, nb, 0.5) - p
+        assert np.allclose(off, 0.5 * 0.5 / np.sqrt(np.pi) * np.array([0.3, -0.2, 0.1]),
+                           atol=1e-15)
+
+
+def test_displacement_forms_agree_when_the_maps_vanish():
+    base = synth.TINY64_DENSE.replace(H=16, W=16)
+    pix = np.arange(256)
+    zero_ray = synth.make_scene(base)
+    zero_ray.tex[...] = 0
+    ref = oracle.OracleScene(zero_ray).render_pixels(pix)
+    none = synth.make_scene(base.replace(disp="none"))
+    assert np.array_equal(oracle.OracleScene(none).render_pixels(pix), ref)
+    vec = synth.make_scene(base.replace(disp="vec3", sh_degree=2))
+    vec.g0, vec.table, vec.weights = zero_ray.g0, zero_ray.table, zero_ray.weights
+    vec.scale[...] = 0                      # zero scale: no displacement
+    assert np.array_equal(oracle.OracleScene(vec).render_pixels(pix), ref)
+
+
+def test_samples_follow_the_vector_displacement():
+    # inside the unit ball the cube map is affine, so the mean sample is
+    # o + t d + m_s * S(m_SH, d): check it on a constant-band map
+    cfg = synth.TINY64.replace(name="vecpin", H=8, W=8, K=3, delta=0.01, tex_R=4,
+                               disp="vec3", sh_degree=1, L=2, log2_T=12, widths=(4, 16, 4))
+    sc = synth.make_scene(cfg)
+    sc.g0[..., 0] = 0.5
+    sc.tex[...] = 0
+    nb = 4
+    sc.tex[..., 0], sc.tex[..., nb], sc.tex[..., 2 * nb] = 0.2, -0.1, 0.3
+    sc.scale[...] = 0.5
+    _, xd, _ = oracle.OracleScene(sc).pixel_samples(np.arange(cfg.rays))
+    off = 0.5 * 0.5 / np.sqrt(np.pi) * np.array([0.2, -0.1, 0.3])
+    for q in range(cfg.rays):
+        j, i = divmod(q, cfg.W)
+        o, d = oracle.camera_ray(sc.cams[0], cfg.W, cfg.H, i, j)
+        assert np.allclose(_uncube(xd[q]).mean(0), o + 0.5 * d + off, atol=1e-7)
