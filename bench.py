@@ -131,6 +131,52 @@ def cpu_baseline(scene, budget_s: float):
                       f"({dt:.1f} s wall, OpenMP over pixels)"}
 
 
+# The paper's profiling points (FPS at 1280x720 on a MacBook M1 Pro in WebGL,
+# one query per pixel): Tab. 3 (levels, table size, MLP) and Tab. 6 (with and
+# without the displacement map).  Context only: other hardware.
+PAPER_FPS = {"tab3_L8_T17_mlp": 27, "tab3_L8_T17": 30, "tab3_L1_T17": 120, "tab3_L8_T5": 35,
+             "tab3_L8_T22": 25, "paper720p": 31, "paper720p_novdd": 35}
+
+
+def time_workload(cfg, steps, warmup):
+    import torch
+    from paper_2312_11841_amd import mixrt, synth
+    scene = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(scene, "cuda:0")
+    out = torch.empty((cfg.rays, 4), dtype=torch.float32, device="cuda:0")
+    stream = torch.cuda.current_stream()
+    r = mixrt.Renderer(0, stream=stream)
+    for _ in range(warmup):
+        r.render(ds, out)
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(steps):
+        r.render(ds, out)
+    b.record(stream)
+    torch.cuda.synchronize()
+    r.close()
+    return a.elapsed_time(b) / steps
+
+
+def paper_tables(steps, warmup):
+    """Tab. 3 and Tab. 6 of the paper re-run on this GPU, plus a level sweep."""
+    from paper_2312_11841_amd import synth
+    rows = []
+    for cfg in synth.TABLE3 + synth.LEVEL_SWEEP + [synth.PAPER720P, synth.PAPER720P_NOVDD]:
+        if any(r["workload"] == cfg.name for r in rows):
+            continue
+        ms = time_workload(cfg, steps, warmup)
+        row = {"workload": cfg.name, "L": cfg.L, "log2_T": cfg.log2_T, "F": cfg.F,
+               "mlp": "-".join(map(str, cfg.widths)) if len(cfg.widths) > 1 else "removed",
+               "displacement": cfg.disp, "ms_per_frame": round(ms, 4),
+               "fps": round(1e3 / ms, 1), "paper_m1_fps": PAPER_FPS.get(cfg.name)}
+        rows.append(row)
+        print(json.dumps(row), file=sys.stderr, flush=True)
+    print(json.dumps({"paper_tables": rows, "resolution": "1280x720", "queries_per_pixel": 1}),
+          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -139,6 +185,8 @@ def main():
     ap.add_argument("--workload", default="view720p")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle work for the CPU baseline (0: skip)")
+    ap.add_argument("--paper-tables", action="store_true",
+                    help="time the paper's Tab. 3 / Tab. 6 profiling points instead")
     ap.add_argument("--no-rooflines", action="store_true",
                     help="skip the microbenchmark rooflines and the standalone MLP leg")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -164,6 +212,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "steps": args.steps}), flush=True)
+        return
+    if args.paper_tables:
+        paper_tables(args.steps, args.warmup)
         return
     cfg = synth.CONFIGS[args.workload]
     print(f"bench: generating {cfg.name} ({cfg.rays} rays, K={cfg.K})", file=sys.stderr,

@@ -141,7 +141,10 @@ typedef struct {
  * ReLU and no biases; the 4 outputs are (sigma_raw, r, g, b) with
  * sigma = exp(sigma_raw), rgb = sigmoid. */
 typedef struct {
-    int32_t n_layers;    /* weight matrices, 2..MIXRT_MAX_LAYERS */
+    int32_t n_layers;    /* weight matrices, 2..MIXRT_MAX_LAYERS; 0 = the MLP
+                            removed (the ablation of Tab. 3): input i is added
+                            to output i mod 4, width[0] a multiple of 4,
+                            view_sh_dim 0, data unused */
     int32_t width[MIXRT_MAX_LAYERS + 1]; /* width[0] = L*F + view_sh_dim,
                             hidden widths equal (16, 32 or 64), last = 4 */
     int32_t view_sh_dim; /* 0 or 16 */

@@ -195,8 +195,15 @@ def hash_encode(x: np.ndarray, table: np.ndarray, n_min: int, n_max: int):
 
 
 def mlp(inp: np.ndarray, weights) -> np.ndarray:
-    """inp [n, w0] (double); weights: list of [in,out] fp16 arrays."""
+    """inp [n, w0] (double); weights: list of [in,out] fp16 arrays (empty: the
+    MLP removed, inputs summed per component mod 4)."""
     inp = _c(inp, np.float64)
+    if not weights:
+        widths = np.array([inp.shape[1]], np.int32)
+        out = np.zeros((inp.shape[0], 4))
+        if lib().orc_mlp(inp.shape[0], _p(inp), 0, _p(widths), None, _p(out)):
+            raise ValueError("mlp: bad arguments")
+        return out
     widths = np.array([weights[0].shape[0]] + [w.shape[1] for w in weights], np.int32)
     flat = np.concatenate([np.asarray(w, np.float16).reshape(-1) for w in weights])
     bits = flat.view(np.uint16).copy()
@@ -230,7 +237,8 @@ class OracleScene:
         g0 = np.ascontiguousarray(scene.g0, np.float32)
         cams = np.ascontiguousarray(scene.cams, np.float32)
         widths = np.array(cfg.widths, np.int32)
-        wbits = scene.weights_flat.view(np.uint16).copy()
+        wbits = (scene.weights_flat.view(np.uint16).copy() if scene.weights
+                 else np.zeros(1, np.uint16))
         self._keep += [g0, cams, widths, wbits, scene.tex, scene.table]
         s = _OrcScene()
         s.views, s.H, s.W = cfg.views, cfg.rows_kept, cfg.W

@@ -381,6 +381,21 @@ int orc_hash_encode(int64_t n, const float *x, int L, int n_min, int n_max, int 
 int orc_mlp(int64_t n, const double *in, int n_layers, const int32_t *widths,
             const uint16_t *weights, double *out4)
 {
+    if (n_layers == 0) {
+        /* The MLP removed (the ablation of Tab. 3): the inputs are summed per
+         * component, input i feeding output i mod 4 = (sigma_raw, r, g, b). */
+        if (widths[0] < 4 || widths[0] % 4)
+            return -1;
+        for (int64_t s = 0; s < n; ++s) {
+            double o[4] = {0.0, 0.0, 0.0, 0.0};
+            for (int i = 0; i < widths[0]; ++i)
+                o[i % 4] += in[s * widths[0] + i];
+            out4[4 * s + 0] = exp(o[0]);
+            for (int c = 1; c < 4; ++c)
+                out4[4 * s + c] = 1.0 / (1.0 + exp(-o[c]));
+        }
+        return 0;
+    }
     if (n_layers < 1 || widths[n_layers] != 4)
         return -1;
     int maxw = 0;

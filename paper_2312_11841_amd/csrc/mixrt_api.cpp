@@ -162,14 +162,27 @@ int check_grid(const mixrt_hash_grid *g, Msg m)
 int check_mlp(const mixrt_mlp *p, int expect_in, Msg m, int *hid, int *nhid)
 {
     if (!p) return vfail(m, MIXRT_EINVAL, "mlp is NULL");
-    if (p->n_layers < 2 || p->n_layers > MIXRT_MAX_LAYERS)
-        return vfail(m, MIXRT_EUNSUPPORTED, "mlp.n_layers=%d outside 2..%d", p->n_layers,
+    if (p->n_layers < 0 || p->n_layers > MIXRT_MAX_LAYERS)
+        return vfail(m, MIXRT_EUNSUPPORTED, "mlp.n_layers=%d outside 0..%d", p->n_layers,
                      MIXRT_MAX_LAYERS);
     if (p->view_sh_dim != 0 && p->view_sh_dim != 16)
         return vfail(m, MIXRT_EUNSUPPORTED, "mlp.view_sh_dim=%d (0 or 16)", p->view_sh_dim);
     if (expect_in >= 0 && p->width[0] != expect_in)
         return vfail(m, MIXRT_EINVAL, "mlp.width[0]=%d but L*F+view_sh_dim=%d", p->width[0],
                      expect_in);
+    if (p->n_layers == 0) {
+        // the MLP removed: inputs summed per component (i mod 4)
+        if (p->view_sh_dim != 0)
+            return vfail(m, MIXRT_EINVAL, "mlp.n_layers=0 takes no view encoding");
+        if (p->width[0] < 4 || p->width[0] % 4)
+            return vfail(m, MIXRT_EINVAL, "mlp.n_layers=0 needs width[0] a multiple of 4");
+        *hid = 0;
+        *nhid = 0;
+        return MIXRT_OK;
+    }
+    if (p->n_layers < 2)
+        return vfail(m, MIXRT_EUNSUPPORTED, "mlp.n_layers=%d (0, or 2..%d)", p->n_layers,
+                     MIXRT_MAX_LAYERS);
     if (p->width[p->n_layers] != 4)
         return vfail(m, MIXRT_EINVAL, "mlp output width %d (must be 4)", p->width[p->n_layers]);
     const int h = p->width[1];

@@ -15,20 +15,37 @@ namespace mixrt {
 // Levels per batch of corner loads in the render kernel.
 constexpr int kLevelGroup = 2;
 
-// G levels of one query into its fp16 row of MLP inputs.
-template <int F, bool TF16, int G, bool DENSE>
+// G levels of one query: into its fp16 row of MLP inputs, or (the MLP
+// removed) added in fp32 to the per-component sums acc[(l F + i) mod 4].
+template <int F, bool TF16, int G, bool DENSE, bool SUM>
 __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, float x0, float x1,
-                                              float x2, _Float16 *row)
+                                              float x2, _Float16 *row, float *acc)
 {
     float f[G][F];
     hash_group<F, TF16, G, DENSE>(gp, l0, x0, x1, x2, f);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
+        if (SUM) {
+            // F = 4: feature i feeds component i; F = 2: level parity picks 0-1 or 2-3
 #pragma unroll
-        for (int i = 0; i < F; i += 2)
-            *(h2 *)(row + (l0 + g) * F + i) = h2{(_Float16)f[g][i], (_Float16)f[g][i + 1]};
+            for (int i = 0; i < F; ++i) {
+                const int comp = (F == 4) ? i : (((l0 + g) & 1) * 2 + i);
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (q == comp) acc[q] += f[g][i];
+            }
+        } else {
+#pragma unroll
+            for (int i = 0; i < F; i += 2)
+                *(h2 *)(row + (l0 + g) * F + i) = h2{(_Float16)f[g][i], (_Float16)f[g][i + 1]};
+        }
     }
 }
+
+// Stand-in for the weights when the MLP is removed.
+struct NoMlp {
+    __device__ __forceinline__ void load(const _Float16 *, int) {}
+};
 
 template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
@@ -45,7 +62,9 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     const int wv = threadIdx.x / kWave;
     _Float16 *rows = s_rows[wv];
 
-    MlpWeights<IN, HID, NHID> Wt;
+    // NHID = 0: the MLP removed; the level features are summed per component
+    constexpr bool SUM = NHID == 0;
+    typename std::conditional<SUM, NoMlp, MlpWeights<IN, HID, NHID>>::type Wt;
     Wt.load(weights, lane);
 
     const int K = rp.K;
@@ -74,21 +93,22 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         // --- hash encoding, features to LDS as fp16: dense levels first (pair
         // loads), then hashed levels, kLevelGroup levels per batch of loads
         _Float16 *row = rows + lane * LD;
+        float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
         if (hit) {
             int l = 0;
             for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
-                encode_levels<F, TF16, kLevelGroup, true>(gp, l, x0, x1, x2, row);
+                encode_levels<F, TF16, kLevelGroup, true, SUM>(gp, l, x0, x1, x2, row, acc);
             for (; l < n_dense; ++l)
-                encode_levels<F, TF16, 1, true>(gp, l, x0, x1, x2, row);
+                encode_levels<F, TF16, 1, true, SUM>(gp, l, x0, x1, x2, row, acc);
             for (; l + kLevelGroup <= L; l += kLevelGroup)
-                encode_levels<F, TF16, kLevelGroup, false>(gp, l, x0, x1, x2, row);
+                encode_levels<F, TF16, kLevelGroup, false, SUM>(gp, l, x0, x1, x2, row, acc);
             for (; l < L; ++l)
-                encode_levels<F, TF16, 1, false>(gp, l, x0, x1, x2, row);
-        } else {
+                encode_levels<F, TF16, 1, false, SUM>(gp, l, x0, x1, x2, row, acc);
+        } else if (!SUM) {
             for (int e = 0; e < L * F; e += 2)
                 *(h2 *)(row + e) = h2{(_Float16)0.0f, (_Float16)0.0f};
         }
-        if (view_sh) {
+        if (!SUM && view_sh) {
             float Y[16];
             sh_basis<16>(ry.dx, ry.dy, ry.dz, Y);
 #pragma unroll
@@ -97,21 +117,28 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
                 *(h2 *)(row + L * F + e) = hv;
             }
         }
-        s_hit[wv][lane] = hit ? 1 : 0;
-        wave_lds_sync();
-        // --- MLP on MFMA, 16 samples per step
-        const int c = lane & 15, g = lane >> 4;
-        const int n_nt = (spt + 15) >> 4;
-        for (int nt = 0; nt < n_nt; ++nt) {
-            const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
-            if (g == 0) {
-                const int s = nt * 16 + c;
-                float4 a = mlp_activate(o);
-                if (!s_hit[wv][s]) a.x = 0.0f;   // no density on a missed ray
-                s_out[wv][s] = a;
+        if constexpr (SUM) {
+            float4 a = mlp_activate(f4{acc[0], acc[1], acc[2], acc[3]});
+            if (!hit) a.x = 0.0f;   // no density on a missed ray
+            s_out[wv][lane] = a;
+            wave_lds_sync();
+        } else {
+            s_hit[wv][lane] = hit ? 1 : 0;
+            wave_lds_sync();
+            // --- MLP on MFMA, 16 samples per step
+            const int c = lane & 15, g = lane >> 4;
+            const int n_nt = (spt + 15) >> 4;
+            for (int nt = 0; nt < n_nt; ++nt) {
+                const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
+                if (g == 0) {
+                    const int s = nt * 16 + c;
+                    float4 a = mlp_activate(o);
+                    if (!s_hit[wv][s]) a.x = 0.0f;   // no density on a missed ray
+                    s_out[wv][s] = a;
+                }
             }
+            wave_lds_sync();
         }
-        wave_lds_sync();
         // --- compositing, one lane per ray
         if (lane < R) {
             const int ray_c = ray0 + lane;
@@ -128,7 +155,8 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
 }
 
 
-// Built render kernels: (texture kind, F, fp16 table, MLP in, hidden, hidden layers).
+// Built render kernels: (texture kind, F, fp16 table, MLP in, hidden, hidden
+// layers); in = hidden = layers = 0 is the MLP removed (any input width).
 #define MIXRT_RENDER_VARIANTS(X)                \
     X(kTexF32Ray, 2, false, 16, 32, 1)          \
     X(kTexF32Ray, 2, false, 32, 32, 1)          \
@@ -142,12 +170,18 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     X(kTexU8Ray, 2, false, 16, 32, 1)           \
     X(kTexNone, 2, false, 16, 32, 1)            \
     X(kTexNone, 2, true, 48, 64, 2)             \
-    X(kTexNone, 4, true, 32, 64, 2)
+    X(kTexNone, 4, true, 32, 64, 2)             \
+    X(kTexNone, 4, true, 32, 16, 2)             \
+    X(kTexNone, 4, true, 0, 0, 0)               \
+    X(kTexNone, 2, false, 0, 0, 0)              \
+    X(kTexF32Ray, 2, false, 0, 0, 0)            \
+    X(kTexU8Vec3D2, 4, true, 0, 0, 0)
 
 bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid)
 {
-#define X(a, b, c, d, e, f) \
-    if (tex == a && F == b && tf16 == c && in == d && hid == e && nhid == f) return true;
+#define X(a, b, c, d, e, f)                                                     \
+    if (tex == a && F == b && tf16 == c && nhid == f && (f == 0 || (in == d && hid == e))) \
+        return true;
     MIXRT_RENDER_VARIANTS(X)
 #undef X
     return false;
@@ -159,7 +193,8 @@ hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
     const int64_t n_tiles = ((int64_t)L.rp.rays + R - 1) / R;
     const int64_t want = (n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
 #define X(a, b, c, d, e, f)                                                                    \
-    if (L.tex == a && L.F == b && L.tf16 == c && L.in == d && L.hid == e && L.nhid == f) {      \
+    if (L.tex == a && L.F == b && L.tf16 == c && L.nhid == f &&                                \
+        (f == 0 || (L.in == d && L.hid == e))) {                                               \
         auto fn = render_kernel<a, b, c, d, e, f>;                                             \
         static int resident = 0; /* blocks resident on the whole device */                    \
         if (!resident) resident = resident_blocks((const void *)fn, L.cus);                    \

@@ -90,6 +90,17 @@ __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict_
     }
 }
 
+// The MLP removed: inputs summed per component (input i feeds output i mod 4).
+__global__ __launch_bounds__(kBlock) void sum_head_kernel(const _Float16 *__restrict__ in, int width,
+                                                          int64_t n, float4 *__restrict__ out4)
+{
+    const int64_t s = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (s >= n) return;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int i = 0; i < width; ++i) acc[i & 3] += (float)in[s * width + i];
+    out4[s] = mlp_activate(f4{acc[0], acc[1], acc[2], acc[3]});
+}
+
 __global__ __launch_bounds__(kBlock) void composite_kernel(const float4 *__restrict__ srgb,
                                                            int64_t rays, int K, float delta,
                                                            float t_term, float bg0, float bg1,
@@ -104,6 +115,7 @@ __global__ __launch_bounds__(kBlock) void composite_kernel(const float4 *__restr
 }
 
 #define MIXRT_MLP_VARIANTS(X) \
+    X(32, 16, 2)              \
     X(16, 32, 1)              \
     X(32, 32, 1)              \
     X(48, 64, 2)              \
@@ -112,6 +124,7 @@ __global__ __launch_bounds__(kBlock) void composite_kernel(const float4 *__restr
 
 bool mlp_variant_supported(int in, int hid, int nhid)
 {
+    if (nhid == 0) return in >= 4 && in % 4 == 0;
 #define X(d, e, f) \
     if (in == d && hid == e && nhid == f) return true;
     MIXRT_MLP_VARIANTS(X)
@@ -159,6 +172,11 @@ hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const 
                       int64_t n, float4 *out4, int cus, hipStream_t stream)
 {
     if (n == 0) return hipSuccess;
+    if (nhid == 0) {
+        hipLaunchKernelGGL(sum_head_kernel, dim3((unsigned)((n + kBlock - 1) / kBlock)),
+                           dim3(kBlock), 0, stream, x, in, n, out4);
+        return hipGetLastError();
+    }
     const int64_t want = ((n + kWave - 1) / kWave + kWavesPerBlock - 1) / kWavesPerBlock;
 #define X(d, e, f)                                                                           \
     if (in == d && hid == e && nhid == f) {                                                  \

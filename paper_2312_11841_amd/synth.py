@@ -59,7 +59,7 @@ class SceneConfig:
     N_max: int
     table_dtype: str          # "f32" | "f16"
     table_range: float        # table values ~ U[-table_range, table_range]
-    widths: tuple             # (in, hidden..., 4)
+    widths: tuple             # (in, hidden..., 4); (in,) = the MLP removed
     view_sh_dim: int          # 0 or 16
     w_std: float              # weights ~ N(0, w_std), stored fp16
     seed: int
@@ -169,9 +169,27 @@ TINY64_VEC3 = TINY64_DENSE.replace(name="tiny64_vec3", disp="vec3", sh_degree=1,
 TINY64_U8 = TINY64_DENSE.replace(name="tiny64_u8", tex_dtype="u8", tex_range=0.3, seed=14)
 TINY64_NODISP = TINY64_DENSE.replace(name="tiny64_nodisp", disp="none", seed=15)
 
+# Tab. 6's ablation: the paper's configuration without the displacement map.
+PAPER720P_NOVDD = PAPER720P.replace(name="paper720p_novdd", disp="none")
+
+
+def table3_config(L: int, log2_T: int, mlp: bool) -> SceneConfig:
+    """Tab. 3's profiling points: one query per pixel, no displacement map, F=4
+    entries over the deployed 256..4096 resolutions, with the MLP (two hidden
+    layers; width 16, the narrowest MFMA tile, for the table's 8) or without
+    it (level features summed per component)."""
+    widths = (L * 4, 16, 16, 4) if mlp else (L * 4,)
+    return PAPER720P.replace(name=f"tab3_L{L}_T{log2_T}" + ("_mlp" if mlp else ""), disp="none",
+                             L=L, log2_T=log2_T, view_sh_dim=0, widths=widths, seed=7)
+
+
+TABLE3 = [table3_config(8, 17, True), table3_config(8, 17, False), table3_config(1, 17, False),
+          table3_config(8, 5, False), table3_config(8, 22, False)]
+LEVEL_SWEEP = [table3_config(L, 17, False) for L in (1, 2, 4, 8, 16)]
+
 CONFIGS = {c.name: c for c in (TINY64, TINY64_DENSE, VIEW720P, VIEW720P_DENSE,
-                               BATCH8X1080P, DEPLOYED720P, PAPER720P, TINY64_VEC3,
-                               TINY64_U8, TINY64_NODISP)}
+                               BATCH8X1080P, DEPLOYED720P, PAPER720P, PAPER720P_NOVDD,
+                               TINY64_VEC3, TINY64_U8, TINY64_NODISP, *TABLE3, *LEVEL_SWEEP)}
 
 
 # --- scene container ----------------------------------------------------------
@@ -192,6 +210,8 @@ class Scene:
 
     @property
     def weights_flat(self) -> np.ndarray:
+        if not self.weights:
+            return np.zeros(0, np.float16)
         return np.concatenate([w.reshape(-1) for w in self.weights]).astype(np.float16)
 
     def digest(self) -> str:
@@ -355,7 +375,7 @@ def make_scene(cfg: SceneConfig) -> Scene:
                         (cfg.L, cfg.T, cfg.F)).astype(np.float32)
     table = table.astype(_NP_DT[cfg.table_dtype])
     assert cfg.widths[0] == cfg.L * cfg.F + cfg.view_sh_dim
-    assert cfg.widths[-1] == 4
+    assert cfg.widths[-1] == 4 or len(cfg.widths) == 1
     weights = []
     for m in range(len(cfg.widths) - 1):
         w = rng.normal(0.0, cfg.w_std, (cfg.widths[m], cfg.widths[m + 1]))

@@ -154,7 +154,7 @@ def _mlp_bound(x, weights):
     return 2.0 * err + 1e-6
 
 
-MLP_SHAPES = [(16, 32, 1), (32, 32, 1), (48, 64, 2), (32, 64, 2), (16, 64, 2)]
+MLP_SHAPES = [(16, 32, 1), (32, 32, 1), (48, 64, 2), (32, 64, 2), (16, 64, 2), (32, 16, 2)]
 
 
 @pytest.mark.parametrize("shape", MLP_SHAPES, ids=lambda s: f"{s[0]}-{s[1]}x{s[2]}")
@@ -177,6 +177,19 @@ def test_mlp_parity(R, shape, n):
     # sigma = exp(o0): relative error ~ |d o0|; rgb = sigmoid: slope <= 1/4
     assert np.all(np.abs(got[:, 0] / ref[:, 0] - 1) <= b[:, 0] * 1.01 + 1e-6)
     assert np.all(np.abs(got[:, 1:] - ref[:, 1:]) <= 0.25 * b[:, 1:] + 1e-6)
+
+
+@pytest.mark.parametrize("width", [4, 32])
+def test_mlp_removed_sums_per_component(R, width):
+    rng = np.random.default_rng(width)
+    n = 777
+    x = rng.uniform(-1, 1, (n, width)).astype(np.float16)
+    m = mixrt.Mlp()
+    m.n_layers, m.width[0] = 0, width
+    got = R.mlp(m, torch.from_numpy(x.view(np.int16).copy()).cuda()).cpu().numpy()
+    ref = oracle.mlp(x.astype(np.float64), [])
+    # fp32 sums of fp16 values; exp / sigmoid to ~1e-6 relative
+    assert np.allclose(got, ref, rtol=1e-5, atol=1e-6)
 
 
 # --------------------------------------------------------------------------
@@ -217,8 +230,9 @@ def _frame_pixels(cfg, rng, n):
 
 
 FRAME_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.VIEW720P_DENSE,
-              synth.DEPLOYED720P, synth.PAPER720P, synth.TINY64_VEC3, synth.TINY64_U8,
-              synth.TINY64_NODISP]
+              synth.DEPLOYED720P, synth.PAPER720P, synth.PAPER720P_NOVDD, synth.TINY64_VEC3,
+              synth.TINY64_U8, synth.TINY64_NODISP, *synth.TABLE3,
+              synth.TINY64_DENSE.replace(name="tiny64_nomlp", widths=(16,), seed=16)]
 
 
 @pytest.mark.parametrize("cfg", FRAME_CFGS, ids=lambda c: c.name)

@@ -416,6 +416,13 @@ def test_mlp_matches_numpy_matmul_chain():
     assert np.allclose(out[:, 1:], scipy.special.expit(h[:, 1:]), rtol=1e-12)
 
 
+def test_mlp_removed_sums_inputs_per_component():
+    x = np.arange(24, dtype=np.float64).reshape(2, 12) / 10.0
+    out = oracle.mlp(x, [])
+    o = x.reshape(2, 3, 4).sum(1)
+    assert np.allclose(out[:, 0], np.exp(o[:, 0])) and np.allclose(out[:, 1:], scipy.special.expit(o[:, 1:]))
+
+
 def test_mlp_identity_passes_input_through():
     x = np.array([[0.5, -0.25, 1.5, -3.0]] * 2 + [[2.0, 1.0, -1.0, 0.0]])
     eye = np.eye(4, dtype=np.float16)
