@@ -69,6 +69,13 @@ def _declare(L):
     L.orc_render_pixels.argtypes = [P, C.c_int64, P, P, C.c_int]
     L.orc_pixel_samples.restype = C.c_int
     L.orc_pixel_samples.argtypes = [P, C.c_int64, P, P, P, P]
+    L.orc_ray_triangle.restype = C.c_int
+    L.orc_ray_triangle.argtypes = [P, P, P, P, C.c_int64, P, P, P, P]
+    L.orc_ray_mesh.restype = C.c_int64
+    L.orc_ray_mesh.argtypes = [P, P, P, P, C.c_int64, P, C.c_double, P, P, P, P, P]
+    L.orc_raycast_pixels.restype = C.c_int
+    L.orc_raycast_pixels.argtypes = [C.c_int, C.c_int, C.c_int, P, P, P, C.c_int64, P,
+                                     C.c_int64, P, P, P, P, P, C.c_int]
     L.orc_max_threads.restype = C.c_int
     L.orc_max_threads.argtypes = []
 
@@ -222,6 +229,47 @@ def composite(srgb: np.ndarray, delta: float, bg) -> np.ndarray:
     out = np.zeros((rays, 4))
     lib().orc_composite(rays, K, _p(srgb), float(delta), _p(bg), _p(out))
     return out
+
+
+# --- the coarse-mesh hit (the G-buffer) ------------------------------------------
+
+def ray_triangle(o, d, positions, faces, f: int):
+    """fp64 Moller-Trumbore against triangle f: (t, b1, b2, cos) or None."""
+    o, d = _c(o, np.float64), _c(d, np.float64)
+    pos, fc = _c(positions, np.float32), _c(faces, np.int32)
+    out = np.zeros(4)
+    ok = lib().orc_ray_triangle(_p(o), _p(d), _p(pos), _p(fc), f, _p(out[0:]), _p(out[1:]),
+                                _p(out[2:]), _p(out[3:]))
+    return tuple(out) if ok else None
+
+
+def ray_mesh(o, d, positions, faces, uv=None, t_min: float = 1e-4):
+    """Closest hit over all triangles: dict(tri, t, bary, uv, normal, ambiguous)."""
+    o, d = _c(o, np.float64), _c(d, np.float64)
+    pos, fc = _c(positions, np.float32), _c(faces, np.int32)
+    uvc = None if uv is None else _c(uv, np.float32)
+    t, bary, uvo, n = np.zeros(1), np.zeros(2), np.zeros(2), np.zeros(3)
+    amb = C.c_int(0)
+    f = lib().orc_ray_mesh(_p(o), _p(d), _p(pos), _p(fc), fc.shape[0], _p(uvc), t_min, _p(t),
+                           _p(bary), _p(uvo), _p(n), C.byref(amb))
+    return {"tri": int(f), "t": float(t[0]), "bary": bary, "uv": uvo, "normal": n,
+            "ambiguous": bool(amb.value)}
+
+
+def raycast_pixels(cams, W: int, H: int, mesh, pix, threads: int = 1):
+    """The G-buffer of flat pixel indices (view-major) by brute force:
+    (g0 [n,4] f64 (t, u, v, 0) with t = -1 for a miss, normal [n,3], tri [n],
+    ambiguous [n] bool)."""
+    cams = _c(cams, np.float32).reshape(-1, 16)
+    pos, fc = _c(mesh.positions, np.float32), _c(mesh.faces, np.int32)
+    uv = _c(mesh.uv, np.float32)
+    pix = _c(pix, np.int64).reshape(-1)
+    g0, n = np.zeros((pix.size, 4)), np.zeros((pix.size, 3))
+    tri, amb = np.zeros(pix.size, np.int64), np.zeros(pix.size, np.int32)
+    lib().orc_raycast_pixels(cams.shape[0], H, W, _p(cams), _p(pos), _p(fc), fc.shape[0],
+                             _p(uv), pix.size, _p(pix), _p(g0), _p(n), _p(tri), _p(amb),
+                             threads)
+    return g0, n, tri, amb.astype(bool)
 
 
 # --- the whole path -------------------------------------------------------------

@@ -603,6 +603,143 @@ int orc_pixel_samples(const orc_scene *sc, int64_t n_pix, const int64_t *pix, fl
     return 0;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Step 2's input: the coarse-mesh hit per pixel (Fig. 2 step 1)              */
+/* ------------------------------------------------------------------------ */
+
+/* Moller-Trumbore in double for triangle f: writes t, the barycentrics
+ * (b1, b2) of corners 1 and 2 and the cosine between d and the face normal;
+ * returns 0 when the ray is parallel to it. */
+int orc_ray_triangle(const double *o, const double *d, const float *pos, const int32_t *faces,
+                     int64_t f, double *t, double *b1, double *b2, double *cosine)
+{
+    const float *a = pos + 3 * (int64_t)faces[3 * f];
+    const float *b = pos + 3 * (int64_t)faces[3 * f + 1];
+    const float *c = pos + 3 * (int64_t)faces[3 * f + 2];
+    double e1[3], e2[3], s[3], p[3], q[3];
+    for (int k = 0; k < 3; ++k) {
+        e1[k] = (double)b[k] - (double)a[k];
+        e2[k] = (double)c[k] - (double)a[k];
+        s[k] = o[k] - (double)a[k];
+    }
+    p[0] = d[1] * e2[2] - d[2] * e2[1];
+    p[1] = d[2] * e2[0] - d[0] * e2[2];
+    p[2] = d[0] * e2[1] - d[1] * e2[0];
+    double det = e1[0] * p[0] + e1[1] * p[1] + e1[2] * p[2];
+    if (fabs(det) < 1e-300)
+        return 0;
+    double n[3] = {e1[1] * e2[2] - e1[2] * e2[1], e1[2] * e2[0] - e1[0] * e2[2],
+                   e1[0] * e2[1] - e1[1] * e2[0]};
+    *cosine = -det / sqrt(n[0] * n[0] + n[1] * n[1] + n[2] * n[2]);  /* det = -d.n */
+    double inv = 1.0 / det;
+    q[0] = s[1] * e1[2] - s[2] * e1[1];
+    q[1] = s[2] * e1[0] - s[0] * e1[2];
+    q[2] = s[0] * e1[1] - s[1] * e1[0];
+    *b1 = (s[0] * p[0] + s[1] * p[1] + s[2] * p[2]) * inv;
+    *b2 = (d[0] * q[0] + d[1] * q[1] + d[2] * q[2]) * inv;
+    *t = (e2[0] * q[0] + e2[1] * q[1] + e2[2] * q[2]) * inv;
+    return 1;
+}
+
+/* Closest intersection of the ray o + t d (t > t_min) with every triangle of
+ * a mesh (brute force); equal t goes to the lower triangle index.  Returns the
+ * triangle (-1 for a miss) and writes t, the barycentrics (b1, b2) of corners
+ * 1 and 2, the interpolated vertex uv, the unit face normal e1 x e2, and
+ * *ambiguous = 1 when a fp32 solver may legitimately answer otherwise: the
+ * hit lies within eps_b of an edge (barycentric margin), or another triangle
+ * that is hit or nearly hit (margin > -eps_b) lies no farther than
+ * t (1 + eps_t); for a miss, when any triangle in front is nearly hit.  Both
+ * slacks widen as 0.1 / |cos| below a cosine of 0.1, since a grazing ray's
+ * rounding error grows like the inverse cosine. */
+static double graze(double cosine)
+{
+    return fmax(1.0, 0.1 / fmax(fabs(cosine), 1e-12));
+}
+
+int64_t orc_ray_mesh(const double *o, const double *d, const float *pos, const int32_t *faces,
+                     int64_t nf, const float *uv, double t_min, double *t_out, double *bary,
+                     double *uv_out, double *normal, int *ambiguous)
+{
+    const double eps_b = 2e-4, eps_t = 1e-4;
+    double best = INFINITY, bb1 = 0.0, bb2 = 0.0, bcos = 1.0, t, b1, b2, cs;
+    int64_t best_i = -1;
+    for (int64_t f = 0; f < nf; ++f) {
+        if (!orc_ray_triangle(o, d, pos, faces, f, &t, &b1, &b2, &cs))
+            continue;
+        if (t > t_min && b1 >= 0.0 && b2 >= 0.0 && b1 + b2 <= 1.0 && t < best) {
+            best = t;              /* strict: an equal t keeps the lower index */
+            best_i = f;
+            bb1 = b1;
+            bb2 = b2;
+            bcos = cs;
+        }
+    }
+    *ambiguous = best_i >= 0 && fmin(fmin(bb1, bb2), 1.0 - bb1 - bb2) < eps_b * graze(bcos);
+    for (int64_t f = 0; f < nf && !*ambiguous; ++f) {
+        if (f == best_i || !orc_ray_triangle(o, d, pos, faces, f, &t, &b1, &b2, &cs))
+            continue;
+        double g = graze(cs) * (best_i >= 0 ? graze(bcos) : 1.0);
+        double reach = best_i >= 0 ? best * (1.0 + eps_t * g) : INFINITY;
+        if (t > t_min && t <= reach && fmin(fmin(b1, b2), 1.0 - b1 - b2) > -eps_b * g)
+            *ambiguous = 1;
+    }
+    if (best_i < 0)
+        return -1;
+    const int32_t *fc = faces + 3 * best_i;
+    double b0 = 1.0 - bb1 - bb2, e1[3], e2[3];
+    for (int k = 0; k < 3; ++k) {
+        e1[k] = (double)pos[3 * fc[1] + k] - (double)pos[3 * fc[0] + k];
+        e2[k] = (double)pos[3 * fc[2] + k] - (double)pos[3 * fc[0] + k];
+    }
+    double n[3] = {e1[1] * e2[2] - e1[2] * e2[1], e1[2] * e2[0] - e1[0] * e2[2],
+                   e1[0] * e2[1] - e1[1] * e2[0]};
+    double nn = sqrt(n[0] * n[0] + n[1] * n[1] + n[2] * n[2]);
+    for (int k = 0; k < 3; ++k)
+        normal[k] = nn > 0.0 ? n[k] / nn : 0.0;
+    for (int k = 0; k < 2; ++k)
+        uv_out[k] = uv ? b0 * uv[2 * fc[0] + k] + bb1 * uv[2 * fc[1] + k] + bb2 * uv[2 * fc[2] + k]
+                       : 0.0;
+    *t_out = best;
+    bary[0] = bb1;
+    bary[1] = bb2;
+    return best_i;
+}
+
+/* The G-buffer of a list of pixels of views x H x W cameras (cams [views][16]):
+ * per pixel g0 = (t, u, v, 0) (t = -1 for a miss), normal [3], triangle id
+ * (-1 miss) and the ambiguity flag. */
+int orc_raycast_pixels(int views, int H, int W, const float *cams, const float *pos,
+                       const int32_t *faces, int64_t nf, const float *uv, int64_t n_pix,
+                       const int64_t *pix, double *g0, double *normal, int64_t *tri, int32_t *amb,
+                       int n_threads)
+{
+    (void)views;
+#ifdef _OPENMP
+    if (n_threads < 1)
+        n_threads = 1;
+#pragma omp parallel for schedule(dynamic, 4) num_threads(n_threads)
+#endif
+    for (int64_t q = 0; q < n_pix; ++q) {
+        int64_t hw = (int64_t)H * W;
+        int view = (int)(pix[q] / hw);
+        int64_t rem = pix[q] % hw;
+        int j = (int)(rem / W), i = (int)(rem % W);
+        double o[3], d[3], t, bary[2], uvo[2], n[3];
+        int ambiguous = 0;
+        orc_camera_ray(cams + 16 * view, W, H, i, j, o, d);
+        int64_t f = orc_ray_mesh(o, d, pos, faces, nf, uv, 1e-4, &t, bary, uvo, n, &ambiguous);
+        tri[q] = f;
+        amb[q] = ambiguous;
+        g0[4 * q + 0] = f < 0 ? -1.0 : t;
+        g0[4 * q + 1] = f < 0 ? 0.0 : uvo[0];
+        g0[4 * q + 2] = f < 0 ? 0.0 : uvo[1];
+        g0[4 * q + 3] = 0.0;
+        for (int k = 0; k < 3; ++k)
+            normal[3 * q + k] = f < 0 ? 0.0 : n[k];
+    }
+    return 0;
+}
+
 int orc_max_threads(void)
 {
 #ifdef _OPENMP

@@ -391,3 +391,130 @@ def make_scene(cfg: SceneConfig) -> Scene:
 
 def dtype_code(name: str) -> int:
     return _DT_CODE[name]
+
+
+# --- procedural low-poly mesh (the G-buffer's geometry) -----------------------
+
+def _icosphere(level: int):
+    """Unit icosphere: 20 * 4^level faces (vertices deduplicated per level)."""
+    t = (1.0 + 5 ** 0.5) / 2.0
+    v = np.array([[-1, t, 0], [1, t, 0], [-1, -t, 0], [1, -t, 0], [0, -1, t], [0, 1, t],
+                  [0, -1, -t], [0, 1, -t], [t, 0, -1], [t, 0, 1], [-t, 0, -1], [-t, 0, 1]],
+                 np.float64)
+    f = np.array([[0, 11, 5], [0, 5, 1], [0, 1, 7], [0, 7, 10], [0, 10, 11], [1, 5, 9],
+                  [5, 11, 4], [11, 10, 2], [10, 7, 6], [7, 1, 8], [3, 9, 4], [3, 4, 2],
+                  [3, 2, 6], [3, 6, 8], [3, 8, 9], [4, 9, 5], [2, 4, 11], [6, 2, 10],
+                  [8, 6, 7], [9, 8, 1]], np.int64)
+    v /= np.linalg.norm(v, axis=1, keepdims=True)
+    for _ in range(level):
+        edges = np.concatenate([f[:, [0, 1]], f[:, [1, 2]], f[:, [2, 0]]])
+        key = np.sort(edges, axis=1)
+        uniq, inv = np.unique(key, axis=0, return_inverse=True)
+        mid = v[uniq[:, 0]] + v[uniq[:, 1]]
+        mid /= np.linalg.norm(mid, axis=1, keepdims=True)
+        m = inv.reshape(3, -1).T + len(v)           # midpoints of edges 01, 12, 20
+        v = np.concatenate([v, mid])
+        a, b, c = f[:, 0], f[:, 1], f[:, 2]
+        m01, m12, m20 = m[:, 0], m[:, 1], m[:, 2]
+        f = np.concatenate([np.stack([a, m01, m20], 1), np.stack([b, m12, m01], 1),
+                            np.stack([c, m20, m12], 1), np.stack([m01, m12, m20], 1)])
+    return v, f
+
+
+@dataclass
+class Mesh:
+    positions: np.ndarray   # [nv, 3] f32
+    faces: np.ndarray       # [nf, 3] i32
+    uv: np.ndarray          # [nv, 2] f32, texture atlas coordinates in [0, 1]
+
+    @property
+    def nbytes(self) -> int:
+        return self.positions.nbytes + self.faces.nbytes + self.uv.nbytes
+
+
+def _box(div: int):
+    """Cube [-1, 1]^3, each face a div x div grid of quads split in two,
+    wound so that e1 x e2 points out; returns positions, faces and each
+    vertex's (face index, s, t) chart coordinates in [0, 1]^2."""
+    g = np.linspace(-1.0, 1.0, div + 1)
+    S, T = np.meshgrid(g, g, indexing="ij")
+    pos, faces, chart = [], [], []
+    for k, (ax, sign) in enumerate([(a, s) for a in range(3) for s in (1.0, -1.0)]):
+        p = np.zeros((div + 1, div + 1, 3))
+        p[..., ax] = sign
+        p[..., (ax + 1) % 3] = S
+        p[..., (ax + 2) % 3] = T
+        idx = np.arange((div + 1) ** 2).reshape(div + 1, div + 1) + k * (div + 1) ** 2
+        q00, q10 = idx[:-1, :-1].ravel(), idx[1:, :-1].ravel()
+        q11, q01 = idx[1:, 1:].ravel(), idx[:-1, 1:].ravel()
+        f = np.concatenate([np.stack([q00, q10, q11], 1), np.stack([q00, q11, q01], 1)])
+        faces.append(f if sign > 0 else f[:, ::-1])
+        pos.append(p.reshape(-1, 3))
+        chart.append(np.stack([np.full(S.size, k), (S.ravel() + 1) / 2, (T.ravel() + 1) / 2], 1))
+    return np.concatenate(pos), np.concatenate(faces), np.concatenate(chart)
+
+
+def _rotation(rng: np.random.Generator) -> np.ndarray:
+    q = rng.normal(size=4)
+    w, x, y, z = q / np.linalg.norm(q)
+    return np.array([[1 - 2 * (y * y + z * z), 2 * (x * y - z * w), 2 * (x * z + y * w)],
+                     [2 * (x * y + z * w), 1 - 2 * (x * x + z * z), 2 * (y * z - x * w)],
+                     [2 * (x * z - y * w), 2 * (y * z + x * w), 1 - 2 * (x * x + y * y)]])
+
+
+def make_mesh(seed: int, room_level: int = 7, n_objects: int = 24, object_level: int = 4,
+              n_boxes: int = 16, box_div: int = 16, room_radius: float = 6.0) -> Mesh:
+    """A perturbed-sphere room seen from inside, with perturbed-sphere and box
+    objects placed clear of a 0.8-radius ball around the origin (where the
+    cameras stand).  Defaults: 499,712 triangles.
+
+    Texture atlas: the room takes the [0, 0.5]^2 quarter with a spherical
+    (azimuth, polar) chart; every object takes one 0.125-sized tile (spheres:
+    spherical chart, boxes: a 3 x 2 grid of face charts)."""
+    rng = np.random.default_rng(seed)
+    tiles = [(0.5 + (k % 4) * 0.125, (k // 4) * 0.125) for k in range(32)] + \
+            [((k % 4) * 0.125, 0.5 + (k // 4) * 0.125) for k in range(32)]
+    pos, faces, uvs = [], [], []
+    base = 0
+
+    def place(reach):
+        while True:
+            c = rng.uniform(-0.6, 0.6, 3) * room_radius
+            if reach + 0.8 < np.linalg.norm(c) < 0.75 * room_radius:
+                return c
+
+    for o in range(1 + n_objects + n_boxes):
+        if o <= n_objects:
+            v, f = _icosphere(room_level if o == 0 else object_level)
+            amp = 0.06 if o == 0 else 0.12
+            r0 = room_radius if o == 0 else rng.uniform(0.2, 0.8)
+            c = np.zeros(3) if o == 0 else place(r0 * (1 + amp))
+            th = np.arccos(np.clip(v[:, 2], -1, 1))
+            ph = np.arctan2(v[:, 1], v[:, 0])
+            k1, k2 = rng.integers(2, 6, 2)
+            ph0 = rng.uniform(0, 2 * np.pi)
+            r = r0 * (1.0 + amp * np.sin(k1 * th) * np.cos(k2 * ph + ph0))
+            p = c + v * r[:, None]
+            cu, cv = (ph + np.pi) / (2 * np.pi), th / np.pi
+            if o == 0:
+                uv = np.stack([0.5 * cu, 0.5 * cv], 1)
+            else:
+                tu, tv = tiles[(o - 1) % len(tiles)]
+                uv = np.stack([tu + 0.125 * cu, tv + 0.125 * cv], 1)
+        else:
+            v, f, chart = _box(box_div)
+            half = rng.uniform(0.15, 0.6, 3)
+            R = _rotation(rng)
+            c = place(float(np.linalg.norm(half)))
+            p = c + (v * half) @ R.T
+            tu, tv = tiles[(o - 1) % len(tiles)]
+            k = chart[:, 0]
+            cell = 0.125 / 3
+            uv = np.stack([tu + (k % 3 + chart[:, 1]) * cell, tv + (k // 3 + chart[:, 2]) * cell], 1)
+        pos.append(p)
+        uvs.append(uv)
+        faces.append(f + base)
+        base += len(p)
+    return Mesh(positions=np.concatenate(pos).astype(np.float32),
+                faces=np.concatenate(faces).astype(np.int32),
+                uv=np.clip(np.concatenate(uvs), 0, 1).astype(np.float32))

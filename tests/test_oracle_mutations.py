@@ -39,6 +39,15 @@ MUTATIONS = {
     "stored_channels": ("s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * m->C + c);",
                         "s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * nch + c);"),
     "no_background": ("out[4 * r + ch] = c[ch] + Tend * bg[3 * r + ch];", "out[4 * r + ch] = c[ch];"),
+    "tie_to_higher_index": ("b1 + b2 <= 1.0 && t < best) {", "b1 + b2 <= 1.0 && t <= best) {"),
+    "hits_behind": ("if (t > t_min && b1 >= 0.0", "if (b1 >= 0.0"),
+    "uv_corner_swap": ("+ bb1 * uv[2 * fc[1] + k] + bb2 * uv[2 * fc[2] + k]",
+                       "+ bb2 * uv[2 * fc[1] + k] + bb1 * uv[2 * fc[2] + k]"),
+    "normal_flip": ("double nn = sqrt(n[0] * n[0] + n[1] * n[1] + n[2] * n[2]);\n    for (int k = 0; k < 3; ++k)\n        normal[k] = nn > 0.0 ? n[k] / nn",
+                    "double nn = sqrt(n[0] * n[0] + n[1] * n[1] + n[2] * n[2]);\n    for (int k = 0; k < 3; ++k)\n        normal[k] = nn > 0.0 ? -n[k] / nn"),
+    "q_uses_e2": ("q[0] = s[1] * e1[2] - s[2] * e1[1];", "q[0] = s[1] * e2[2] - s[2] * e2[1];"),
+    "no_grazing_slack": ("return fmax(1.0, 0.1 / fmax(fabs(cosine), 1e-12));", "return 1.0;"),
+    "no_near_miss": ("fmin(fmin(b1, b2), 1.0 - b1 - b2) > -eps_b * g)", "fmin(fmin(b1, b2), 1.0 - b1 - b2) > 0.0)"),
 }
 
 
@@ -54,6 +63,7 @@ def test_pins_reject_planted_mistake(name, tmp_path):
                     "-fPIC", str(mut), "-o", str(lib), "-lm"], check=True)
     env = dict(os.environ, MIXRT_ORACLE_LIB=str(lib))
     r = subprocess.run([sys.executable, "-m", "pytest", os.path.join(ROOT, "tests", "test_oracle_pins.py"),
+                        os.path.join(ROOT, "tests", "test_oracle_mesh_pins.py"),
                         "-x", "-q", "-p", "no:cacheprovider"], cwd=ROOT, env=env,
                        capture_output=True, text=True, timeout=300)
     assert r.returncode != 0, f"pins did not catch {name}:\n{r.stdout[-2000:]}"
