@@ -3,7 +3,8 @@
 One step = one mixrt_render call over one frame of the 1280x720 workload
 (every stage of the path: ray setup, Eq. 2 calibration, K samples,
 contraction, hash encoding, MLP, compositing), inputs already resident in
-HBM.  Prints one JSON line.
+HBM.  For mesh workloads (--workload mesh720p) a step is the ray cast of the
+mesh into the G-buffer followed by that render call.  Prints one JSON line.
 """
 import argparse
 import json
@@ -112,23 +113,52 @@ def algorithmic_work(cfg):
 
 
 def cpu_baseline(scene, budget_s: float):
-    """The oracle, as it is, on a bounded random sample of the frame's pixels."""
+    """The oracle, as it is, on a bounded random sample of the frame's pixels
+    (for mesh workloads: its brute-force ray cast of those pixels, then its
+    render of them)."""
+    import dataclasses
     import oracle
     threads = oracle.max_threads()
-    orc = oracle.OracleScene(scene)
+    cfg = scene.cfg
+
+    def run(pix):
+        if scene.mesh is None:
+            return oracle.OracleScene(scene).render_pixels(pix, threads=threads)
+        g0, _, _, _ = oracle.raycast_pixels(scene.cams, cfg.W, cfg.H, scene.mesh, pix,
+                                            threads=threads)
+        flat = scene.g0.reshape(-1, 4).copy()
+        flat[pix] = g0.astype(np.float32)
+        sc = dataclasses.replace(scene, g0=flat.reshape(scene.g0.shape))
+        return oracle.OracleScene(sc).render_pixels(pix, threads=threads)
+
     rng = np.random.default_rng(0)
-    probe = rng.choice(scene.cfg.rays, 2000, replace=False)
+    n0 = 2000 if scene.mesh is None else 200
+    probe = rng.choice(cfg.rays, n0, replace=False)
     t0 = time.perf_counter()
-    orc.render_pixels(probe, threads=threads)
+    run(probe)
     dt = time.perf_counter() - t0
-    n = int(min(scene.cfg.rays, max(2000, 2000 * budget_s / max(dt, 1e-6))))
-    pix = rng.choice(scene.cfg.rays, n, replace=False)
+    n = int(min(cfg.rays, max(n0, n0 * budget_s / max(dt, 1e-6))))
+    pix = rng.choice(cfg.rays, n, replace=False)
     t0 = time.perf_counter()
-    orc.render_pixels(pix, threads=threads)
+    run(pix)
     dt = time.perf_counter() - t0
+    what = "brute-force ray cast + render" if scene.mesh is not None else "render"
     return {"value": n / dt / 1e6, "unit": "Mpix/s", "cores": threads, "kind": "oracle",
-            "sample": f"{n} random pixels of one {scene.cfg.W}x{scene.cfg.H} frame "
+            "sample": f"{n} random pixels of one {cfg.W}x{cfg.H} frame, {what} "
                       f"({dt:.1f} s wall, OpenMP over pixels)"}
+
+
+def time_launches(stream, fn, steps):
+    """Average ms of fn() over steps launches, HIP events on `stream`."""
+    import torch
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record(stream)
+    for _ in range(steps):
+        fn()
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps
 
 
 # The paper's profiling points (FPS at 1280x720 on a MacBook M1 Pro in WebGL,
@@ -224,36 +254,58 @@ def main():
     out = torch.empty((cfg.rays, 4), dtype=torch.float32, device="cuda:0")
     stream = torch.cuda.current_stream()
     r = mixrt.Renderer(0, stream=stream)
+    mesh = None
+    if scene.mesh is not None:
+        # load time, outside the timed region: grid build on the host + upload
+        t0 = time.perf_counter()
+        mesh = mixrt.DeviceMesh(r, scene.mesh)
+        mesh_load_s = time.perf_counter() - t0
+
+    def raycast():
+        r.raycast(mesh, ds.cams, cfg.W, cfg.H, out=(ds.g0, None))
+
+    def render():
+        r.render(ds, out)
+
+    def step():
+        if mesh is not None:
+            raycast()
+        render()
 
     for _ in range(args.warmup):
-        r.render(ds, out)
+        step()
     torch.cuda.synchronize()
     print(f"bench: warmup done, timing {args.steps} frames", file=sys.stderr, flush=True)
 
-    # The render kernel is the only kernel of a step; HIP events on the
-    # renderer's stream bracket exactly the timed launches.
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
+    # HIP events on the renderer's stream bracket exactly the timed launches.
     t_wall = time.perf_counter()
-    start.record(stream)
-    for _ in range(args.steps):
-        r.render(ds, out)
-    end.record(stream)
-    torch.cuda.synchronize()
+    ms = time_launches(stream, step, args.steps)
     t_wall = time.perf_counter() - t_wall
-    ms = start.elapsed_time(end) / args.steps
+    # The roofline's kernel timed on its own (for a render-only step this is
+    # the step itself).
+    render_ms = ms if mesh is None else time_launches(stream, render, args.steps)
     extra = {}
+    if mesh is not None:
+        ray_ms = time_launches(stream, raycast, args.steps)
+        extra["raycast"] = {
+            "kernel": "raycast_kernel (uniform-grid walk + fp32 Moller-Trumbore)",
+            "ms": round(ray_ms, 4), "render_ms": round(render_ms, 4),
+            "Mrays_per_s": round(cfg.rays / (ray_ms * 1e-3) / 1e6, 1),
+            "mesh_faces": int(len(scene.mesh.faces)), "mesh_bytes": int(scene.mesh.nbytes),
+            "grid": mesh.info, "load_s": round(mesh_load_s, 2)}
     if not args.no_rooflines:
         extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
         extra["rooflines_measured"] = measured_rooflines(cfg)
+    if mesh is not None:
+        mesh.close()
     r.close()
 
     work = algorithmic_work(cfg)
     traffic, traffic_src = measured_traffic(cfg.name)
     sec = ms * 1e-3
+    rsec = render_ms * 1e-3
     total_bytes = work["hash_bytes"] + work["ray_bytes"]
-    achieved = total_bytes / sec / 1e9
+    achieved = total_bytes / rsec / 1e9
     mpix = cfg.rays / sec / 1e6
     line = {
         "metric": "Mpix/s and ms/frame at 1280x720 (1 GPU); hash-encode GB/s, MLP MFMA util",
@@ -273,13 +325,16 @@ def main():
             "workload": f"{cfg.name}: {cfg.views}x{cfg.W}x{cfg.H} px, K={cfg.K}, "
                         f"hash L={cfg.L} T=2^{cfg.log2_T} F={cfg.F} {cfg.table_dtype} "
                         f"N {cfg.N_min}-{cfg.N_max}, texture {cfg.tex_R}^2x{cfg.tex_V} "
-                        f"{cfg.tex_dtype}, MLP {'-'.join(map(str, cfg.widths))} fp16",
+                        f"{cfg.tex_dtype}, MLP {'-'.join(map(str, cfg.widths))} fp16"
+                        + (f"; G-buffer ray-cast from a {len(scene.mesh.faces)}-triangle mesh "
+                           "in each step" if scene.mesh is not None else ""),
             "rays": cfg.rays,
             "samples": cfg.samples,
             "parallelism": "single GPU",
         },
         "roofline": {
-            "kernel": "render_kernel (fused path, the only kernel of a step)",
+            "kernel": "render_kernel (fused path" + (", the only kernel of a step)" if mesh is None
+                                                      else "; timed alone)"),
             "bound": "hbm",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBPS,
@@ -291,10 +346,10 @@ def main():
             "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
                                            "ray": work["per_ray_bytes"]},
         },
-        "hash_encode_GBps": round(work["hash_bytes"] / sec / 1e9, 1),
-        "hash_lane_loads_per_s": round(cfg.samples * cfg.L * 8 / sec),
-        "mlp_mfma_util": round(work["mlp_flops"] / sec / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
-        "mlp_tflops": round(work["mlp_flops"] / sec / 1e12, 2),
+        "hash_encode_GBps": round(work["hash_bytes"] / rsec / 1e9, 1),
+        "hash_lane_loads_per_s": round(cfg.samples * cfg.L * 8 / rsec),
+        "mlp_mfma_util": round(work["mlp_flops"] / rsec / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
+        "mlp_tflops": round(work["mlp_flops"] / rsec / 1e12, 2),
         "wall_s_timed": round(t_wall, 3),
         "kernel_source_digest": kernel_source_digest(),
     }

@@ -230,6 +230,78 @@ int mixrt_debug_mlp(mixrt_ctx *ctx, const mixrt_mlp *mlp, const uint16_t *in_f16
 int mixrt_debug_composite(mixrt_ctx *ctx, const float *srgb, int64_t rays,
                           const mixrt_sampling *smp, const float *bg, float *out_rgba);
 
+/* ---- geometry: the coarse-mesh hit per pixel (Fig. 2 step 1) -------------- */
+
+/* The G-buffer the rendering path reads (g0: hit distance t and texture
+ * coordinate p_t) is the intersection of each pixel's ray with the low-poly
+ * mesh (Sec. 4.3, Fig. 2 step 1), which the paper obtains by rasterising the
+ * mesh.  These entry points compute it by ray casting on the GPU instead: a
+ * mesh is uploaded once into a uniform grid of triangle lists, then each
+ * pixel's ray walks the grid cells it crosses and keeps the closest triangle
+ * hit (t > MIXRT_RAY_T_MIN).  Hits at equal t go to the lower triangle index. */
+
+#define MIXRT_RAY_T_MIN 1e-4f
+
+typedef struct mixrt_mesh mixrt_mesh;
+
+typedef struct {
+    int64_t n_vertices;      /* 3 .. 2^31-1 */
+    int64_t n_faces;         /* 1 .. 2^31-1 */
+    const float *positions;  /* host [n_vertices][3], finite */
+    const int32_t *faces;    /* host [n_faces][3] vertex indices in [0, n_vertices);
+                                the face normal is e1 x e2 with e1 = p1 - p0,
+                                e2 = p2 - p0 */
+    const float *uv;         /* host [n_vertices][2] texture coordinates, or NULL
+                                (then the G-buffer's p_t is (0, 0)) */
+    int32_t grid_res[3];     /* cells per axis (1..1024 each, at most 2^26 in all),
+                                or all 0: chosen from the bounds so that the
+                                grid has about cells_per_face * n_faces cells */
+    float cells_per_face;    /* for grid_res = 0; 0 means 2 */
+} mixrt_mesh_desc;
+
+typedef struct {
+    int32_t grid_res[3];     /* cells per axis */
+    float lo[3], hi[3];      /* the grid's box (the mesh bounds, padded) */
+    int64_t n_faces;
+    int64_t n_refs;          /* triangle entries over all cell lists */
+    int64_t device_bytes;    /* device memory the mesh holds */
+} mixrt_mesh_info;
+
+/* Pure host (makes no HIP call): validate desc and report the grid that
+ * mixrt_mesh_create would build for it (resolution, bounds, entries, device
+ * bytes).  msg (may be NULL) receives a NUL-terminated message of at most
+ * cap bytes on failure.  info may be NULL to validate only. */
+int mixrt_mesh_plan(const mixrt_mesh_desc *desc, mixrt_mesh_info *info, char *msg, size_t cap);
+
+/* Build the grid on the host (deterministic: each cell lists every triangle
+ * whose bounding box, padded by 1/500 of a cell, overlaps it, in ascending
+ * triangle order) and upload it to ctx's device: triangle records in cell
+ * order (v0, e1, e2 and the triangle index), cell offsets and per-triangle
+ * texture coordinates.  The mesh owns this device memory; the copies are
+ * synchronous, so desc's arrays may be released on return.  *out is NULL on
+ * failure (MIXRT_EINVAL for a bad descriptor, MIXRT_ENOMEM if the device
+ * memory cannot be allocated). */
+int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **out);
+
+/* Sizes of a created mesh (host only). */
+int mixrt_mesh_get_info(const mixrt_mesh *mesh, mixrt_mesh_info *info);
+
+/* Free the mesh's device memory.  NULL is a no-op.  Work that reads the
+ * mesh must have completed (hipFree synchronises the device). */
+int mixrt_mesh_destroy(mixrt_mesh *mesh);
+
+/* Ray-cast views * H * W pixels (the cameras and pixel rays of
+ * mixrt_render) against the mesh, writing the G-buffer mixrt_render reads:
+ * out_g0 (device float [views][H][W][4], 16-byte aligned) = (t, u, v, 0),
+ * with t the distance along the unit ray direction and (u, v) the
+ * barycentric interpolation of the hit triangle's vertex uv; a miss gets
+ * (-1, 0, 0, 0).  out_g1 (device float [views][H][W][4], or NULL) = the unit
+ * face normal and, in the fourth component, the bits of the int32 triangle
+ * index (-1 for a miss).  The mesh must have been created on ctx's device.
+ * Enqueued on the context's stream; no device memory is allocated. */
+int mixrt_raycast(mixrt_ctx *ctx, const mixrt_mesh *mesh, int32_t views, int32_t W, int32_t H,
+                  const mixrt_camera *cams, float *out_g0, float *out_g1);
+
 /* ---- errors ------------------------------------------------------------------- */
 
 /* Static description of a status code. */

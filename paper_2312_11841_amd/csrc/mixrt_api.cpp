@@ -2,7 +2,9 @@
 //
 // Host side: descriptor validation (pure host code, no HIP call), the level
 // resolution table, camera constants, and the launches of the kernels in
-// mixrt_render.hip and mixrt_stages.hip on the context's stream.
+// mixrt_render.hip and mixrt_stages.hip on the context's stream; the mesh
+// objects of the geometry stage (grid built in mixrt_mesh.cpp, kernel in
+// mixrt_raycast.hip).
 #include "mixrt.h"
 
 #include <hip/hip_runtime.h>
@@ -15,6 +17,7 @@
 #include <string>
 
 #include "mixrt_launch.hpp"
+#include "mixrt_mesh.hpp"
 
 struct mixrt_ctx {
     int device = 0;
@@ -22,6 +25,13 @@ struct mixrt_ctx {
     uint32_t flags = 0;
     int cus = 0;
     std::string err;
+};
+
+struct mixrt_mesh {
+    int device = 0;
+    void *mem = nullptr;           // one device allocation holding every array
+    mixrt::MeshGridK k{};
+    mixrt_mesh_info info{};
 };
 
 namespace {
@@ -80,6 +90,20 @@ int vfail(Msg m, int code, const char *fmt, ...)
     return code;
 }
 
+int check_cams(const mixrt_camera *cams, int views, Msg m)
+{
+    if (!cams) return vfail(m, MIXRT_EINVAL, "cams is NULL");
+    for (int v = 0; v < views; ++v) {
+        const mixrt_camera &c = cams[v];
+        if (!(c.fov_y_deg > 0.0f && c.fov_y_deg < 180.0f))
+            return vfail(m, MIXRT_EINVAL, "cams[%d].fov_y_deg=%g outside (0,180)", v, c.fov_y_deg);
+        for (int i = 0; i < 12; ++i)
+            if (!std::isfinite(c.c2w[i]))
+                return vfail(m, MIXRT_EINVAL, "cams[%d].c2w has a non-finite entry", v);
+    }
+    return MIXRT_OK;
+}
+
 int check_gbuf(const mixrt_gbuffer *g, const mixrt_camera *cams, Msg m)
 {
     if (!g) return vfail(m, MIXRT_EINVAL, "gbuf is NULL");
@@ -90,16 +114,7 @@ int check_gbuf(const mixrt_gbuffer *g, const mixrt_camera *cams, Msg m)
         return vfail(m, MIXRT_EUNSUPPORTED, "more than 2^31-1 pixels per call");
     if (!g->g0) return vfail(m, MIXRT_EINVAL, "gbuf.g0 is NULL");
     if (!aligned16(g->g0)) return vfail(m, MIXRT_EINVAL, "gbuf.g0 not 16-byte aligned");
-    if (!cams) return vfail(m, MIXRT_EINVAL, "cams is NULL");
-    for (int v = 0; v < g->views; ++v) {
-        const mixrt_camera &c = cams[v];
-        if (!(c.fov_y_deg > 0.0f && c.fov_y_deg < 180.0f))
-            return vfail(m, MIXRT_EINVAL, "cams[%d].fov_y_deg=%g outside (0,180)", v, c.fov_y_deg);
-        for (int i = 0; i < 12; ++i)
-            if (!std::isfinite(c.c2w[i]))
-                return vfail(m, MIXRT_EINVAL, "cams[%d].c2w has a non-finite entry", v);
-    }
-    return MIXRT_OK;
+    return check_cams(cams, g->views, m);
 }
 
 int disp_channels(const mixrt_disp_tex *d)
@@ -236,6 +251,22 @@ int validate_all(const mixrt_gbuffer *gbuf, const mixrt_camera *cams, const mixr
     return MIXRT_OK;
 }
 
+// Camera constants: rotation, centre, 1 / focal length in pixels, background.
+void fill_cams(mixrt::CamK *out, const mixrt_camera *cams, int views, int H)
+{
+    for (int v = 0; v < views; ++v) {
+        const mixrt_camera &c = cams[v];
+        mixrt::CamK &k = out[v];
+        for (int r = 0; r < 3; ++r) {
+            for (int q = 0; q < 3; ++q) k.R[3 * r + q] = c.c2w[4 * r + q];
+            k.o[r] = c.c2w[4 * r + 3];
+        }
+        const double half = 0.5 * (double)c.fov_y_deg * 3.14159265358979323846 / 180.0;
+        k.inv_f = (float)(std::tan(half) / (0.5 * (double)H));
+        for (int q = 0; q < 3; ++q) k.bg[q] = c.bg[q];
+    }
+}
+
 void fill_ray_params(mixrt::RayParams &rp, const mixrt_gbuffer *g, const mixrt_camera *cams,
                      const mixrt_disp_tex *d, const mixrt_sampling *s)
 {
@@ -258,17 +289,7 @@ void fill_ray_params(mixrt::RayParams &rp, const mixrt_gbuffer *g, const mixrt_c
     rp.K = s->K;
     rp.delta = s->delta;
     rp.t_term = s->t_term;
-    for (int v = 0; v < g->views; ++v) {
-        const mixrt_camera &c = cams[v];
-        mixrt::CamK &k = rp.cams[v];
-        for (int r = 0; r < 3; ++r) {
-            for (int q = 0; q < 3; ++q) k.R[3 * r + q] = c.c2w[4 * r + q];
-            k.o[r] = c.c2w[4 * r + 3];
-        }
-        const double half = 0.5 * (double)c.fov_y_deg * 3.14159265358979323846 / 180.0;
-        k.inv_f = (float)(std::tan(half) / (0.5 * (double)g->H));
-        for (int q = 0; q < 3; ++q) k.bg[q] = c.bg[q];
-    }
+    fill_cams(rp.cams, cams, g->views, g->H);
 }
 
 void fill_grid_params(mixrt::GridParams &gp, const mixrt_hash_grid *g)
@@ -326,6 +347,143 @@ const char *mixrt_status_string(int s)
     case MIXRT_EUNSUPPORTED: return "unsupported configuration";
     default: return "unknown status";
     }
+}
+
+int mixrt_mesh_plan(const mixrt_mesh_desc *desc, mixrt_mesh_info *info, char *msg, size_t cap)
+{
+    clear_err(nullptr);
+    if (msg && cap) msg[0] = 0;
+    mixrt::MeshGridHost g;
+    char buf[512] = "";
+    int rc = mixrt::build_mesh_grid(desc, false, g, buf, sizeof buf);
+    if (rc) {
+        if (msg && cap) snprintf(msg, cap, "%s", buf);
+        return fail(nullptr, rc, "%s", buf);
+    }
+    if (info) {
+        memset(info, 0, sizeof *info);
+        for (int a = 0; a < 3; ++a) {
+            info->grid_res[a] = g.n[a];
+            info->lo[a] = (float)g.lo[a];
+            info->hi[a] = (float)g.hi[a];
+        }
+        info->n_faces = desc->n_faces;
+        info->n_refs = g.n_refs;
+        info->device_bytes = mixrt::mesh_device_bytes(g, desc->n_faces);
+    }
+    return MIXRT_OK;
+}
+
+int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **out)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    if (!out) return fail(ctx, MIXRT_EINVAL, "out is NULL");
+    *out = nullptr;
+    mixrt::MeshGridHost g;
+    char buf[512] = "";
+    int rc = mixrt::build_mesh_grid(desc, true, g, buf, sizeof buf);
+    if (rc) return fail(ctx, rc, "%s", buf);
+    if ((rc = bind_device(ctx))) return rc;
+    const int64_t cells = (int64_t)g.n[0] * g.n[1] * g.n[2];
+    const int64_t b_start = ((cells + 1) * 4 + 255) & ~int64_t(255);
+    const int64_t b_refs = (g.n_refs * 48 + 255) & ~int64_t(255);
+    const int64_t bytes = mixrt::mesh_device_bytes(g, desc->n_faces);
+    mixrt_mesh *mesh = new (std::nothrow) mixrt_mesh;
+    if (!mesh) return fail(ctx, MIXRT_ENOMEM, "host allocation failed");
+    hipError_t e = hipMalloc(&mesh->mem, (size_t)bytes);
+    if (e != hipSuccess) {
+        delete mesh;
+        return fail(ctx, MIXRT_ENOMEM, "hipMalloc(%lld) for the mesh: %s", (long long)bytes,
+                    hipGetErrorString(e));
+    }
+    char *base = (char *)mesh->mem;
+    e = hipMemcpy(base, g.cell_start.data(), (size_t)(cells + 1) * 4, hipMemcpyHostToDevice);
+    if (e == hipSuccess && g.n_refs)
+        e = hipMemcpy(base + b_start, g.refs.data(), (size_t)g.n_refs * 48, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(base + b_start + b_refs, g.attr.data(), (size_t)desc->n_faces * 32,
+                      hipMemcpyHostToDevice);
+    if (e != hipSuccess) {
+        (void)hipFree(mesh->mem);
+        delete mesh;
+        return fail(ctx, MIXRT_EDEVICE, "mesh upload: %s", hipGetErrorString(e));
+    }
+    mesh->device = ctx->device;
+    mixrt::MeshGridK &k = mesh->k;
+    for (int a = 0; a < 3; ++a) {
+        k.lo[a] = (float)g.lo[a];
+        k.hi[a] = (float)g.hi[a];
+        k.cell[a] = (float)g.cell[a];
+        k.inv_cell[a] = (float)(1.0 / g.cell[a]);
+        k.n[a] = g.n[a];
+        mesh->info.grid_res[a] = g.n[a];
+        mesh->info.lo[a] = k.lo[a];
+        mesh->info.hi[a] = k.hi[a];
+    }
+    k.cell_start = (const uint32_t *)base;
+    k.refs = (const float4 *)(base + b_start);
+    k.attr = (const float4 *)(base + b_start + b_refs);
+    mesh->info.n_faces = desc->n_faces;
+    mesh->info.n_refs = g.n_refs;
+    mesh->info.device_bytes = bytes;
+    *out = mesh;
+    return MIXRT_OK;
+}
+
+int mixrt_mesh_get_info(const mixrt_mesh *mesh, mixrt_mesh_info *info)
+{
+    clear_err(nullptr);
+    if (!mesh || !info) return fail(nullptr, MIXRT_EINVAL, "mesh or info is NULL");
+    *info = mesh->info;
+    return MIXRT_OK;
+}
+
+int mixrt_mesh_destroy(mixrt_mesh *mesh)
+{
+    clear_err(nullptr);
+    if (!mesh) return MIXRT_OK;
+    int prev = 0;
+    hipError_t e = hipGetDevice(&prev);
+    if (e == hipSuccess) e = hipSetDevice(mesh->device);
+    if (e == hipSuccess) e = hipFree(mesh->mem);
+    (void)hipSetDevice(prev);
+    delete mesh;
+    if (e != hipSuccess) return fail(nullptr, MIXRT_EDEVICE, "mesh free: %s", hipGetErrorString(e));
+    return MIXRT_OK;
+}
+
+int mixrt_raycast(mixrt_ctx *ctx, const mixrt_mesh *mesh, int32_t views, int32_t W, int32_t H,
+                  const mixrt_camera *cams, float *out_g0, float *out_g1)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    if (!mesh) return fail(ctx, MIXRT_EINVAL, "mesh is NULL");
+    if (mesh->device != ctx->device)
+        return fail(ctx, MIXRT_EINVAL, "mesh lives on device %d, ctx on device %d", mesh->device,
+                    ctx->device);
+    if (views < 1 || views > MIXRT_MAX_VIEWS)
+        return fail(ctx, MIXRT_EINVAL, "views=%d outside 1..%d", views, MIXRT_MAX_VIEWS);
+    if (W < 1 || H < 1) return fail(ctx, MIXRT_EINVAL, "W=%d H=%d", W, H);
+    if ((int64_t)views * H * W >= ((int64_t)1 << 31))
+        return fail(ctx, MIXRT_EUNSUPPORTED, "more than 2^31-1 pixels per call");
+    char msg[512];
+    int rc = check_cams(cams, views, Msg{msg, sizeof msg});
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (!out_g0 || !aligned16(out_g0))
+        return fail(ctx, MIXRT_EINVAL, "out_g0 is NULL or not 16-byte aligned");
+    if (out_g1 && !aligned16(out_g1)) return fail(ctx, MIXRT_EINVAL, "out_g1 not 16-byte aligned");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::RaycastLaunch L;
+    memset(&L, 0, sizeof L);
+    L.grid = mesh->k;
+    fill_cams(L.cams, cams, views, H);
+    L.views = views;
+    L.W = W;
+    L.H = H;
+    L.g0 = (float4 *)out_g0;
+    L.g1 = (float4 *)out_g1;
+    return finish_launch(ctx, mixrt::launch_raycast(L, ctx->stream), "raycast");
 }
 
 const char *mixrt_last_error(const mixrt_ctx *ctx) { return ctx ? ctx->err.c_str() : ""; }

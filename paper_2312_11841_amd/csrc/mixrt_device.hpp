@@ -68,16 +68,12 @@ struct Ray {
     int32_t view;
 };
 
-__device__ __forceinline__ Ray pixel_ray(const RayParams &p, int32_t ray)
+// The ray through the centre of pixel (i, j) of a W x H view (Sec. 3.1).
+__device__ __forceinline__ Ray camera_ray(const CamK &c, int32_t W, int32_t H, uint32_t i,
+                                          uint32_t j)
 {
-    const uint32_t hw = (uint32_t)p.H * (uint32_t)p.W;
-    const uint32_t view = (uint32_t)ray / hw;
-    const uint32_t rem = (uint32_t)ray - view * hw;
-    const uint32_t j = rem / (uint32_t)p.W;
-    const uint32_t i = rem - j * (uint32_t)p.W;
-    const CamK &c = p.cams[view];
-    const float cx = ((float)i + 0.5f - 0.5f * (float)p.W) * c.inv_f;
-    const float cy = -(((float)j + 0.5f - 0.5f * (float)p.H) * c.inv_f);
+    const float cx = ((float)i + 0.5f - 0.5f * (float)W) * c.inv_f;
+    const float cy = -(((float)j + 0.5f - 0.5f * (float)H) * c.inv_f);
     float dx = c.R[0] * cx + c.R[1] * cy - c.R[2];
     float dy = c.R[3] * cx + c.R[4] * cy - c.R[5];
     float dz = c.R[6] * cx + c.R[7] * cy - c.R[8];
@@ -89,6 +85,18 @@ __device__ __forceinline__ Ray pixel_ray(const RayParams &p, int32_t ray)
     r.dx = dx * inv;
     r.dy = dy * inv;
     r.dz = dz * inv;
+    r.view = 0;
+    return r;
+}
+
+__device__ __forceinline__ Ray pixel_ray(const RayParams &p, int32_t ray)
+{
+    const uint32_t hw = (uint32_t)p.H * (uint32_t)p.W;
+    const uint32_t view = (uint32_t)ray / hw;
+    const uint32_t rem = (uint32_t)ray - view * hw;
+    const uint32_t j = rem / (uint32_t)p.W;
+    const uint32_t i = rem - j * (uint32_t)p.W;
+    Ray r = camera_ray(p.cams[view], p.W, p.H, i, j);
     r.view = (int32_t)view;
     return r;
 }

@@ -1,0 +1,65 @@
+// Internal interface of the geometry stage: the uniform grid of triangle
+// lists (built on the host in mixrt_mesh.cpp) and the ray-casting kernel
+// that walks it (mixrt_raycast.hip) to produce the G-buffer of the coarse
+// mesh (Fig. 2 step 1).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <vector>
+
+#include "mixrt.h"
+#include "mixrt_device.hpp"
+
+namespace mixrt {
+
+inline constexpr int kMaxGridAxis = 1024;
+inline constexpr int64_t kMaxGridCells = int64_t(1) << 26;
+// Triangle boxes are padded by this fraction of a cell when binned, so that
+// a hit computed in fp32 near a cell face is listed in the cell on either side.
+inline constexpr double kBinPad = 1.0 / 500.0;
+
+// Device view of an uploaded mesh.  Cell (x, y, z) is index (z*ny + y)*nx + x;
+// its triangles are refs[cell_start[c] .. cell_start[c+1]).  A ref is three
+// float4: (v0, triangle index bits), (e1, 0), (e2, 0).  attr[tri] is two
+// float4: (uv0, uv1), (uv2, 0, 0).
+struct MeshGridK {
+    float lo[3], hi[3], cell[3], inv_cell[3];
+    int32_t n[3];
+    const uint32_t *cell_start;
+    const float4 *refs;
+    const float4 *attr;
+};
+
+// The grid as built on the host, before upload.
+struct MeshGridHost {
+    int32_t n[3] = {0, 0, 0};
+    double lo[3] = {0, 0, 0}, hi[3] = {0, 0, 0}, cell[3] = {0, 0, 0};
+    int64_t n_refs = 0;
+    std::vector<uint32_t> cell_start;   // cells + 1
+    std::vector<float> refs;            // n_refs * 12
+    std::vector<float> attr;            // n_faces * 8
+};
+
+// Validate desc and choose bounds and resolution; with fill, also count and
+// fill the cell lists (otherwise only n_refs is computed).  Returns a
+// mixrt_status and writes a message to msg on failure.
+int build_mesh_grid(const mixrt_mesh_desc *desc, bool fill, MeshGridHost &g, char *msg,
+                    size_t cap);
+
+// Bytes of device memory an uploaded grid occupies (each array 256-aligned).
+int64_t mesh_device_bytes(const MeshGridHost &g, int64_t n_faces);
+
+struct RaycastLaunch {
+    MeshGridK grid;
+    CamK cams[MIXRT_MAX_VIEWS];
+    int32_t views, W, H;
+    float4 *g0;
+    float4 *g1;
+};
+
+hipError_t launch_raycast(const RaycastLaunch &L, hipStream_t stream);
+
+}  // namespace mixrt

@@ -32,8 +32,11 @@ EXPORTS = (
     "mixrt_create", "mixrt_destroy", "mixrt_sync", "mixrt_validate",
     "mixrt_level_resolutions", "mixrt_render", "mixrt_debug_ray_setup",
     "mixrt_debug_hash_encode", "mixrt_debug_mlp", "mixrt_debug_composite",
+    "mixrt_mesh_plan", "mixrt_mesh_create", "mixrt_mesh_get_info", "mixrt_mesh_destroy",
+    "mixrt_raycast",
     "mixrt_status_string", "mixrt_last_error", "mixrt_thread_error",
 )
+RAY_T_MIN = 1e-4
 
 
 class MixrtUnavailable(RuntimeError):
@@ -82,6 +85,17 @@ class Sampling(C.Structure):
     _fields_ = [("K", C.c_int32), ("delta", C.c_float), ("t_term", C.c_float)]
 
 
+class MeshDesc(C.Structure):
+    _fields_ = [("n_vertices", C.c_int64), ("n_faces", C.c_int64), ("positions", C.c_void_p),
+                ("faces", C.c_void_p), ("uv", C.c_void_p), ("grid_res", C.c_int32 * 3),
+                ("cells_per_face", C.c_float)]
+
+
+class MeshInfo(C.Structure):
+    _fields_ = [("grid_res", C.c_int32 * 3), ("lo", C.c_float * 3), ("hi", C.c_float * 3),
+                ("n_faces", C.c_int64), ("n_refs", C.c_int64), ("device_bytes", C.c_int64)]
+
+
 _lib = None
 
 
@@ -112,6 +126,13 @@ def lib():
             "mixrt_debug_hash_encode": (C.c_int, [P, C.POINTER(HashGrid), P, I64, P, P, P, P]),
             "mixrt_debug_mlp": (C.c_int, [P, C.POINTER(Mlp), P, I64, P]),
             "mixrt_debug_composite": (C.c_int, [P, P, I64, C.POINTER(Sampling), P, P]),
+            "mixrt_mesh_plan": (C.c_int, [C.POINTER(MeshDesc), C.POINTER(MeshInfo), C.c_char_p,
+                                          C.c_size_t]),
+            "mixrt_mesh_create": (C.c_int, [P, C.POINTER(MeshDesc), C.POINTER(C.c_void_p)]),
+            "mixrt_mesh_get_info": (C.c_int, [P, C.POINTER(MeshInfo)]),
+            "mixrt_mesh_destroy": (C.c_int, [P]),
+            "mixrt_raycast": (C.c_int, [P, P, C.c_int32, C.c_int32, C.c_int32,
+                                        C.POINTER(Camera), P, P]),
             "mixrt_status_string": (C.c_char_p, [C.c_int]),
             "mixrt_last_error": (C.c_char_p, [P]),
             "mixrt_thread_error": (C.c_char_p, []),
@@ -216,6 +237,59 @@ class DeviceScene:
                    mlp, smp, cfg.rays)
 
 
+# --- meshes (the geometry stage) ---------------------------------------------------
+
+def make_mesh_desc(positions, faces, uv=None, grid_res=(0, 0, 0), cells_per_face=0.0):
+    """Descriptor of host arrays; returns (desc, keep) where keep holds the
+    contiguous copies the descriptor points to."""
+    pos = np.ascontiguousarray(positions, np.float32)
+    fc = np.ascontiguousarray(faces, np.int32)
+    uvc = None if uv is None else np.ascontiguousarray(uv, np.float32)
+    d = MeshDesc(pos.shape[0], fc.shape[0], pos.ctypes.data, fc.ctypes.data,
+                 None if uvc is None else uvc.ctypes.data, (C.c_int32 * 3)(*grid_res),
+                 float(cells_per_face))
+    return d, (pos, fc, uvc)
+
+
+def _info_dict(info: MeshInfo) -> dict:
+    return {"grid_res": tuple(info.grid_res), "lo": tuple(info.lo), "hi": tuple(info.hi),
+            "n_faces": info.n_faces, "n_refs": info.n_refs, "device_bytes": info.device_bytes}
+
+
+def mesh_plan(positions, faces, uv=None, grid_res=(0, 0, 0), cells_per_face=0.0):
+    """Pure-host grid plan: (status, message, info dict or None)."""
+    d, _keep = make_mesh_desc(positions, faces, uv, grid_res, cells_per_face)
+    info = MeshInfo()
+    buf = C.create_string_buffer(512)
+    rc = lib().mixrt_mesh_plan(C.byref(d), C.byref(info), buf, 512)
+    return rc, buf.value.decode(), (_info_dict(info) if rc == MIXRT_OK else None)
+
+
+class DeviceMesh:
+    """A mesh uploaded into the ray-casting grid; owns its device memory."""
+
+    def __init__(self, renderer: "Renderer", mesh, grid_res=(0, 0, 0), cells_per_face=0.0):
+        d, _keep = make_mesh_desc(mesh.positions, mesh.faces, getattr(mesh, "uv", None),
+                                  grid_res, cells_per_face)
+        h = C.c_void_p()
+        renderer._check(lib().mixrt_mesh_create(renderer._h, C.byref(d), C.byref(h)))
+        self._h = h
+        info = MeshInfo()
+        lib().mixrt_mesh_get_info(h, C.byref(info))
+        self.info = _info_dict(info)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().mixrt_mesh_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 # --- the library handle ------------------------------------------------------------
 
 class Renderer:
@@ -262,6 +336,22 @@ class Renderer:
                                        C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp),
                                        _ptr(out)))
         return out
+
+    # -- geometry
+    def raycast(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):
+        """G-buffer of views x H x W pixels: (g0, g1) device float [views, H, W, 4]
+        (g1 None unless asked for)."""
+        import torch
+        cam_arr = cams if isinstance(cams, C.Array) else make_cameras(np.asarray(cams))
+        views = len(cam_arr)
+        dev = torch.device("cuda", self.device)
+        if out is None:
+            out = (torch.empty((views, H, W, 4), dtype=torch.float32, device=dev),
+                   torch.empty((views, H, W, 4), dtype=torch.float32, device=dev) if g1 else None)
+        g0t, g1t = out
+        self._check(lib().mixrt_raycast(self._h, mesh._h, views, W, H, cam_arr, _ptr(g0t),
+                                        _ptr(g1t)))
+        return g0t, g1t
 
     # -- stage entry points
     def ray_setup(self, ds: DeviceScene):

@@ -47,7 +47,8 @@ class SceneConfig:
     W: int
     K: int
     delta: float
-    gbuf: str                 # "iid" (cache-hostile) or "room" (coherent)
+    gbuf: str                 # "iid" (cache-hostile), "room" (coherent) or
+                              # "mesh" (computed by ray casting `mesh_seed`'s mesh)
     tex_R: int
     tex_V: int
     tex_dtype: str            # "f32" | "f16"
@@ -72,6 +73,8 @@ class SceneConfig:
                               # printed (SH vector x scale map); "none"
     sh_degree: int = 0        # "vec3": SH degree D, 3 (D+1)^2 channels
     scale_range: tuple = (0.0, 1.0)  # "vec3": scale map values
+    mesh_seed: int = -1       # "mesh": seed of make_mesh
+    mesh_args: tuple = ()     # "mesh": other make_mesh arguments, (name, value) pairs
 
     @property
     def T(self) -> int:
@@ -187,9 +190,22 @@ TABLE3 = [table3_config(8, 17, True), table3_config(8, 17, False), table3_config
           table3_config(8, 5, False), table3_config(8, 22, False)]
 LEVEL_SWEEP = [table3_config(L, 17, False) for L in (1, 2, 4, 8, 16)]
 
+# The whole pipeline including geometry: a seeded 499,712-triangle mesh (a
+# perturbed-sphere room of radius 6 with 24 perturbed spheres and 16 boxes,
+# 11 MB) ray-cast per pixel into the G-buffer, then view720p's displacement,
+# grid, MLP and compositing at 1280x720.
+MESH720P = VIEW720P.replace(name="mesh720p", gbuf="mesh", mesh_seed=7)
+# Small enough for the oracle's brute-force ray casting of every pixel
+# (1,280 + 6 x 320 + 4 x 108 = 3,632 triangles).
+TINY64_MESH = TINY64_DENSE.replace(
+    name="tiny64_mesh", gbuf="mesh", mesh_seed=8, seed=16,
+    mesh_args=(("room_level", 3), ("n_objects", 6), ("object_level", 2), ("n_boxes", 4),
+               ("box_div", 3)))
+
 CONFIGS = {c.name: c for c in (TINY64, TINY64_DENSE, VIEW720P, VIEW720P_DENSE,
                                BATCH8X1080P, DEPLOYED720P, PAPER720P, PAPER720P_NOVDD,
-                               TINY64_VEC3, TINY64_U8, TINY64_NODISP, *TABLE3, *LEVEL_SWEEP)}
+                               TINY64_VEC3, TINY64_U8, TINY64_NODISP, MESH720P, TINY64_MESH,
+                               *TABLE3, *LEVEL_SWEEP)}
 
 
 # --- scene container ----------------------------------------------------------
@@ -207,6 +223,8 @@ class Scene:
     q_scale: tuple = (0.0, 0.0)   # 8-bit maps: value = q_offset + q_scale * q
     q_offset: tuple = (0.0, 0.0)  # ([0] coefficient map, [1] scale map)
     extra: dict = field(default_factory=dict)
+    mesh: "Mesh" = None       # "mesh" workloads: the geometry; g0/g1 then hold
+                              # misses until a ray cast fills them
 
     @property
     def weights_flat(self) -> np.ndarray:
@@ -352,8 +370,15 @@ def make_scene(cfg: SceneConfig) -> Scene:
     """Draw every input of `cfg` in a fixed order: G-buffer, camera, texture,
     table, weights."""
     rng = np.random.default_rng(cfg.seed)
+    mesh = None
     if cfg.gbuf == "iid":
         g0, g1 = _iid_gbuffer(cfg, rng)
+    elif cfg.gbuf == "mesh":
+        mesh = make_mesh(cfg.mesh_seed, **dict(cfg.mesh_args))
+        shape = (cfg.views, cfg.rows_kept, cfg.W, 4)
+        g0 = np.zeros(shape, np.float32)
+        g0[..., 0] = -1.0
+        g1 = np.zeros(shape, np.float32)
     else:
         g0, g1 = _room_gbuffer(cfg, rng)
     cams = _camera_rows(cfg, rng)
@@ -386,7 +411,7 @@ def make_scene(cfg: SceneConfig) -> Scene:
                  cams=cams, tex=np.ascontiguousarray(tex),
                  table=np.ascontiguousarray(table), weights=weights,
                  scale=None if scale is None else np.ascontiguousarray(scale),
-                 q_scale=q_scale, q_offset=q_offset)
+                 q_scale=q_scale, q_offset=q_offset, mesh=mesh)
 
 
 def dtype_code(name: str) -> int:

@@ -39,7 +39,8 @@ def test_struct_layout_matches_header():
     structs = {"mixrt_create_info": mixrt.CreateInfo, "mixrt_gbuffer": mixrt.GBuffer,
                "mixrt_camera": mixrt.Camera, "mixrt_disp_tex": mixrt.DispTex,
                "mixrt_hash_grid": mixrt.HashGrid, "mixrt_mlp": mixrt.Mlp,
-               "mixrt_sampling": mixrt.Sampling}
+               "mixrt_sampling": mixrt.Sampling, "mixrt_mesh_desc": mixrt.MeshDesc,
+               "mixrt_mesh_info": mixrt.MeshInfo}
     lines = ['#include <stdio.h>', '#include <stddef.h>', '#include "mixrt.h"', "int main(void){"]
     for cname, py in structs.items():
         lines.append(f'printf("{cname} size %zu\\n", sizeof({cname}));')
@@ -186,3 +187,85 @@ def test_library_level_table_equals_oracle(L, nmin, nmax):
 def test_level_table_rejects_bad_grid():
     with pytest.raises(mixrt.MixrtError):
         mixrt.level_resolutions(mixrt.HashGrid(0, 19, 2, 16, 256, 1, FAKE))
+
+
+# --- the geometry stage's grid plan (pure host) ---------------------------------
+
+def _plan_refs_numpy(pos, faces, res, lo, hi):
+    """The binning rule restated: a triangle is listed in each cell of its
+    bounding box padded by 1/500 cell whose padded box its plane crosses."""
+    pos = pos.astype(np.float64)
+    lo, hi, res = np.array(lo, np.float64), np.array(hi, np.float64), np.array(res)
+    cell = (hi - lo) / res
+    pad = cell / 500.0
+    half = cell * (0.5 + 1.0 / 500.0)
+    total = 0
+    for f in faces:
+        P = pos[f]
+        c0 = np.clip(np.floor((P.min(0) - pad - lo) * res / (hi - lo)).astype(int), 0, res - 1)
+        c1 = np.clip(np.floor((P.max(0) + pad - lo) * res / (hi - lo)).astype(int), 0, res - 1)
+        if np.all(c0 == c1):
+            total += 1
+            continue
+        n = np.cross(P[1] - P[0], P[2] - P[0])
+        reach = np.abs(n) @ half
+        g = np.stack(np.meshgrid(*[np.arange(a, b + 1) for a, b in zip(c0, c1)], indexing="ij"), -1)
+        ctr = lo + (g.reshape(-1, 3) + 0.5) * cell
+        total += int(np.sum(np.abs((ctr - P[0]) @ n) <= reach * (1 + 1e-9)))
+    return total
+
+
+def test_mesh_plan_automatic_grid():
+    m = synth.make_mesh(3, room_level=3, n_objects=4, object_level=2, n_boxes=3, box_div=4)
+    rc, msg, info = mixrt.mesh_plan(m.positions, m.faces, m.uv)
+    assert rc == mixrt.MIXRT_OK, msg
+    lo, hi, res = np.array(info["lo"]), np.array(info["hi"]), np.array(info["grid_res"])
+    assert np.all(lo < m.positions.min(0)) and np.all(hi > m.positions.max(0))
+    cells = np.prod(res)
+    assert 0.5 * 2 * len(m.faces) < cells < 2.0 * 2 * len(m.faces)   # about 2 cells per face
+    assert info["n_faces"] == len(m.faces)
+    assert info["n_refs"] == _plan_refs_numpy(m.positions, m.faces, res, lo, hi)
+    assert info["device_bytes"] >= 4 * (cells + 1) + 48 * info["n_refs"] + 32 * len(m.faces)
+    rc, _, dense = mixrt.mesh_plan(m.positions, m.faces, m.uv, cells_per_face=8.0)
+    assert np.prod(dense["grid_res"]) > 2 * cells
+
+
+def test_mesh_plan_explicit_grid_and_flat_mesh():
+    pos = np.array([[-1, -1, -2], [3, -1, -2], [-1, 3, -2]], np.float32)
+    faces = np.array([[0, 1, 2]], np.int32)
+    rc, msg, info = mixrt.mesh_plan(pos, faces, grid_res=(7, 5, 3))
+    assert rc == mixrt.MIXRT_OK, msg
+    assert info["grid_res"] == (7, 5, 3)
+    assert info["hi"][2] > info["lo"][2]                     # a flat mesh gets a thick box
+    assert info["n_refs"] == _plan_refs_numpy(pos, faces, (7, 5, 3), info["lo"], info["hi"])
+    rc, msg, info = mixrt.mesh_plan(pos, faces, grid_res=(1, 1, 1))
+    assert rc == mixrt.MIXRT_OK and info["n_refs"] == 1
+
+
+MESH_BAD = [
+    ("index high", lambda p, f, kw: f.__setitem__((0, 1), len(p)), mixrt.MIXRT_EINVAL),
+    ("index negative", lambda p, f, kw: f.__setitem__((0, 2), -1), mixrt.MIXRT_EINVAL),
+    ("nan vertex", lambda p, f, kw: p.__setitem__((1, 0), np.nan), mixrt.MIXRT_EINVAL),
+    ("partial grid_res", lambda p, f, kw: kw.update(grid_res=(4, 0, 4)), mixrt.MIXRT_EINVAL),
+    ("grid axis > 1024", lambda p, f, kw: kw.update(grid_res=(1025, 1, 1)), mixrt.MIXRT_EINVAL),
+    ("grid > 2^26 cells", lambda p, f, kw: kw.update(grid_res=(1024, 1024, 65)), mixrt.MIXRT_EINVAL),
+    ("cells_per_face < 0", lambda p, f, kw: kw.update(cells_per_face=-1.0), mixrt.MIXRT_EINVAL),
+    ("cells_per_face nan", lambda p, f, kw: kw.update(cells_per_face=float("nan")), mixrt.MIXRT_EINVAL),
+]
+
+
+@pytest.mark.parametrize("name,mutate,code", MESH_BAD, ids=[b[0] for b in MESH_BAD])
+def test_mesh_plan_rejects(name, mutate, code):
+    m = synth.make_mesh(3, room_level=1, n_objects=1, object_level=0, n_boxes=1, box_div=1)
+    pos, faces, kw = m.positions.copy(), m.faces.copy(), {}
+    mutate(pos, faces, kw)
+    rc, msg, info = mixrt.mesh_plan(pos, faces, m.uv, **kw)
+    assert rc == code and msg and info is None
+
+
+def test_mesh_plan_rejects_null_and_tiny():
+    rc = mixrt.lib().mixrt_mesh_plan(None, None, None, 0)
+    assert rc == mixrt.MIXRT_EINVAL
+    d = mixrt.MeshDesc(2, 1, 0, 0, None, (C.c_int32 * 3)(0, 0, 0), 0.0)
+    assert mixrt.lib().mixrt_mesh_plan(C.byref(d), None, None, 0) == mixrt.MIXRT_EINVAL
+    assert b"n_vertices" in mixrt.lib().mixrt_thread_error()
