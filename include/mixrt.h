@@ -256,7 +256,7 @@ typedef struct {
     int32_t grid_res[3];     /* cells per axis (1..1024 each, at most 2^26 in all),
                                 or all 0: chosen from the bounds so that the
                                 grid has about cells_per_face * n_faces cells */
-    float cells_per_face;    /* for grid_res = 0; 0 means 2 */
+    float cells_per_face;    /* for grid_res = 0; 0 means 8 */
 } mixrt_mesh_desc;
 
 typedef struct {
@@ -274,10 +274,12 @@ typedef struct {
 int mixrt_mesh_plan(const mixrt_mesh_desc *desc, mixrt_mesh_info *info, char *msg, size_t cap);
 
 /* Build the grid on the host (deterministic: each cell lists every triangle
- * whose bounding box, padded by 1/500 of a cell, overlaps it, in ascending
- * triangle order) and upload it to ctx's device: triangle records in cell
- * order (v0, e1, e2 and the triangle index), cell offsets and per-triangle
- * texture coordinates.  The mesh owns this device memory; the copies are
+ * whose plane crosses the cell and whose bounding box overlaps it, both with
+ * the cell padded by 1/500 of its size, in ascending triangle order; empty
+ * cells hold their Chebyshev distance to the nearest listed cell, which lets
+ * the walk leap across empty space) and upload it to ctx's device: triangle
+ * records in cell order (v0, e1, e2 and the triangle index), cell records
+ * and per-triangle texture coordinates.  The mesh owns this device memory; the copies are
  * synchronous, so desc's arrays may be released on return.  *out is NULL on
  * failure (MIXRT_EINVAL for a bad descriptor, MIXRT_ENOMEM if the device
  * memory cannot be allocated). */

@@ -386,7 +386,7 @@ int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **
     if (rc) return fail(ctx, rc, "%s", buf);
     if ((rc = bind_device(ctx))) return rc;
     const int64_t cells = (int64_t)g.n[0] * g.n[1] * g.n[2];
-    const int64_t b_start = ((cells + 1) * 4 + 255) & ~int64_t(255);
+    const int64_t b_cells = (cells * 8 + 255) & ~int64_t(255);
     const int64_t b_refs = (g.n_refs * 48 + 255) & ~int64_t(255);
     const int64_t bytes = mixrt::mesh_device_bytes(g, desc->n_faces);
     mixrt_mesh *mesh = new (std::nothrow) mixrt_mesh;
@@ -398,11 +398,11 @@ int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **
                     hipGetErrorString(e));
     }
     char *base = (char *)mesh->mem;
-    e = hipMemcpy(base, g.cell_start.data(), (size_t)(cells + 1) * 4, hipMemcpyHostToDevice);
+    e = hipMemcpy(base, g.cells.data(), (size_t)cells * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess && g.n_refs)
-        e = hipMemcpy(base + b_start, g.refs.data(), (size_t)g.n_refs * 48, hipMemcpyHostToDevice);
+        e = hipMemcpy(base + b_cells, g.refs.data(), (size_t)g.n_refs * 48, hipMemcpyHostToDevice);
     if (e == hipSuccess)
-        e = hipMemcpy(base + b_start + b_refs, g.attr.data(), (size_t)desc->n_faces * 32,
+        e = hipMemcpy(base + b_cells + b_refs, g.attr.data(), (size_t)desc->n_faces * 32,
                       hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(mesh->mem);
@@ -421,9 +421,9 @@ int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **
         mesh->info.lo[a] = k.lo[a];
         mesh->info.hi[a] = k.hi[a];
     }
-    k.cell_start = (const uint32_t *)base;
-    k.refs = (const float4 *)(base + b_start);
-    k.attr = (const float4 *)(base + b_start + b_refs);
+    k.cells = (const uint2 *)base;
+    k.refs = (const float4 *)(base + b_cells);
+    k.attr = (const float4 *)(base + b_cells + b_refs);
     mesh->info.n_faces = desc->n_faces;
     mesh->info.n_refs = g.n_refs;
     mesh->info.device_bytes = bytes;

@@ -77,6 +77,42 @@ void for_cells(const MeshGridHost &g, const double p[3][3], F &&visit)
             }
 }
 
+// Chebyshev distance transform of the occupancy: dist 0 on cells with
+// triangles, else the largest D (capped at 255) such that every cell within
+// D-1 on each axis is empty.  Two raster passes with the 26-neighbourhood
+// give the exact chessboard distance; cells beyond the grid count as empty.
+void chessboard_distance(const int32_t n[3], std::vector<uint8_t> &dist)
+{
+    const int nx = n[0], ny = n[1], nz = n[2];
+    auto at = [&](int x, int y, int z) -> uint8_t & {
+        return dist[((int64_t)z * ny + y) * nx + x];
+    };
+    for (int pass = 0; pass < 2; ++pass) {
+        const int s = pass == 0 ? 1 : -1;
+        for (int zi = 0; zi < nz; ++zi)
+            for (int yi = 0; yi < ny; ++yi)
+                for (int xi = 0; xi < nx; ++xi) {
+                    const int x = pass == 0 ? xi : nx - 1 - xi;
+                    const int y = pass == 0 ? yi : ny - 1 - yi;
+                    const int z = pass == 0 ? zi : nz - 1 - zi;
+                    uint8_t &d = at(x, y, z);
+                    if (d == 0) continue;
+                    int best = d;
+                    // the 13 neighbours already visited in this pass's order
+                    for (int dz = -1; dz <= 0; ++dz)
+                        for (int dy = -1; dy <= 1; ++dy)
+                            for (int dx = -1; dx <= 1; ++dx) {
+                                if (dz == 0 && (dy > 0 || (dy == 0 && dx >= 0))) continue;
+                                const int X = x + s * dx, Y = y + s * dy, Z = z + s * dz;
+                                if (X < 0 || Y < 0 || Z < 0 || X >= nx || Y >= ny || Z >= nz)
+                                    continue;
+                                best = std::min(best, at(X, Y, Z) + 1);
+                            }
+                    d = (uint8_t)std::min(best, 255);
+                }
+    }
+}
+
 void load_tri(const mixrt_mesh_desc *d, int64_t f, double p[3][3])
 {
     for (int k = 0; k < 3; ++k) {
@@ -90,7 +126,7 @@ void load_tri(const mixrt_mesh_desc *d, int64_t f, double p[3][3])
 int64_t mesh_device_bytes(const MeshGridHost &g, int64_t n_faces)
 {
     const int64_t cells = (int64_t)g.n[0] * g.n[1] * g.n[2];
-    return align256((cells + 1) * 4) + align256(g.n_refs * 48) + align256(n_faces * 32);
+    return align256(cells * 8) + align256(g.n_refs * 48) + align256(n_faces * 32);
 }
 
 int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *msg, size_t cap)
@@ -150,7 +186,7 @@ int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *
         ext[a] = (double)(float)(hi[a] + pad) - g.lo[a];
     }
     if (autores) {
-        const double cpf = d->cells_per_face > 0.0f ? d->cells_per_face : 2.0;
+        const double cpf = d->cells_per_face > 0.0f ? d->cells_per_face : 8.0;
         double s = cbrt(cpf * (double)d->n_faces / (ext[0] * ext[1] * ext[2]));
         for (;;) {
             int64_t cells = 1;
@@ -171,7 +207,7 @@ int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *
     }
 
     const int64_t cells = (int64_t)g.n[0] * g.n[1] * g.n[2];
-    std::vector<uint32_t> count(cells + 1, 0);
+    std::vector<uint32_t> count(fill ? cells : 0, 0);
     int64_t refs = 0;
     double p[3][3];
     for (int64_t f = 0; f < d->n_faces; ++f) {
@@ -187,9 +223,20 @@ int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *
     g.n_refs = refs;
     if (!fill) return MIXRT_OK;
 
-    g.cell_start.assign(cells + 1, 0);
-    for (int64_t c = 0; c < cells; ++c) g.cell_start[c + 1] = g.cell_start[c] + count[c];
-    std::vector<uint32_t> cursor(g.cell_start.begin(), g.cell_start.end() - 1);
+    std::vector<uint32_t> cursor(cells);
+    std::vector<uint8_t> dist(cells);
+    uint32_t first = 0;
+    for (int64_t c = 0; c < cells; ++c) {
+        cursor[c] = first;
+        first += count[c];
+        dist[c] = count[c] ? 0 : 255;
+    }
+    chessboard_distance(g.n, dist);
+    g.cells.assign(2 * cells, 0);
+    for (int64_t c = 0; c < cells; ++c) {
+        g.cells[2 * c] = count[c] ? cursor[c] : dist[c];
+        g.cells[2 * c + 1] = count[c];
+    }
     g.refs.assign(refs * 12, 0.0f);
     for (int64_t f = 0; f < d->n_faces; ++f) {
         load_tri(d, f, p);

@@ -21,14 +21,17 @@ inline constexpr int64_t kMaxGridCells = int64_t(1) << 26;
 // a hit computed in fp32 near a cell face is listed in the cell on either side.
 inline constexpr double kBinPad = 1.0 / 500.0;
 
-// Device view of an uploaded mesh.  Cell (x, y, z) is index (z*ny + y)*nx + x;
-// its triangles are refs[cell_start[c] .. cell_start[c+1]).  A ref is three
-// float4: (v0, triangle index bits), (e1, 0), (e2, 0).  attr[tri] is two
-// float4: (uv0, uv1), (uv2, 0, 0).
+// Device view of an uploaded mesh.  Cell (x, y, z) is index (z*ny + y)*nx + x
+// and cells[c] = (first, count): a cell with triangles lists them in
+// refs[first .. first+count); an empty cell (count 0) holds in `first` its
+// Chebyshev distance D (in cells, 1..255) to the nearest cell with
+// triangles, so every cell within D-1 of it on each axis is empty as well.
+// A ref is three float4: (v0, triangle index bits), (e1, 0), (e2, 0).
+// attr[tri] is two float4: (uv0, uv1), (uv2, 0, 0).
 struct MeshGridK {
     float lo[3], hi[3], cell[3], inv_cell[3];
     int32_t n[3];
-    const uint32_t *cell_start;
+    const uint2 *cells;
     const float4 *refs;
     const float4 *attr;
 };
@@ -38,7 +41,7 @@ struct MeshGridHost {
     int32_t n[3] = {0, 0, 0};
     double lo[3] = {0, 0, 0}, hi[3] = {0, 0, 0}, cell[3] = {0, 0, 0};
     int64_t n_refs = 0;
-    std::vector<uint32_t> cell_start;   // cells + 1
+    std::vector<uint32_t> cells;        // 2 per cell: (first or distance, count)
     std::vector<float> refs;            // n_refs * 12
     std::vector<float> attr;            // n_faces * 8
 };

@@ -3,6 +3,9 @@
 // walks the uniform grid's cells in the order the ray crosses them (3D DDA),
 // intersects the triangles listed in each cell (Moller-Trumbore in fp32) and
 // stops after the first cell whose exit distance is beyond the closest hit.
+// Empty space is crossed in leaps: an empty cell at Chebyshev distance D from
+// the nearest occupied cell sits in a cube of (2D-1)^3 empty cells, so the ray
+// moves straight to the face where it leaves that cube.
 //
 // Launch shape: one 256-lane block per 16 x 16 pixel tile, each wave an 8 x 8
 // quadrant, so the 64 rays of a wave cross nearly the same cells and their
@@ -24,10 +27,18 @@ struct Hit {
     uint32_t ref;
 };
 
-__device__ __forceinline__ void test_ref(const float4 *__restrict__ refs, uint32_t r, const Ray &ray,
-                                         Hit &h)
+struct Tri {
+    float4 a, e1, e2;
+};
+
+__device__ __forceinline__ Tri load_tri(const float4 *__restrict__ refs, uint32_t r)
 {
-    const float4 A = refs[3 * r], E1 = refs[3 * r + 1], E2 = refs[3 * r + 2];
+    return Tri{refs[3 * r], refs[3 * r + 1], refs[3 * r + 2]};
+}
+
+__device__ __forceinline__ void test_tri(const Tri &T, uint32_t r, const Ray &ray, Hit &h)
+{
+    const float4 &A = T.a, &E1 = T.e1, &E2 = T.e2;
     const float px = ray.dy * E2.z - ray.dz * E2.y;
     const float py = ray.dz * E2.x - ray.dx * E2.z;
     const float pz = ray.dx * E2.y - ray.dy * E2.x;
@@ -60,6 +71,71 @@ __device__ __forceinline__ float next_face(const MeshGridK &g, int a, int c, int
     return (g.lo[a] + (float)(c + (step > 0)) * g.cell[a] - o) * inv;
 }
 
+// The walk's state: current cell, step direction and the distance to the
+// next face on each axis.
+struct Walk {
+    int c[3], st[3];
+    float tn[3];
+};
+
+// Move to the next cell: one DDA step (leap <= 1), or out of the empty cube
+// c +- (leap - 1) through its nearest face, where that axis moves leap cells
+// and the others go to the cell holding the exit point, kept inside the cube
+// and never moved backwards.  False once the ray leaves the grid.
+__device__ __forceinline__ bool advance(const MeshGridK &g, const float o[3], const float d[3],
+                                        const float inv[3], int leap, Walk &w)
+{
+    if (leap <= 1) {
+        const int ax = (w.tn[0] <= w.tn[1] && w.tn[0] <= w.tn[2]) ? 0 : (w.tn[1] <= w.tn[2] ? 1 : 2);
+        int ca = 0;
+#pragma unroll
+        for (int a = 0; a < 3; ++a)
+            if (a == ax) ca = w.c[a] + w.st[a];
+        if (ca < 0 || ca >= g.n[ax]) return false;
+#pragma unroll
+        for (int a = 0; a < 3; ++a)
+            if (a == ax) {
+                w.c[a] = ca;
+                w.tn[a] = next_face(g, a, ca, w.st[a], o[a], inv[a]);
+            }
+        return true;
+    }
+    float te[3];
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+        te[a] = w.st[a] ? next_face(g, a, w.c[a] + w.st[a] * (leap - 1), w.st[a], o[a], inv[a]) : kInf;
+    const int ax = (te[0] <= te[1] && te[0] <= te[2]) ? 0 : (te[1] <= te[2] ? 1 : 2);
+    const float t = fminf(te[0], fminf(te[1], te[2]));
+    bool out = false;
+#pragma unroll
+    for (int a = 0; a < 3; ++a) {
+        int ca;
+        if (a == ax) {
+            ca = w.c[a] + w.st[a] * leap;
+        } else if (w.st[a] == 0) {
+            ca = w.c[a];
+        } else {
+            ca = (int)floorf((o[a] + t * d[a] - g.lo[a]) * g.inv_cell[a]);
+            const int lo_a = w.st[a] > 0 ? w.c[a] : w.c[a] - (leap - 1);
+            const int hi_a = w.st[a] < 0 ? w.c[a] : w.c[a] + (leap - 1);
+            ca = min(max(ca, lo_a), hi_a);
+        }
+        out |= ca < 0 || ca >= g.n[a];
+        w.c[a] = ca;
+    }
+    if (out) return false;
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+        w.tn[a] = w.st[a] ? next_face(g, a, w.c[a], w.st[a], o[a], inv[a]) : kInf;
+    return true;
+}
+
+__device__ __forceinline__ uint2 cell_rec(const MeshGridK &g, const Walk &w)
+{
+    return g.cells[((uint32_t)w.c[2] * (uint32_t)g.n[1] + (uint32_t)w.c[1]) * (uint32_t)g.n[0] +
+                   (uint32_t)w.c[0]];
+}
+
 __device__ __forceinline__ Hit cast(const MeshGridK &g, const Ray &r)
 {
     Hit h{kInf, 0.0f, 0.0f, INT32_MAX, 0u};
@@ -73,38 +149,43 @@ __device__ __forceinline__ Hit cast(const MeshGridK &g, const Ray &r)
         t1 = fminf(t1, fmaxf(ta, tb));
     }
     if (!(t0 <= t1) || !(t0 < kInf)) return h;
-    int c[3], st[3];
-    float tn[3];
+    Walk w;
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
         const int ca = (int)floorf((o[a] + t0 * d[a] - g.lo[a]) * g.inv_cell[a]);
-        c[a] = min(max(ca, 0), g.n[a] - 1);
-        st[a] = d[a] > 0.0f ? 1 : (d[a] < 0.0f ? -1 : 0);
-        tn[a] = st[a] ? next_face(g, a, c[a], st[a], o[a], inv[a]) : kInf;
+        w.c[a] = min(max(ca, 0), g.n[a] - 1);
+        w.st[a] = d[a] > 0.0f ? 1 : (d[a] < 0.0f ? -1 : 0);
+        w.tn[a] = w.st[a] ? next_face(g, a, w.c[a], w.st[a], o[a], inv[a]) : kInf;
     }
-    // Every step moves one cell along one axis, so the walk leaves the grid
-    // within nx + ny + nz steps; the counter bounds it whatever the rounding.
+    // Every move goes at least one cell along the ray's direction on some
+    // axis and never back on any, so the walk leaves the grid within
+    // nx + ny + nz moves; the counter bounds it whatever the rounding.
     int steps = g.n[0] + g.n[1] + g.n[2];
-    const uint32_t nx = (uint32_t)g.n[0], ny = (uint32_t)g.n[1];
+    uint2 rec = cell_rec(g, w);
     for (;;) {
-        const uint32_t cell = ((uint32_t)c[2] * ny + (uint32_t)c[1]) * nx + (uint32_t)c[0];
-        const uint32_t s = g.cell_start[cell], e = g.cell_start[cell + 1];
-        for (uint32_t k = s; k < e; ++k) test_ref(g.refs, k, r, h);
-        const float t_exit = fminf(tn[0], fminf(tn[1], tn[2]));
-        if (h.t <= t_exit || --steps <= 0) break;
-        if (tn[0] <= tn[1] && tn[0] <= tn[2]) {
-            c[0] += st[0];
-            if (c[0] < 0 || c[0] >= g.n[0]) break;
-            tn[0] = next_face(g, 0, c[0], st[0], o[0], inv[0]);
-        } else if (tn[1] <= tn[2]) {
-            c[1] += st[1];
-            if (c[1] < 0 || c[1] >= g.n[1]) break;
-            tn[1] = next_face(g, 1, c[1], st[1], o[1], inv[1]);
-        } else {
-            c[2] += st[2];
-            if (c[2] < 0 || c[2] >= g.n[2]) break;
-            tn[2] = next_face(g, 2, c[2], st[2], o[2], inv[2]);
+        // Traversal: every lane moves on until it stands in a cell with
+        // triangles, so that the lanes of a wave test triangles together.
+        bool alive = true;
+        while (rec.y == 0) {
+            if (--steps <= 0 || !advance(g, o, d, inv, (int)rec.x, w)) {
+                alive = false;
+                break;
+            }
+            rec = cell_rec(g, w);
         }
+        if (!alive) break;
+        // Intersection, with the next record's loads issued before the
+        // current one is tested (the last index is reloaded, never passed).
+        const uint32_t e = rec.x + rec.y;
+        Tri T = load_tri(g.refs, rec.x);
+        for (uint32_t k = rec.x; k < e; ++k) {
+            const Tri nT = load_tri(g.refs, k + 1 < e ? k + 1 : k);
+            test_tri(T, k, r, h);
+            T = nT;
+        }
+        if (h.t <= fminf(w.tn[0], fminf(w.tn[1], w.tn[2]))) break;
+        if (--steps <= 0 || !advance(g, o, d, inv, 1, w)) break;
+        rec = cell_rec(g, w);
     }
     return h;
 }

@@ -222,11 +222,11 @@ def test_mesh_plan_automatic_grid():
     lo, hi, res = np.array(info["lo"]), np.array(info["hi"]), np.array(info["grid_res"])
     assert np.all(lo < m.positions.min(0)) and np.all(hi > m.positions.max(0))
     cells = np.prod(res)
-    assert 0.5 * 2 * len(m.faces) < cells < 2.0 * 2 * len(m.faces)   # about 2 cells per face
+    assert 0.5 * 8 * len(m.faces) < cells < 2.0 * 8 * len(m.faces)   # about 8 cells per face
     assert info["n_faces"] == len(m.faces)
     assert info["n_refs"] == _plan_refs_numpy(m.positions, m.faces, res, lo, hi)
-    assert info["device_bytes"] >= 4 * (cells + 1) + 48 * info["n_refs"] + 32 * len(m.faces)
-    rc, _, dense = mixrt.mesh_plan(m.positions, m.faces, m.uv, cells_per_face=8.0)
+    assert info["device_bytes"] >= 8 * cells + 48 * info["n_refs"] + 32 * len(m.faces)
+    rc, _, dense = mixrt.mesh_plan(m.positions, m.faces, m.uv, cells_per_face=32.0)
     assert np.prod(dense["grid_res"]) > 2 * cells
 
 
