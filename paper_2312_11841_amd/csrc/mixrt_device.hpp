@@ -300,6 +300,64 @@ __device__ __forceinline__ void contract_to_cube(float qx, float qy, float qz, f
     if (!(x2 == x2)) x2 = 0.0f;
 }
 
+// The along-ray displacement computed jointly by the 8 lanes that hold
+// samples of one ray (consecutive lanes, 8-aligned, all taking this call),
+// when a texel is one 16-byte line: lane j loads half (j >> 2) of tap (j & 3),
+// weighs its channels by the tap weight and the SH values, and three
+// butterfly exchanges within the 8 lanes sum the partial products.  One
+// 8-byte load per lane instead of four 16-byte loads.
+template <typename TK>
+__device__ __forceinline__ void displacement_ray8(const RayParams &p, float u, float v, float dx,
+                                                  float dy, float dz, int sub, float &ox,
+                                                  float &oy, float &oz)
+{
+    typedef typename TK::T XT;
+    constexpr int EH = 8 / (int)sizeof(XT);   // channels in half a texel
+    const XT *tex = (const XT *)p.tex;
+    const Bilinear B = bilinear_taps(p.tex_R, p.tex_C, u, v);
+    const int tap = sub & 3, half = (sub >> 2) & 1;
+    int64_t off = B.t[0];
+    float w = B.w[0];
+#pragma unroll
+    for (int q = 1; q < 4; ++q)
+        if (tap == q) {
+            off = B.t[q];
+            w = B.w[q];
+        }
+    XT e[EH];
+    *(uint2 *)e = *(const uint2 *)(tex + off + half * EH);
+    float Y[16];
+    sh_basis<16>(dx, dy, dz, Y);
+    const float qs = p.q_scale[0], qo = p.q_offset[0];
+    // the lane's SH values, picked by a bit mask (a select of two array
+    // elements would become a dynamic index into a private array)
+    const uint32_t pick = 0u - (uint32_t)half;
+    float part = 0.0f;
+#pragma unroll
+    for (int i = 0; i < EH; ++i) {
+        const float y = __uint_as_float((__float_as_uint(Y[i]) & ~pick) |
+                                        (__float_as_uint(Y[EH + i]) & pick));
+        if (half * EH + i < p.tex_V) part += y * tex_elem(e[i], qs, qo);
+    }
+    part *= w;
+    part += __shfl_xor(part, 1);
+    part += __shfl_xor(part, 2);
+    part += __shfl_xor(part, 4);
+    ox = part * dx;
+    oy = part * dy;
+    oz = part * dz;
+}
+
+// Whether displacement_ray8 serves a call: the along-ray form, 16-byte
+// texels, and K a multiple of 8 dividing 64 (a ray's samples then sit in
+// whole 8-lane groups).
+template <typename TK>
+__device__ __forceinline__ bool ray8_applies(const RayParams &p)
+{
+    return TK::mode == kDispAlongRay && p.tex_C * (int)sizeof(typename TK::T) == 16 &&
+           (p.K & 7) == 0 && 64 % p.K == 0;
+}
+
 // Steps before the grid for sample k of a ray: hit test, Eq. 2 calibration,
 // sample placement, contraction.  Returns false for a miss.
 template <typename TK>
@@ -313,7 +371,10 @@ __device__ __forceinline__ bool sample_position(const RayParams &p, const Ray &r
         return false;
     }
     float ox, oy, oz;
-    displacement<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, ox, oy, oz);
+    if (ray8_applies<TK>(p))
+        displacement_ray8<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, k & 7, ox, oy, oz);
+    else
+        displacement<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, ox, oy, oz);
     const float off = t + ((float)k - 0.5f * (float)(p.K - 1)) * p.delta;
     contract_to_cube(r.ox + ox + off * r.dx, r.oy + oy + off * r.dy, r.oz + oz + off * r.dz, x0,
                      x1, x2);
