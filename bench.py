@@ -213,6 +213,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="view720p")
+    ap.add_argument("--geometry", choices=("raster", "raycast"), default="raster",
+                    help="mesh workloads: how each step computes the G-buffer")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle work for the CPU baseline (0: skip)")
     ap.add_argument("--paper-tables", action="store_true",
@@ -262,14 +264,19 @@ def main():
         mesh_load_s = time.perf_counter() - t0
 
     def raycast():
-        r.raycast(mesh, ds.cams, cfg.W, cfg.H, out=(ds.g0, None))
+        r.raycast(mesh, ds.cams, cfg.W, cfg.H, g1=False, out=(ds.g0, None))
+
+    def rasterize():
+        r.rasterize(mesh, ds.cams, cfg.W, cfg.H, g1=False, out=(ds.g0, None))
+
+    geometry = rasterize if args.geometry == "raster" else raycast
 
     def render():
         r.render(ds, out)
 
     def step():
         if mesh is not None:
-            raycast()
+            geometry()
         render()
 
     for _ in range(args.warmup):
@@ -287,10 +294,17 @@ def main():
     extra = {}
     if mesh is not None:
         ray_ms = time_launches(stream, raycast, args.steps)
-        extra["raycast"] = {
-            "kernel": "raycast_kernel (uniform-grid walk + fp32 Moller-Trumbore)",
-            "ms": round(ray_ms, 4), "render_ms": round(render_ms, 4),
-            "Mrays_per_s": round(cfg.rays / (ray_ms * 1e-3) / 1e6, 1),
+        ras_ms = time_launches(stream, rasterize, args.steps)
+        extra["geometry"] = {
+            "route": args.geometry + " (in the timed step)",
+            "raster_ms": round(ras_ms, 4),
+            "raster_kernels": "clear + raster (wave-balanced triangle x pixel pairs, 64-bit "
+                              "atomic min) + resolve",
+            "raycast_ms": round(ray_ms, 4),
+            "raycast_kernel": "uniform-grid walk with empty-space leaps + fp32 Moller-Trumbore",
+            "render_ms": round(render_ms, 4),
+            "Mpix_per_s": {"raster": round(cfg.rays / (ras_ms * 1e-3) / 1e6, 1),
+                           "raycast": round(cfg.rays / (ray_ms * 1e-3) / 1e6, 1)},
             "mesh_faces": int(len(scene.mesh.faces)), "mesh_bytes": int(scene.mesh.nbytes),
             "grid": mesh.info, "load_s": round(mesh_load_s, 2)}
     if not args.no_rooflines:
@@ -326,8 +340,8 @@ def main():
                         f"hash L={cfg.L} T=2^{cfg.log2_T} F={cfg.F} {cfg.table_dtype} "
                         f"N {cfg.N_min}-{cfg.N_max}, texture {cfg.tex_R}^2x{cfg.tex_V} "
                         f"{cfg.tex_dtype}, MLP {'-'.join(map(str, cfg.widths))} fp16"
-                        + (f"; G-buffer ray-cast from a {len(scene.mesh.faces)}-triangle mesh "
-                           "in each step" if scene.mesh is not None else ""),
+                        + (f"; G-buffer computed from a {len(scene.mesh.faces)}-triangle mesh "
+                           f"in each step ({args.geometry})" if scene.mesh is not None else ""),
             "rays": cfg.rays,
             "samples": cfg.samples,
             "parallelism": "single GPU",

@@ -253,7 +253,7 @@ typedef struct {
                                 e2 = p2 - p0 */
     const float *uv;         /* host [n_vertices][2] texture coordinates, or NULL
                                 (then the G-buffer's p_t is (0, 0)) */
-    int32_t grid_res[3];     /* cells per axis (1..1024 each, at most 2^26 in all),
+    int32_t grid_res[3];     /* ray-casting grid: cells per axis (1..1024 each, at most 2^26 in all),
                                 or all 0: chosen from the bounds so that the
                                 grid has about cells_per_face * n_faces cells */
     float cells_per_face;    /* for grid_res = 0; 0 means 8 */
@@ -278,8 +278,9 @@ int mixrt_mesh_plan(const mixrt_mesh_desc *desc, mixrt_mesh_info *info, char *ms
  * the cell padded by 1/500 of its size, in ascending triangle order; empty
  * cells hold their Chebyshev distance to the nearest listed cell, which lets
  * the walk leap across empty space) and upload it to ctx's device: triangle
- * records in cell order (v0, e1, e2 and the triangle index), cell records
- * and per-triangle texture coordinates.  The mesh owns this device memory; the copies are
+ * records in cell order (v0, e1, e2 and the triangle index), cell records,
+ * per-triangle texture coordinates, and the triangle records once more in
+ * triangle order (for mixrt_rasterize).  The mesh owns this device memory; the copies are
  * synchronous, so desc's arrays may be released on return.  *out is NULL on
  * failure (MIXRT_EINVAL for a bad descriptor, MIXRT_ENOMEM if the device
  * memory cannot be allocated). */
@@ -303,6 +304,17 @@ int mixrt_mesh_destroy(mixrt_mesh *mesh);
  * Enqueued on the context's stream; no device memory is allocated. */
 int mixrt_raycast(mixrt_ctx *ctx, const mixrt_mesh *mesh, int32_t views, int32_t W, int32_t H,
                   const mixrt_camera *cams, float *out_g0, float *out_g1);
+
+/* The same G-buffer as mixrt_raycast (same per-pixel rays, same fp32
+ * ray-triangle test, same closest-hit rule), computed the way the paper
+ * obtains it: by rasterising the mesh (Fig. 2 step 1) with compute kernels
+ * into a visibility buffer of (t, triangle) keys kept by atomic minimum.
+ * Faster than mixrt_raycast for whole frames.  The keys live in out_g0
+ * until the last of the call's three launches overwrites them, so no
+ * device memory is allocated.  Fewer than 2^26 pixels per view
+ * (MIXRT_EUNSUPPORTED beyond); other arguments as for mixrt_raycast. */
+int mixrt_rasterize(mixrt_ctx *ctx, const mixrt_mesh *mesh, int32_t views, int32_t W, int32_t H,
+                    const mixrt_camera *cams, float *out_g0, float *out_g1);
 
 /* ---- errors ------------------------------------------------------------------- */
 

@@ -9,7 +9,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmixrt.so")
 SOURCES = ["mixrt_api.cpp", "mixrt_mesh.cpp", "mixrt_render.hip", "mixrt_stages.hip",
-           "mixrt_raycast.hip"]
+           "mixrt_raycast.hip", "mixrt_raster.hip"]
 MB_LIB = os.path.join(PKG, "libmixrt_microbench.so")
 MB_SOURCES = ["microbench.hip"]
 

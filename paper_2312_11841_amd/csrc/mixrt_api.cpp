@@ -401,8 +401,12 @@ int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **
     e = hipMemcpy(base, g.cells.data(), (size_t)cells * 8, hipMemcpyHostToDevice);
     if (e == hipSuccess && g.n_refs)
         e = hipMemcpy(base + b_cells, g.refs.data(), (size_t)g.n_refs * 48, hipMemcpyHostToDevice);
+    const int64_t b_attr = (desc->n_faces * 32 + 255) & ~int64_t(255);
     if (e == hipSuccess)
         e = hipMemcpy(base + b_cells + b_refs, g.attr.data(), (size_t)desc->n_faces * 32,
+                      hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(base + b_cells + b_refs + b_attr, g.tris.data(), (size_t)desc->n_faces * 48,
                       hipMemcpyHostToDevice);
     if (e != hipSuccess) {
         (void)hipFree(mesh->mem);
@@ -424,6 +428,8 @@ int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **
     k.cells = (const uint2 *)base;
     k.refs = (const float4 *)(base + b_cells);
     k.attr = (const float4 *)(base + b_cells + b_refs);
+    k.tris = (const float4 *)(base + b_cells + b_refs + b_attr);
+    k.n_faces = (int32_t)desc->n_faces;
     mesh->info.n_faces = desc->n_faces;
     mesh->info.n_refs = g.n_refs;
     mesh->info.device_bytes = bytes;
@@ -484,6 +490,50 @@ int mixrt_raycast(mixrt_ctx *ctx, const mixrt_mesh *mesh, int32_t views, int32_t
     L.g0 = (float4 *)out_g0;
     L.g1 = (float4 *)out_g1;
     return finish_launch(ctx, mixrt::launch_raycast(L, ctx->stream), "raycast");
+}
+
+int mixrt_rasterize(mixrt_ctx *ctx, const mixrt_mesh *mesh, int32_t views, int32_t W, int32_t H,
+                    const mixrt_camera *cams, float *out_g0, float *out_g1)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    if (!mesh) return fail(ctx, MIXRT_EINVAL, "mesh is NULL");
+    if (mesh->device != ctx->device)
+        return fail(ctx, MIXRT_EINVAL, "mesh lives on device %d, ctx on device %d", mesh->device,
+                    ctx->device);
+    if (views < 1 || views > MIXRT_MAX_VIEWS)
+        return fail(ctx, MIXRT_EINVAL, "views=%d outside 1..%d", views, MIXRT_MAX_VIEWS);
+    if (W < 1 || H < 1) return fail(ctx, MIXRT_EINVAL, "W=%d H=%d", W, H);
+    if ((int64_t)W * H >= ((int64_t)1 << 26) || (int64_t)views * H * W >= ((int64_t)1 << 31))
+        return fail(ctx, MIXRT_EUNSUPPORTED, "rasterize takes fewer than 2^26 pixels per view");
+    char msg[512];
+    int rc = check_cams(cams, views, Msg{msg, sizeof msg});
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (!out_g0 || !aligned16(out_g0))
+        return fail(ctx, MIXRT_EINVAL, "out_g0 is NULL or not 16-byte aligned");
+    if (out_g1 && !aligned16(out_g1)) return fail(ctx, MIXRT_EINVAL, "out_g1 not 16-byte aligned");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::RasterLaunch L;
+    memset(&L, 0, sizeof L);
+    L.tris = mesh->k.tris;
+    L.attr = mesh->k.attr;
+    L.n_faces = mesh->k.n_faces;
+    fill_cams(L.cams, cams, views, H);
+    for (int v = 0; v < views; ++v) {
+        // Clip depth: half of t_min times the smallest |d_z| of the view's
+        // pixel rays (reached at a corner), so every hit with t > t_min lies
+        // in front of the clipping plane.
+        const double inv_f = L.cams[v].inv_f;
+        const double cx = (0.5 * W) * inv_f, cy = (0.5 * H) * inv_f;
+        const double dz = 1.0 / std::sqrt(cx * cx + cy * cy + 1.0);
+        L.near_z[v] = (float)(0.5 * (double)MIXRT_RAY_T_MIN * dz);
+    }
+    L.views = views;
+    L.W = W;
+    L.H = H;
+    L.g0 = (float4 *)out_g0;
+    L.g1 = (float4 *)out_g1;
+    return finish_launch(ctx, mixrt::launch_rasterize(L, ctx->stream), "rasterize");
 }
 
 const char *mixrt_last_error(const mixrt_ctx *ctx) { return ctx ? ctx->err.c_str() : ""; }

@@ -126,7 +126,8 @@ void load_tri(const mixrt_mesh_desc *d, int64_t f, double p[3][3])
 int64_t mesh_device_bytes(const MeshGridHost &g, int64_t n_faces)
 {
     const int64_t cells = (int64_t)g.n[0] * g.n[1] * g.n[2];
-    return align256(cells * 8) + align256(g.n_refs * 48) + align256(n_faces * 32);
+    return align256(cells * 8) + align256(g.n_refs * 48) + align256(n_faces * 32) +
+           align256(n_faces * 48);
 }
 
 int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *msg, size_t cap)
@@ -238,6 +239,7 @@ int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *
         g.cells[2 * c + 1] = count[c];
     }
     g.refs.assign(refs * 12, 0.0f);
+    g.tris.assign(d->n_faces * 12, 0.0f);
     for (int64_t f = 0; f < d->n_faces; ++f) {
         load_tri(d, f, p);
         const float *v0 = d->positions + 3 * (int64_t)d->faces[3 * f];
@@ -253,6 +255,7 @@ int build_mesh_grid(const mixrt_mesh_desc *d, bool fill, MeshGridHost &g, char *
         memcpy(&rec[3], &id, 4);
         rec[7] = rec[11] = 0.0f;
         for_cells(g, p, [&](int64_t c) { memcpy(&g.refs[12 * (int64_t)cursor[c]++], rec, sizeof rec); });
+        memcpy(&g.tris[12 * f], rec, sizeof rec);
     }
     g.attr.assign(d->n_faces * 8, 0.0f);
     if (d->uv)

@@ -34,6 +34,8 @@ struct MeshGridK {
     const uint2 *cells;
     const float4 *refs;
     const float4 *attr;
+    const float4 *tris;   // [n_faces] records like refs, in triangle order
+    int32_t n_faces;
 };
 
 // The grid as built on the host, before upload.
@@ -44,6 +46,7 @@ struct MeshGridHost {
     std::vector<uint32_t> cells;        // 2 per cell: (first or distance, count)
     std::vector<float> refs;            // n_refs * 12
     std::vector<float> attr;            // n_faces * 8
+    std::vector<float> tris;            // n_faces * 12, triangle order
 };
 
 // Validate desc and choose bounds and resolution; with fill, also count and
@@ -64,5 +67,21 @@ struct RaycastLaunch {
 };
 
 hipError_t launch_raycast(const RaycastLaunch &L, hipStream_t stream);
+
+// The rasteriser: per view, triangles are clipped at camera depth near_z
+// (chosen on the host so that no hit with t > MIXRT_RAY_T_MIN is closer).
+// Pixels per view must be below 2^26 (box areas of a wave sum in 32 bits).
+struct RasterLaunch {
+    const float4 *tris;
+    const float4 *attr;
+    int32_t n_faces;
+    CamK cams[MIXRT_MAX_VIEWS];
+    float near_z[MIXRT_MAX_VIEWS];
+    int32_t views, W, H;
+    float4 *g0;
+    float4 *g1;
+};
+
+hipError_t launch_rasterize(const RasterLaunch &L, hipStream_t stream);
 
 }  // namespace mixrt

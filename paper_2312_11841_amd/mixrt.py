@@ -33,7 +33,7 @@ EXPORTS = (
     "mixrt_level_resolutions", "mixrt_render", "mixrt_debug_ray_setup",
     "mixrt_debug_hash_encode", "mixrt_debug_mlp", "mixrt_debug_composite",
     "mixrt_mesh_plan", "mixrt_mesh_create", "mixrt_mesh_get_info", "mixrt_mesh_destroy",
-    "mixrt_raycast",
+    "mixrt_raycast", "mixrt_rasterize",
     "mixrt_status_string", "mixrt_last_error", "mixrt_thread_error",
 )
 RAY_T_MIN = 1e-4
@@ -133,6 +133,8 @@ def lib():
             "mixrt_mesh_destroy": (C.c_int, [P]),
             "mixrt_raycast": (C.c_int, [P, P, C.c_int32, C.c_int32, C.c_int32,
                                         C.POINTER(Camera), P, P]),
+            "mixrt_rasterize": (C.c_int, [P, P, C.c_int32, C.c_int32, C.c_int32,
+                                          C.POINTER(Camera), P, P]),
             "mixrt_status_string": (C.c_char_p, [C.c_int]),
             "mixrt_last_error": (C.c_char_p, [P]),
             "mixrt_thread_error": (C.c_char_p, []),
@@ -339,8 +341,15 @@ class Renderer:
 
     # -- geometry
     def raycast(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):
-        """G-buffer of views x H x W pixels: (g0, g1) device float [views, H, W, 4]
-        (g1 None unless asked for)."""
+        """G-buffer of views x H x W pixels by ray casting the mesh's grid:
+        (g0, g1) device float [views, H, W, 4] (g1 None unless asked for)."""
+        return self._gbuffer(lib().mixrt_raycast, mesh, cams, W, H, g1, out)
+
+    def rasterize(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):
+        """The same G-buffer by rasterising the mesh (visibility buffer)."""
+        return self._gbuffer(lib().mixrt_rasterize, mesh, cams, W, H, g1, out)
+
+    def _gbuffer(self, fn, mesh, cams, W, H, g1, out):
         import torch
         cam_arr = cams if isinstance(cams, C.Array) else make_cameras(np.asarray(cams))
         views = len(cam_arr)
@@ -349,8 +358,7 @@ class Renderer:
             out = (torch.empty((views, H, W, 4), dtype=torch.float32, device=dev),
                    torch.empty((views, H, W, 4), dtype=torch.float32, device=dev) if g1 else None)
         g0t, g1t = out
-        self._check(lib().mixrt_raycast(self._h, mesh._h, views, W, H, cam_arr, _ptr(g0t),
-                                        _ptr(g1t)))
+        self._check(fn(self._h, mesh._h, views, W, H, cam_arr, _ptr(g0t), _ptr(g1t)))
         return g0t, g1t
 
     # -- stage entry points
