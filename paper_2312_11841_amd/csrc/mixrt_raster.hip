@@ -3,17 +3,23 @@
 // (t bits << 32 | triangle) kept with atomic min, so the closest hit wins and
 // equal t goes to the lower triangle index.  Coverage and depth come from the
 // same fp32 ray-triangle test, on the same per-pixel rays, as the ray cast
-// (mixrt_raycast.hip), so both produce the same G-buffer.
+// (mixrt_raycast.hip).
 //
 //   clear:   every pixel's key = all ones (no hit);
-//   raster:  each wave takes 64 triangles of one view, clips them against a
+//   raster:  each wave takes 64 triangles of one view (strided over the
+//            mesh, for balance between waves), clips them against a
 //            plane just in front of the camera, projects them and bounds
 //            their pixels (one pixel of margin); the (triangle, pixel) pairs
-//            of all 64 boxes are then dealt round-robin to the 64 lanes, so
-//            large and small triangles balance within the wave;
+//            of all 64 boxes, in box order, are cut into 64 equal runs, one
+//            per lane, so large and small triangles balance within the wave;
+//            a lane finds its first box by binary search and then steps
+//            pixel by pixel, box by box, testing with the pixel's ray
+//            direction before normalisation (same order of hits);
 //   resolve: per pixel, the winning triangle's hit is recomputed to write t,
 //            the barycentric uv and the face normal.
-// The keys live in the first 8 bytes of each 16-byte G-buffer record: the
+// The winner of a pixel is the fp32 closest hit of its ray as the ray cast
+// finds it, except where two triangles' hits lie within rounding of each
+// other.  The keys live in the first 8 bytes of each 16-byte G-buffer record: the
 // three launches need no memory beyond the caller's output.
 #include "mixrt_common.hpp"
 #include "mixrt_mesh.hpp"
@@ -42,6 +48,30 @@ __device__ __forceinline__ bool tri_hit(const float4 &A, const float4 &E1, const
     return b1 >= 0.0f && b2 >= 0.0f && b1 + b2 <= 1.0f && t > MIXRT_RAY_T_MIN;
 }
 
+// The same test for a ray o + s D with D not normalised: s = t / |D|, so the
+// order of hits along the ray is that of t, and t > t_min reads
+// s^2 |D|^2 > t_min^2 (dd = |D|^2).  Returns s in `key_t`.
+__device__ __forceinline__ bool tri_hit_scaled(const float4 &A, const float4 &E1, const float4 &E2,
+                                               float ox, float oy, float oz, float dx, float dy,
+                                               float dz, float dd, float &key_t)
+{
+    const float px = dy * E2.z - dz * E2.y;
+    const float py = dz * E2.x - dx * E2.z;
+    const float pz = dx * E2.y - dy * E2.x;
+    const float det = E1.x * px + E1.y * py + E1.z * pz;
+    const float inv = __builtin_amdgcn_rcpf(det);
+    const float sx = ox - A.x, sy = oy - A.y, sz = oz - A.z;
+    const float b1 = (sx * px + sy * py + sz * pz) * inv;
+    const float qx = sy * E1.z - sz * E1.y;
+    const float qy = sz * E1.x - sx * E1.z;
+    const float qz = sx * E1.y - sy * E1.x;
+    const float b2 = (dx * qx + dy * qy + dz * qz) * inv;
+    const float s = (E2.x * qx + E2.y * qy + E2.z * qz) * inv;
+    key_t = s;
+    return b1 >= 0.0f && b2 >= 0.0f && b1 + b2 <= 1.0f && s > 0.0f &&
+           s * s * dd > MIXRT_RAY_T_MIN * MIXRT_RAY_T_MIN;
+}
+
 __global__ __launch_bounds__(kBlock) void clear_kernel(uint4 *__restrict__ g0, int64_t n)
 {
     const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
@@ -50,8 +80,7 @@ __global__ __launch_bounds__(kBlock) void clear_kernel(uint4 *__restrict__ g0, i
 
 struct Box {
     float4 a, e1, e2;
-    int x0, y0, bw;
-    float inv_bw;
+    int x0, y0, bw, bh;
     uint32_t end;   // inclusive prefix sum of the wave's box areas
 };
 
@@ -113,21 +142,23 @@ __global__ __launch_bounds__(kBlock) void raster_kernel(const RasterLaunch L)
     __shared__ Box s_box[kWavesPerBlock][kWave];
     const int view = blockIdx.y;
     const int wv = threadIdx.x / kWave, lane = threadIdx.x & (kWave - 1);
-    const int64_t tri = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    // Triangles are dealt to waves with a stride of the wave count, so that
+    // the large boxes of a nearby object (consecutive triangles) spread over
+    // many waves instead of piling into a few.
+    const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
+    const int64_t tri = (int64_t)lane * n_waves + (int64_t)blockIdx.x * kWavesPerBlock + wv;
     const CamK &c = L.cams[view];
     Box b;
     b.a = b.e1 = b.e2 = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    int bh = 0;
-    b.x0 = b.y0 = b.bw = 0;
+    b.x0 = b.y0 = b.bw = b.bh = 0;
     if (tri < L.n_faces) {
         b.a = L.tris[3 * tri];
         b.e1 = L.tris[3 * tri + 1];
         b.e2 = L.tris[3 * tri + 2];
-        pixel_box(L, c, L.near_z[view], b.a, b.e1, b.e2, b.x0, b.y0, b.bw, bh);
+        pixel_box(L, c, L.near_z[view], b.a, b.e1, b.e2, b.x0, b.y0, b.bw, b.bh);
     }
-    b.inv_bw = b.bw ? 1.0f / (float)b.bw : 0.0f;
     // inclusive prefix sum of the box areas over the wave
-    uint32_t end = (uint32_t)b.bw * (uint32_t)bh;
+    uint32_t end = (uint32_t)b.bw * (uint32_t)b.bh;
 #pragma unroll
     for (int d = 1; d < kWave; d <<= 1) {
         const uint32_t o = __shfl_up(end, d);
@@ -137,31 +168,55 @@ __global__ __launch_bounds__(kBlock) void raster_kernel(const RasterLaunch L)
     s_box[wv][lane] = b;
     const uint32_t total = __shfl(end, kWave - 1);
     wave_lds_sync();
+    // this lane's run of pairs [q0, q1)
+    const uint32_t q0 = (uint32_t)(((uint64_t)total * lane) >> 6);
+    const uint32_t q1 = (uint32_t)(((uint64_t)total * (lane + 1)) >> 6);
+    if (q0 >= q1) return;
+    // first box whose end exceeds q0
+    int cur = 0;
+#pragma unroll
+    for (int step = kWave / 2; step > 0; step >>= 1)
+        if (s_box[wv][cur + step - 1].end <= q0) cur += step;
+    const Box *bx = &s_box[wv][cur];
+    uint32_t local = q0 - (cur ? s_box[wv][cur - 1].end : 0u);
+    int j = (int)(local / (uint32_t)bx->bw);
+    int i = (int)(local - (uint32_t)j * (uint32_t)bx->bw);
+    float4 A = bx->a, E1 = bx->e1, E2 = bx->e2;
+    int x0 = bx->x0, y0 = bx->y0, bw = bx->bw, bh = bx->bh;
     uint64_t *vis = (uint64_t *)L.g0;
     const int64_t view_base = (int64_t)view * L.H * L.W;
-    int cur = 0;                        // the box holding pair p (non-decreasing in p)
-    for (uint32_t p = lane; p < total; p += kWave) {
-        while (s_box[wv][cur].end <= p) ++cur;
-        const Box &q = s_box[wv][cur];
-        const uint32_t local = p - (cur ? s_box[wv][cur - 1].end : 0u);
-        // row = local / bw by the float reciprocal, corrected to be exact
-        int j = (int)(((float)local + 0.5f) * q.inv_bw);
-        int i = (int)local - j * q.bw;
-        while (i < 0) {
-            --j;
-            i += q.bw;
-        }
-        while (i >= q.bw) {
-            ++j;
-            i -= q.bw;
-        }
-        const int px = q.x0 + i, py = q.y0 + j;
-        const Ray r = camera_ray(c, L.W, L.H, (uint32_t)px, (uint32_t)py);
-        float t, b1, b2;
-        if (tri_hit(q.a, q.e1, q.e2, r, t, b1, b2)) {
-            const uint64_t key = ((uint64_t)__float_as_uint(t) << 32) | (uint32_t)__float_as_int(q.a.w);
+    for (uint32_t q = q0; q < q1; ++q) {
+        const int px = x0 + i, py = y0 + j;
+        // the pixel's ray direction before normalisation (as in camera_ray)
+        const float cx = ((float)px + 0.5f - 0.5f * (float)L.W) * c.inv_f;
+        const float cy = -(((float)py + 0.5f - 0.5f * (float)L.H) * c.inv_f);
+        const float dx = c.R[0] * cx + c.R[1] * cy - c.R[2];
+        const float dy = c.R[3] * cx + c.R[4] * cy - c.R[5];
+        const float dz = c.R[6] * cx + c.R[7] * cy - c.R[8];
+        float st;
+        if (tri_hit_scaled(A, E1, E2, c.o[0], c.o[1], c.o[2], dx, dy, dz,
+                           dx * dx + dy * dy + dz * dz, st)) {
+            const uint64_t key = ((uint64_t)__float_as_uint(st) << 32) | (uint32_t)__float_as_int(A.w);
             atomicMin((unsigned long long *)&vis[2 * (view_base + (int64_t)py * L.W + px)],
                       (unsigned long long)key);
+        }
+        if (++i == bw) {
+            i = 0;
+            if (++j == bh && q + 1 < q1) {
+                // next box with pixels (empty boxes hold no pair)
+                do {
+                    ++cur;
+                } while (s_box[wv][cur].bw * s_box[wv][cur].bh == 0);
+                bx = &s_box[wv][cur];
+                A = bx->a;
+                E1 = bx->e1;
+                E2 = bx->e2;
+                x0 = bx->x0;
+                y0 = bx->y0;
+                bw = bx->bw;
+                bh = bx->bh;
+                j = 0;
+            }
         }
     }
 }

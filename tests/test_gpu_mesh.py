@@ -252,8 +252,9 @@ def test_gbuffer_500k_mesh_sampled(R, method):
 
 def test_rasterize_equals_raycast_on_the_500k_mesh(R):
     """Both routes take the fp32 closest hit of the same rays: the same
-    triangle on every pixel, and the same hit up to the rounding of the same
-    arithmetic compiled twice."""
+    triangle except where two hits lie within rounding of each other (the
+    rasteriser orders hits with the unnormalised ray direction), and the
+    same hit up to fp32 rounding."""
     cfg = synth.MESH720P
     sc = synth.make_scene(cfg)
     dm = mixrt.DeviceMesh(R, sc.mesh)
@@ -265,7 +266,15 @@ def test_rasterize_equals_raycast_on_the_500k_mesh(R):
     idb = b1.cpu().numpy()[..., 3].view(np.int32)
     diff = (ida != idb).mean()
     say(f"  triangle differs on {diff:.2e} of {ida.size} px")
-    assert diff <= 1e-5
+    assert diff <= 1e-4
+    # where the two routes pick different triangles, both answers must lie
+    # within fp32 rounding of each other: the oracle flags such pixels
+    # ambiguous
+    odd = np.nonzero((ida != idb).reshape(-1))[0]
+    if odd.size:
+        _, _, _, amb = oracle.raycast_pixels(cams, cfg.W, cfg.H, sc.mesh, odd,
+                                             threads=oracle.max_threads())
+        assert np.all(amb), odd[~amb]
     # t: the same formula on the same fp32 inputs, compiled in two kernels
     # (multiply-adds may contract differently); grazing hits amplify that
     # like any fp32 rounding, so the oracle bar's 1/|cos| factor applies
