@@ -121,31 +121,39 @@ def cpu_baseline(scene, budget_s: float):
     threads = oracle.max_threads()
     cfg = scene.cfg
 
-    def run(pix):
+    def run(pix, nthreads):
         if scene.mesh is None:
-            return oracle.OracleScene(scene).render_pixels(pix, threads=threads)
+            return oracle.OracleScene(scene).render_pixels(pix, threads=nthreads)
         g0, _, _, _ = oracle.raycast_pixels(scene.cams, cfg.W, cfg.H, scene.mesh, pix,
-                                            threads=threads)
+                                            threads=nthreads)
         flat = scene.g0.reshape(-1, 4).copy()
         flat[pix] = g0.astype(np.float32)
         sc = dataclasses.replace(scene, g0=flat.reshape(scene.g0.shape))
-        return oracle.OracleScene(sc).render_pixels(pix, threads=threads)
+        return oracle.OracleScene(sc).render_pixels(pix, threads=nthreads)
 
     rng = np.random.default_rng(0)
+    # one thread on a small sample first (the single-core rate)
+    n1 = 300 if scene.mesh is None else 20
+    pix1 = rng.choice(cfg.rays, n1, replace=False)
+    t0 = time.perf_counter()
+    run(pix1, 1)
+    single = n1 / (time.perf_counter() - t0) / 1e6
     n0 = 2000 if scene.mesh is None else 200
     probe = rng.choice(cfg.rays, n0, replace=False)
     t0 = time.perf_counter()
-    run(probe)
+    run(probe, threads)
     dt = time.perf_counter() - t0
     n = int(min(cfg.rays, max(n0, n0 * budget_s / max(dt, 1e-6))))
     pix = rng.choice(cfg.rays, n, replace=False)
     t0 = time.perf_counter()
-    run(pix)
+    run(pix, threads)
     dt = time.perf_counter() - t0
     what = "brute-force ray cast + render" if scene.mesh is not None else "render"
     return {"value": n / dt / 1e6, "unit": "Mpix/s", "cores": threads, "kind": "oracle",
             "sample": f"{n} random pixels of one {cfg.W}x{cfg.H} frame, {what} "
-                      f"({dt:.1f} s wall, OpenMP over pixels)"}
+                      f"({dt:.1f} s wall, OpenMP over pixels)",
+            "single_thread_value": single, "single_thread_sample": f"{n1} pixels",
+            "cpu_model": cpu_model()}
 
 
 def time_launches(stream, fn, steps):
@@ -207,6 +215,69 @@ def paper_tables(steps, warmup):
           flush=True)
 
 
+def sweep(steps, warmup):
+    """The ray x sample sweep: the first 2^16..2^24 rays of a coherent
+    4096x4096 view x K in {1..32}, on view720p's texture, grid and MLP.  The
+    view is generated once and its first rows rendered for each ray count."""
+    import dataclasses
+    import torch
+    from paper_2312_11841_amd import mixrt, synth
+    full = synth.sweep_config(1 << 24, 8)
+    print("bench: generating the 4096x4096 sweep view (about a minute)", file=sys.stderr,
+          flush=True)
+    scene = synth.make_scene(full)
+    ds = mixrt.DeviceScene.from_scene(scene, "cuda:0")
+    stream = torch.cuda.current_stream()
+    r = mixrt.Renderer(0, stream=stream)
+    rows_out = []
+    for log2r in (16, 18, 20, 22, 24):
+        rays = 1 << log2r
+        out = torch.empty((rays, 4), dtype=torch.float32, device="cuda:0")
+        gbuf = mixrt.GBuffer(1, full.W, rays // full.W, ds.gbuf.g0, 0)
+        for K in (1, 2, 4, 8, 16, 32):
+            d = dataclasses.replace(ds, gbuf=gbuf, rays=rays,
+                                    smp=mixrt.make_sampling(K, full.delta, full.t_term))
+            n = max(steps, int(2e7 // (rays * K)))   # small launches: more of them
+            for _ in range(warmup):
+                r.render(d, out)
+            ms = time_launches(stream, lambda: r.render(d, out), n)
+            samples = rays * K
+            c = full.replace(rows=rays // full.W, K=K)
+            work = algorithmic_work(c)
+            row = {"rays": rays, "K": K, "samples": samples, "launches": n, "ms": round(ms, 4),
+                   "ns_per_sample": round(ms * 1e6 / samples, 4),
+                   "hash_GBps": round(work["hash_bytes"] / (ms * 1e-3) / 1e9, 1),
+                   "mlp_TFLOPs": round(work["mlp_flops"] / (ms * 1e-3) / 1e12, 1)}
+            rows_out.append(row)
+            print(json.dumps(row), file=sys.stderr, flush=True)
+    r.close()
+    print(json.dumps({"sweep": rows_out, "view": "first rows of a coherent 4096x4096 view",
+                      "grid": "L16 T2^19 F2 f16 N 16-4096", "mlp": "48-64-64-4 fp16"}), flush=True)
+
+
+def environment():
+    """What the numbers were measured on."""
+    import torch
+    p = torch.cuda.get_device_properties(0)
+    env = {"device": p.name, "arch": getattr(p, "gcnArchName", None),
+           "compute_units": p.multi_processor_count, "hip": torch.version.hip,
+           "torch": torch.__version__}
+    clk = getattr(p, "clock_rate", None)
+    if clk:
+        env["clock_MHz"] = round(clk / 1000)
+    return env
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,6 +288,8 @@ def main():
                     help="mesh workloads: how each step computes the G-buffer")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
                     help="seconds of oracle work for the CPU baseline (0: skip)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the rays x K sweep (2^16..2^24 rays, K 1..32) instead")
     ap.add_argument("--paper-tables", action="store_true",
                     help="time the paper's Tab. 3 / Tab. 6 profiling points instead")
     ap.add_argument("--no-rooflines", action="store_true",
@@ -247,6 +320,9 @@ def main():
         return
     if args.paper_tables:
         paper_tables(args.steps, args.warmup)
+        return
+    if args.sweep:
+        sweep(min(args.steps, 20), min(args.warmup, 3))
         return
     cfg = synth.CONFIGS[args.workload]
     print(f"bench: generating {cfg.name} ({cfg.rays} rays, K={cfg.K})", file=sys.stderr,
@@ -368,6 +444,13 @@ def main():
         "kernel_source_digest": kernel_source_digest(),
     }
     line.update(extra)
+    rm = extra.get("rooflines_measured")
+    if rm:
+        g = rm["gather_random_lane_loads_per_s"]
+        rate = cfg.samples * cfg.L * 8 / rsec
+        line["hash_vs_measured_random_gather"] = {
+            k: round(rate / v["value"], 2) for k, v in g.items()}
+    line["environment"] = environment()
     if args.cpu_budget > 0:
         line["cpu_baseline"] = cpu_baseline(scene, args.cpu_budget)
     print(json.dumps(line), flush=True)
