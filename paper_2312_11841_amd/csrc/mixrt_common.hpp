@@ -2,6 +2,8 @@
 // mixrt_stages.hip.
 #pragma once
 
+#include <atomic>
+
 #include "mixrt_device.hpp"
 
 namespace mixrt {
@@ -25,14 +27,18 @@ __device__ __forceinline__ void wave_lds_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
-// Blocks of `fn` resident on the whole device at once (at least one per CU).
-inline int resident_blocks(const void *fn, int cus)
+// Blocks of `fn` (kBlock threads) resident on one CU at once, at least 1;
+// queried once per kernel and kept in `cache` (the value depends only on the
+// kernel), so concurrent first calls at worst query twice.
+inline int blocks_per_cu(const void *fn, std::atomic<int> &cache)
 {
-    int per_cu = 0;
+    int per_cu = cache.load(std::memory_order_relaxed);
+    if (per_cu > 0) return per_cu;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kBlock, 0) != hipSuccess ||
         per_cu < 1)
         per_cu = 1;
-    return per_cu * cus;
+    cache.store(per_cu, std::memory_order_relaxed);
+    return per_cu;
 }
 
 }  // namespace mixrt

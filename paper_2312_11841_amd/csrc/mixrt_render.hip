@@ -230,9 +230,9 @@ hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
     if (L.tex == a && L.F == b && L.tf16 == c && L.nhid == f &&                                \
         (f == 0 || (L.in == d && L.hid == e))) {                                               \
         auto fn = render_kernel<a, b, c, d, e, f>;                                             \
-        static int resident = 0; /* blocks resident on the whole device */                    \
-        if (!resident) resident = resident_blocks((const void *)fn, L.cus);                    \
-        int64_t blocks = resident;                                                             \
+        static std::atomic<int> per_cu{0};                                                     \
+        /* blocks resident on the whole device */                                              \
+        int64_t blocks = (int64_t)blocks_per_cu((const void *)fn, per_cu) * L.cus;             \
         if (want < blocks) blocks = want;                                                      \
         if (blocks > 8) blocks -= blocks % 8;                                                  \
         if (blocks < 1) blocks = 1;                                                            \

@@ -181,8 +181,8 @@ hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const 
 #define X(d, e, f)                                                                           \
     if (in == d && hid == e && nhid == f) {                                                  \
         auto fn = mlp_kernel<d, e, f>;                                                       \
-        static int resident = 0;                                                             \
-        if (!resident) resident = resident_blocks((const void *)fn, cus);                    \
+        static std::atomic<int> per_cu{0};                                                   \
+        const int64_t resident = (int64_t)blocks_per_cu((const void *)fn, per_cu) * cus;     \
         const int64_t blocks = want < resident ? want : resident;                            \
         hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, weights, x, n, \
                            out4);                                                            \
