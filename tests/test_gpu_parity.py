@@ -294,8 +294,13 @@ def test_sweep_rays_by_samples(R, K):
 # Edge cases of the frame path
 # --------------------------------------------------------------------------
 
+# Tiles are pixel blocks whose shape depends on K (16 x 4 rays at K = 1,
+# 16 x 2 at 2, 8 x 2 at 4, 8 x 1 at 8, 4 x 1 at 16, 2 x 1 at 32, one ray at
+# 64, row segments of 64/K rays otherwise): every shape meets ragged edges.
 @pytest.mark.parametrize("H,W,K,views", [(1, 1, 8, 1), (23, 37, 3, 1), (17, 5, 64, 1),
-                                         (9, 11, 5, 3), (33, 31, 1, 2), (8, 8, 7, 16)])
+                                         (9, 11, 5, 3), (33, 31, 1, 2), (8, 8, 7, 16),
+                                         (19, 21, 2, 2), (13, 29, 4, 1), (7, 9, 16, 1),
+                                         (5, 7, 32, 3)])
 def test_ragged_shapes(R, H, W, K, views):
     cfg = synth.TINY64_DENSE.replace(name=f"rag{H}x{W}k{K}v{views}", H=H, W=W, K=K,
                                      views=views, gbuf="iid")
