@@ -3,8 +3,9 @@
 One step = one mixrt_render call over one frame of the 1280x720 workload
 (every stage of the path: ray setup, Eq. 2 calibration, K samples,
 contraction, hash encoding, MLP, compositing), inputs already resident in
-HBM.  For mesh workloads (--workload mesh720p) a step is the ray cast of the
-mesh into the G-buffer followed by that render call.  Prints one JSON line.
+HBM.  For mesh workloads (--workload mesh720p) a step computes the G-buffer
+from the mesh (rasterised by default, ray cast with --geometry raycast) and
+then makes that render call.  Prints one JSON line.
 """
 import argparse
 import json

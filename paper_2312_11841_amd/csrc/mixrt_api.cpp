@@ -3,8 +3,8 @@
 // Host side: descriptor validation (pure host code, no HIP call), the level
 // resolution table, camera constants, and the launches of the kernels in
 // mixrt_render.hip and mixrt_stages.hip on the context's stream; the mesh
-// objects of the geometry stage (grid built in mixrt_mesh.cpp, kernel in
-// mixrt_raycast.hip).
+// objects of the geometry stage (arrays built in mixrt_mesh.cpp, kernels in
+// mixrt_raster.hip and mixrt_raycast.hip).
 #include "mixrt.h"
 
 #include <hip/hip_runtime.h>

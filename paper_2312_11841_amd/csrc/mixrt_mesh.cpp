@@ -1,5 +1,6 @@
-// Host-side construction of the uniform grid of triangle lists that the
-// ray-casting kernel walks (mixrt_raycast.hip).  Deterministic: the result
+// Host-side construction of a mesh's device arrays: the uniform grid of
+// triangle lists that the ray-casting kernel walks (mixrt_raycast.hip) and the
+// triangle records the rasteriser reads (mixrt_raster.hip).  Deterministic: the result
 // depends only on the descriptor, and every cell lists its triangles in
 // ascending index order.
 #include <math.h>

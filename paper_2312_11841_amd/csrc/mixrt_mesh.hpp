@@ -1,7 +1,8 @@
-// Internal interface of the geometry stage: the uniform grid of triangle
-// lists (built on the host in mixrt_mesh.cpp) and the ray-casting kernel
-// that walks it (mixrt_raycast.hip) to produce the G-buffer of the coarse
-// mesh (Fig. 2 step 1).
+// Internal interface of the geometry stage, which produces the G-buffer of
+// the coarse mesh (Fig. 2 step 1): the uploaded mesh (triangle records and the
+// uniform grid of triangle lists, built on the host in mixrt_mesh.cpp), the
+// rasteriser (mixrt_raster.hip) and the ray-casting kernel that walks the grid
+// (mixrt_raycast.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>

@@ -268,7 +268,8 @@ def mesh_plan(positions, faces, uv=None, grid_res=(0, 0, 0), cells_per_face=0.0)
 
 
 class DeviceMesh:
-    """A mesh uploaded into the ray-casting grid; owns its device memory."""
+    """A mesh uploaded for the geometry stage (triangle records and the
+    ray-casting grid); owns its device memory."""
 
     def __init__(self, renderer: "Renderer", mesh, grid_res=(0, 0, 0), cells_per_face=0.0):
         d, _keep = make_mesh_desc(mesh.positions, mesh.faces, getattr(mesh, "uv", None),

@@ -48,7 +48,7 @@ class SceneConfig:
     K: int
     delta: float
     gbuf: str                 # "iid" (cache-hostile), "room" (coherent) or
-                              # "mesh" (computed by ray casting `mesh_seed`'s mesh)
+                              # "mesh" (computed from `mesh_seed`'s mesh)
     tex_R: int
     tex_V: int
     tex_dtype: str            # "f32" | "f16"
@@ -192,7 +192,7 @@ LEVEL_SWEEP = [table3_config(L, 17, False) for L in (1, 2, 4, 8, 16)]
 
 # The whole pipeline including geometry: a seeded 499,712-triangle mesh (a
 # perturbed-sphere room of radius 6 with 24 perturbed spheres and 16 boxes,
-# 11 MB) ray-cast per pixel into the G-buffer, then view720p's displacement,
+# 11 MB) turned into the G-buffer per frame, then view720p's displacement,
 # grid, MLP and compositing at 1280x720.
 MESH720P = VIEW720P.replace(name="mesh720p", gbuf="mesh", mesh_seed=7)
 # Small enough for the oracle's brute-force ray casting of every pixel
