@@ -391,3 +391,24 @@ def test_pipeline_parity(R, cfg, method):
     assert err <= FRAME_TOL
     assert np.all(np.isfinite(got))
     assert hit.mean() > 0.95                          # the room encloses the camera
+
+
+def test_contexts_on_their_own_streams_agree_bitwise():
+    """A context bound to a created (default-priority) stream gives the same
+    rasterised G-buffer and frame as one on the current stream."""
+    cfg = synth.TINY64_MESH
+    sc = synth.make_scene(cfg)
+    outs = []
+    for stream in (None, torch.cuda.Stream()):
+        r = mixrt.Renderer(0, stream=stream, sync_check=True)
+        ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+        torch.cuda.synchronize()
+        dm = mixrt.DeviceMesh(r, sc.mesh)
+        r.rasterize(dm, ds.cams, cfg.W, cfg.H, g1=False, out=(ds.g0, None))
+        out = r.render(ds)
+        r.sync()
+        outs.append((ds.g0.clone(), out.clone()))
+        dm.close()
+        r.close()
+    assert torch.equal(outs[0][0], outs[1][0])
+    assert torch.equal(outs[0][1], outs[1][1])
