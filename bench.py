@@ -258,14 +258,18 @@ def sweep(steps, warmup):
 
 def environment():
     """What the numbers were measured on."""
+    import subprocess
     import torch
+    from paper_2312_11841_amd import microbench as mb
     p = torch.cuda.get_device_properties(0)
-    env = {"device": p.name, "arch": getattr(p, "gcnArchName", None),
-           "compute_units": p.multi_processor_count, "hip": torch.version.hip,
-           "torch": torch.__version__}
-    clk = getattr(p, "clock_rate", None)
-    if clk:
-        env["clock_MHz"] = round(clk / 1000)
+    env = {"device": p.name, "hip": torch.version.hip, "torch": torch.__version__}
+    env.update(mb.device_info(0))
+    try:
+        out = subprocess.run(["/opt/rocm/bin/hipcc", "--version"], capture_output=True,
+                             text=True, timeout=30).stdout
+        env["hipcc"] = next((l.strip() for l in out.splitlines() if "HIP version" in l), None)
+    except (OSError, subprocess.SubprocessError):
+        env["hipcc"] = None
     return env
 
 

@@ -33,6 +33,12 @@ int mixrt_mb_copy(const void *src, void *dst, uint64_t bytes, int blocks, void *
  * out: device float [blocks*256]. */
 int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
 
+/* Properties of HIP device `device` the measurements are quoted against:
+ * peak shader clock (kHz), memory clock (kHz), compute units, L2 bytes, and
+ * the architecture name (NUL-terminated, at most cap bytes written). */
+int mixrt_mb_device_info(int device, int *clock_khz, int *mem_clock_khz, int *cus,
+                         int *l2_bytes, char *arch, int cap);
+
 #ifdef __cplusplus
 }
 #endif

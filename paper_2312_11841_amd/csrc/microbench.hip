@@ -7,6 +7,7 @@
 //   - mfma:   a dependent-free fp16 16x16x32 MFMA loop (matrix-core peak).
 // Entry points launch on the given stream and return hipError_t codes; the
 // caller times them with events on that stream.
+#include <string.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -150,6 +151,23 @@ int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream)
     hipLaunchKernelGGL(mfma_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream, iters,
                        out);
     return hipGetLastError();
+}
+
+int mixrt_mb_device_info(int device, int *clock_khz, int *mem_clock_khz, int *cus,
+                         int *l2_bytes, char *arch, int cap)
+{
+    hipDeviceProp_t p;
+    const hipError_t e = hipGetDeviceProperties(&p, device);
+    if (e != hipSuccess) return (int)e;
+    if (clock_khz) *clock_khz = p.clockRate;
+    if (mem_clock_khz) *mem_clock_khz = p.memoryClockRate;
+    if (cus) *cus = p.multiProcessorCount;
+    if (l2_bytes) *l2_bytes = p.l2CacheSize;
+    if (arch && cap > 0) {
+        strncpy(arch, p.gcnArchName, (size_t)cap - 1);
+        arch[cap - 1] = 0;
+    }
+    return 0;
 }
 
 }  // extern "C"

@@ -23,7 +23,9 @@ def lib():
                                       P, P]
         L.mixrt_mb_copy.argtypes = [P, P, C.c_uint64, C.c_int, P]
         L.mixrt_mb_mfma.argtypes = [C.c_int, C.c_int, P, P]
-        for f in (L.mixrt_mb_gather, L.mixrt_mb_copy, L.mixrt_mb_mfma):
+        IP = C.POINTER(C.c_int)
+        L.mixrt_mb_device_info.argtypes = [C.c_int, IP, IP, IP, IP, C.c_char_p, C.c_int]
+        for f in (L.mixrt_mb_gather, L.mixrt_mb_copy, L.mixrt_mb_mfma, L.mixrt_mb_device_info):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -98,3 +100,13 @@ def mfma(iters: int = 4096, blocks: int | None = None):
     t = _timed(launch)
     flops = blocks * 4 * iters * 8 * (2 * 16 * 16 * 32)
     return {"seconds": t, "TFLOPs": flops / t / 1e12}
+
+
+def device_info(device: int = 0) -> dict:
+    """Clock rates, CU count, L2 size and architecture of a HIP device."""
+    clk, mclk, cus, l2 = C.c_int(), C.c_int(), C.c_int(), C.c_int()
+    arch = C.create_string_buffer(64)
+    _check(lib().mixrt_mb_device_info(device, C.byref(clk), C.byref(mclk), C.byref(cus),
+                                      C.byref(l2), arch, 64))
+    return {"clock_MHz": clk.value // 1000, "mem_clock_MHz": mclk.value // 1000,
+            "compute_units": cus.value, "l2_bytes": l2.value, "arch": arch.value.decode()}
