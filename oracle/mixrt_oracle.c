@@ -14,7 +14,10 @@
  * Paper: "MixRT: Mixed Neural Representations For Real-Time NeRF Rendering"
  * (arXiv 2312.11841).  Steps of one pixel, in the paper's order:
  *   1. ray r = o + t d through the pixel                      (Sec. 3.1)
- *   2. ray-mesh hit p and texture coordinate p_t (G-buffer)   (Fig. 2 step 1)
+ *   2. ray-mesh hit p and texture coordinate p_t: read from a
+ *      G-buffer, or found by testing the ray against every
+ *      triangle of the mesh (the closest hit at t > 1e-4, equal
+ *      t to the lower triangle index)                          (Fig. 2 step 1)
  *   3. calibrated point p_cali from the view-dependent
  *      displacement map                                        (Sec. 4.3.2, Eq. 2)
  *   4. K samples around p_cali, contracted into a ball of
@@ -37,7 +40,11 @@
  *     factor from N_min to N_max; dense indexing when (N_l+1)^3 <= T, else the
  *     XOR-of-primes spatial hash (1, 2654435761, 805459861) modulo T.
  *   - MLP without biases, ReLU hidden layers, outputs (sigma_raw, r, g, b),
- *     sigma = exp, rgb = sigmoid.
+ *     sigma = exp, rgb = sigmoid; with the MLP removed (Tab. 3), feature i
+ *     is added to output i mod 4.
+ *   - 8-bit maps stand for q_offset + q_scale * q.
+ *   - the ray-mesh hit is sampled at the pixel centre, as rasterisation
+ *     does; uv is the barycentric interpolation of the vertex uv.
  *
  * Build: gcc -O2 -fno-fast-math -ffp-contract=off -fopenmp -shared -fPIC.
  */
