@@ -36,6 +36,12 @@ MUTATIONS = {
     "vec3_axis_stride": ("s += y[v] * m[a * nb + v];", "s += y[v] * m[v * 3 + a];"),
     "u8_offset": ("return m->q_offset + m->q_scale * (double)((const uint8_t *)m->data)[i];",
                   "return m->q_scale * (double)((const uint8_t *)m->data)[i];"),
+    "scale_map_takes_coef_pair": ("sc->scale, sc->q_scale[1], sc->q_offset[1]};",
+                                  "sc->scale, sc->q_scale[0], sc->q_offset[0]};"),
+    "coef_map_takes_scale_pair": ("sc->tex, sc->q_scale[0], sc->q_offset[0]};",
+                                  "sc->tex, sc->q_scale[1], sc->q_offset[1]};"),
+    "dense_boundary_hashed": ("if (side * side * side <= T)", "if (side * side * side < T)"),
+    "view_sh_scaled": ("hk[L * F + e] = sh[e];", "hk[L * F + e] = sh[e] * 0.5;"),
     "stored_channels": ("s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * m->C + c);",
                         "s += w[y][x] * map_value(m, ((int64_t)jb[y] * R + ia[x]) * nch + c);"),
     "no_background": ("out[4 * r + ch] = c[ch] + Tend * bg[3 * r + ch];", "out[4 * r + ch] = c[ch];"),

@@ -296,15 +296,18 @@ def _dense_positions(N):
     return v, ((v + 0.5) / N).astype(np.float32)
 
 
-def test_dense_levels_index_every_vertex_once():
-    cfg = synth.TINY64
-    N = oracle.level_resolutions(cfg.L, cfg.N_min, cfg.N_max)
-    for l in (0, 1):
+@pytest.mark.parametrize("L, T, n_min, n_max, levels", [
+    (synth.TINY64.L, synth.TINY64.T, synth.TINY64.N_min, synth.TINY64.N_max, (0, 1)),
+    (2, 4096, 15, 31, (0,)),          # (N+1)^3 == T exactly: still one entry per vertex
+])
+def test_dense_levels_index_every_vertex_once(L, T, n_min, n_max, levels):
+    N = oracle.level_resolutions(L, n_min, n_max)
+    for l in levels:
         n = int(N[l])
-        assert (n + 1) ** 3 <= cfg.T
+        assert (n + 1) ** 3 <= T
         v, x = _dense_positions(n)
-        table = np.zeros((cfg.L, cfg.T, cfg.F), np.float32)
-        corner, idx, _, _ = oracle.hash_encode(x, table, cfg.N_min, cfg.N_max)
+        table = np.zeros((L, T, 2), np.float32)
+        corner, idx, _, _ = oracle.hash_encode(x, table, n_min, n_max)
         assert np.array_equal(corner[:, l], v)
         seen = {}
         for s in range(v.shape[0]):
@@ -503,6 +506,29 @@ def test_samples_are_centred_on_calibrated_point(tex_val):
         assert np.allclose(steps, sc.cfg.delta * d, atol=1e-12)
 
 
+def test_view_direction_sh_feeds_the_mlp():
+    # zero table: the MLP sees only the 16 SH values of the ray direction, so
+    # all K samples share (sigma, rgb) and compositing has a closed form
+    cfg = synth.TINY64.replace(name="shpin", H=6, W=10, K=4, delta=0.05, L=2, log2_T=12,
+                               view_sh_dim=16, widths=(2 * 2 + 16, 4))
+    sc = synth.make_scene(cfg)
+    sc.g0[..., 0] = 0.5
+    sc.table[...] = 0
+    Wt = sc.weights[0].astype(np.float64)
+    assert Wt.shape == (20, 4)
+    out = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays))
+    assert 0.01 < out[:, 3].min() and out[:, 3].max() < 0.99      # neither clear nor opaque
+    bg = np.array(sc.cams[0, 13:16], np.float64)
+    for q in range(cfg.rays):
+        j, i = divmod(q, cfg.W)
+        _, d = oracle.camera_ray(sc.cams[0], cfg.W, cfg.H, i, j)
+        o = oracle.sh_basis(16, d)[0] @ Wt[4:]
+        T_end = np.exp(-cfg.K * np.exp(o[0]) * cfg.delta)
+        rgb = scipy.special.expit(o[1:])
+        assert np.allclose(out[q, :3], rgb * (1 - T_end) + bg * T_end, atol=1e-12)
+        assert out[q, 3] == pytest.approx(1 - T_end, abs=1e-12)
+
+
 def test_miss_pixels_return_background():
     sc = synth.make_scene(synth.TINY64_DENSE)
     sc.g0[0, 0, :4, 0] = [0.0, -1.0, np.nan, np.inf]
@@ -549,6 +575,36 @@ def test_u8_map_is_dequantised_affinely():
     # texel centre: exactly q_offset + q_scale * q
     assert oracle.map_bilinear(q, 1, 2.5 / R, 5.5 / R, qs, qo)[0] == pytest.approx(
         qo + qs * float(q[5, 2, 0]), abs=1e-15)
+
+
+@pytest.mark.parametrize("disp", ["ray", "vec3"])
+def test_u8_maps_use_their_own_affine_pairs_end_to_end(disp):
+    # 8-bit coefficient and scale maps, each constant, with distinct affine
+    # pairs: the mean sample must move by the dequantised values, so taking a
+    # map's pair from the other map shows up as a wrong offset.
+    cfg = synth.TINY64.replace(name="u8pin", H=8, W=8, K=3, delta=0.01, tex_R=4,
+                               tex_dtype="u8", disp=disp, sh_degree=1, L=2, log2_T=12,
+                               widths=(4, 16, 4))
+    sc = synth.make_scene(cfg)
+    sc.g0[..., 0] = 0.5
+    sc.q_scale, sc.q_offset = (0.002, 0.004), (-0.25, 0.1)
+    sc.tex[...] = 125                          # dequantises to exactly 0
+    y00 = 0.5 / np.sqrt(np.pi)
+    if disp == "ray":
+        sc.tex[..., 0] = 200                   # m_0 = -0.25 + 0.002 * 200 = 0.15
+        along, off = y00 * 0.15, np.zeros(3)
+    else:
+        nb = 4
+        sc.tex[..., 0], sc.tex[..., nb], sc.tex[..., 2 * nb] = 225, 50, 175
+        coef = -0.25 + 0.002 * np.array([225.0, 50.0, 175.0])    # (0.2, -0.15, 0.1)
+        sc.scale[...] = 100                    # m_s = 0.1 + 0.004 * 100 = 0.5
+        along, off = 0.0, 0.5 * y00 * coef
+    _, xd, hit = oracle.OracleScene(sc).pixel_samples(np.arange(cfg.rays))
+    assert np.all(hit == 1)
+    for q in range(cfg.rays):
+        j, i = divmod(q, cfg.W)
+        o, d = oracle.camera_ray(sc.cams[0], cfg.W, cfg.H, i, j)
+        assert np.allclose(_uncube(xd[q]).mean(0), o + (0.5 + along) * d + off, atol=1e-7)
 
 
 def test_padding_channels_are_ignored():
