@@ -37,6 +37,13 @@ def test_single_triangle_closed_form():
         want = (1 - b1 - b2) * uv[0] + b1 * uv[1] + b2 * uv[2]
         np.testing.assert_allclose(r["uv"], want, rtol=0, atol=1e-14)
         np.testing.assert_allclose(r["normal"], [0, 0, 1], atol=1e-15)
+        # the cosine between the ray and the unit face normal e1 x e2 = +z:
+        # d_z, negative for a ray against the normal, positive once rewound
+        t, c1, c2, cos = O.ray_triangle([0, 0, 0], d, QUAD, TRI, 0)
+        assert (t, c1, c2) == pytest.approx((r["t"], b1, b2), abs=1e-14)
+        assert cos == pytest.approx(d[2], abs=1e-15) and cos < 0
+        assert O.ray_triangle([0, 0, 0], d, QUAD, TRI[:, [0, 2, 1]], 0)[3] == pytest.approx(
+            -d[2], abs=1e-15)
 
 
 def test_uv_reproduces_an_affine_map():
@@ -86,6 +93,18 @@ def test_equal_distance_goes_to_the_lower_index_and_is_ambiguous():
     assert r["tri"] == 0 and r["ambiguous"]
     r = O.ray_mesh([0, 0, 0], _unit([0.2, 0.1, -1.0]), pos, faces[::-1].copy())
     assert r["tri"] == 0 and r["ambiguous"]   # index 0 of the reversed list
+
+
+def test_a_second_surface_just_behind_is_ambiguous():
+    """A clear hit with a second, clearly hit triangle behind it: within the
+    depth slack t (1 + 1e-4) the pixel is ambiguous, well beyond it is not."""
+    d = _unit([0.2, 0.1, -1.0])
+    faces = np.array([[0, 1, 2], [3, 4, 5]], np.int32)
+    for gap, amb in ((3e-5, True), (1e-3, False)):
+        behind = QUAD * np.array([1, 1, 1 + gap], np.float32)
+        r = O.ray_mesh([0, 0, 0], d, np.concatenate([QUAD, behind]), faces)
+        assert r["tri"] == 0 and r["ambiguous"] == amb
+        assert r["t"] == pytest.approx(2.0 / -d[2], rel=1e-14)
 
 
 def test_shared_edge_is_ambiguous_centre_is_not():
@@ -204,6 +223,23 @@ def test_raycast_pixels_of_a_wall():
     assert np.all(g0[~inside & ok, 0] == -1.0)
     # the wall's lower-right triangle holds the pixels below its diagonal y = x
     np.testing.assert_array_equal(tri[hit] == 0, p[hit, 1] < p[hit, 0])
+
+
+def test_raycast_pixels_minimum_hit_distance():
+    """The G-buffer takes hits beyond t = 1e-4 only: a wall 2e-3 in front of
+    the camera is hit by every pixel, one 5e-5 in front by none."""
+    W, H = 8, 6
+    cam = np.zeros(16, np.float32)
+    cam[:12] = np.concatenate([np.eye(3), np.zeros((3, 1))], 1).reshape(-1)
+    cam[12] = 60.0
+    faces = np.array([[0, 1, 2], [0, 2, 3]], np.int32)
+    for z, hit in ((2e-3, True), (5e-5, False)):
+        pos = np.array([[-1, -1, -z], [1, -1, -z], [1, 1, -z], [-1, 1, -z]], np.float32)
+        mesh = synth.Mesh(positions=pos, faces=faces, uv=np.zeros((4, 2), np.float32))
+        g0, _, tri, _ = O.raycast_pixels(cam[None], W, H, mesh, np.arange(W * H))
+        assert np.all((tri >= 0) == hit)
+        if hit:
+            assert np.all((g0[:, 0] >= np.float32(2e-3)) & (g0[:, 0] < 3e-3))
 
 
 def test_procedural_mesh_is_closed_and_seeded():

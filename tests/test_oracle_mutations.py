@@ -53,6 +53,10 @@ MUTATIONS = {
                     "double nn = sqrt(n[0] * n[0] + n[1] * n[1] + n[2] * n[2]);\n    for (int k = 0; k < 3; ++k)\n        normal[k] = nn > 0.0 ? -n[k] / nn"),
     "q_uses_e2": ("q[0] = s[1] * e1[2] - s[2] * e1[1];", "q[0] = s[1] * e2[2] - s[2] * e2[1];"),
     "no_grazing_slack": ("return fmax(1.0, 0.1 / fmax(fabs(cosine), 1e-12));", "return 1.0;"),
+    "no_depth_slack": ("double reach = best_i >= 0 ? best * (1.0 + eps_t * g) : INFINITY;",
+                       "double reach = best_i >= 0 ? best : INFINITY;"),
+    "gbuffer_t_min": ("uv, 1e-4, &t, bary, uvo, n, &ambiguous);", "uv, 1e-2, &t, bary, uvo, n, &ambiguous);"),
+    "cosine_sign": ("*cosine = -det / sqrt", "*cosine = det / sqrt"),
     "no_near_miss": ("fmin(fmin(b1, b2), 1.0 - b1 - b2) > -eps_b * g)", "fmin(fmin(b1, b2), 1.0 - b1 - b2) > 0.0)"),
 }
 
