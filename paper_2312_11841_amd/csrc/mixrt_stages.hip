@@ -62,24 +62,37 @@ __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict_
                                                      const _Float16 *__restrict__ in, int64_t n,
                                                      float4 *__restrict__ out4)
 {
+    static_assert(IN % 8 == 0, "rows are staged in 16-byte chunks");
     constexpr int LD = IN + 8;
+    constexpr int CH = IN / 8;   // 16-byte chunks per row, and per lane per tile
     __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][kWave * LD];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
     _Float16 *rows = s_rows[wv];
     MlpWeights<IN, HID, NHID> Wt;
     Wt.load(weights, lane);
-    // persistent: weights are loaded once per wave, then 64-row tiles
+    // Persistent: weights are loaded once per wave, then 64-row tiles.  A
+    // tile's rows are one contiguous block of 64 * CH chunks; lane l reads
+    // chunks l, l + 64, ... (coalesced) and writes each into its row in LDS.
+    // (Fetching the next tile into registers during the current one costs
+    // a wave per SIMD of occupancy and was slower.)
     const int64_t n_tiles = (n + kWave - 1) / kWave;
     const int64_t total = (int64_t)gridDim.x * kWavesPerBlock;
     const int c = lane & 15, g = lane >> 4;
     for (int64_t tile = (int64_t)blockIdx.x * kWavesPerBlock + wv; tile < n_tiles; tile += total) {
         const int64_t base = tile * kWave;
-        // stage 64 rows (zeros past n), 16 bytes at a time
-        const int64_t r = base + lane;
+        const h8 *src = (const h8 *)(in + base * IN);
+        h8 buf[CH];
 #pragma unroll
-        for (int e = 0; e < IN; e += 8)
-            *(h8 *)(rows + lane * LD + e) = r < n ? *(const h8 *)(in + r * IN + e) : h8{};
+        for (int e = 0; e < CH; ++e) {
+            const int q = lane + kWave * e;
+            buf[e] = base + q / CH < n ? src[q] : h8{};   // rows past n are zeros
+        }
+#pragma unroll
+        for (int e = 0; e < CH; ++e) {
+            const int q = lane + kWave * e;
+            *(h8 *)(rows + (q / CH) * LD + (q % CH) * 8) = buf[e];
+        }
         wave_lds_sync();
         for (int nt = 0; nt < 4; ++nt) {
             const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
