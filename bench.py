@@ -257,19 +257,17 @@ def sweep(steps, warmup):
 
 
 def environment():
-    """What the numbers were measured on."""
-    import subprocess
+    """What the numbers were measured on.  The compiler version comes from
+    the record the build wrote beside the library: no compiler is started
+    here (under a counter-collecting profiler a child process would inherit
+    its GPU-initialising preload)."""
     import torch
+    from paper_2312_11841_amd import build as hip_build
     from paper_2312_11841_amd import microbench as mb
     p = torch.cuda.get_device_properties(0)
     env = {"device": p.name, "hip": torch.version.hip, "torch": torch.__version__}
     env.update(mb.device_info(0))
-    try:
-        out = subprocess.run(["/opt/rocm/bin/hipcc", "--version"], capture_output=True,
-                             text=True, timeout=30).stdout
-        env["hipcc"] = next((l.strip() for l in out.splitlines() if "HIP version" in l), None)
-    except (OSError, subprocess.SubprocessError):
-        env["hipcc"] = None
+    env["hipcc"] = hip_build.build_info().get("hipcc")
     return env
 
 

@@ -1,4 +1,7 @@
-"""Build the gfx950 HIP library libmixrt.so in-tree with hipcc."""
+"""Build the gfx950 HIP library libmixrt.so in-tree with hipcc, and record
+the compiler version and flags beside it (libmixrt.build.json), so that a
+benchmark can report them without starting the compiler."""
+import json
 import os
 import subprocess
 import sys
@@ -12,6 +15,7 @@ SOURCES = ["mixrt_api.cpp", "mixrt_mesh.cpp", "mixrt_render.hip", "mixrt_stages.
            "mixrt_raycast.hip", "mixrt_raster.hip"]
 MB_LIB = os.path.join(PKG, "libmixrt_microbench.so")
 MB_SOURCES = ["microbench.hip"]
+BUILD_INFO = os.path.join(PKG, "libmixrt.build.json")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -28,7 +32,26 @@ FLAGS = [
 def build(verbose: bool = False, extra=()) -> str:
     _build_one(LIB, SOURCES, verbose, extra)
     _build_one(MB_LIB, MB_SOURCES, verbose, extra)
+    _write_build_info(extra)
     return LIB
+
+
+def _write_build_info(extra):
+    r = subprocess.run([HIPCC, "--version"], capture_output=True, text=True)
+    version = next((l.strip() for l in r.stdout.splitlines() if "HIP version" in l), None)
+    info = {"hipcc": version, "flags": FLAGS + list(extra)}
+    with open(BUILD_INFO + ".tmp", "w") as f:
+        json.dump(info, f)
+    os.replace(BUILD_INFO + ".tmp", BUILD_INFO)
+
+
+def build_info() -> dict:
+    """The record written by the last build (empty if there is none)."""
+    try:
+        with open(BUILD_INFO) as f:
+            return json.load(f)
+    except (OSError, ValueError):
+        return {}
 
 
 def _build_one(lib, sources, verbose, extra):
