@@ -54,7 +54,7 @@ def measured_traffic(workload: str):
 def measured_rooflines(cfg):
     """Achievable rates on this GPU from libmixrt_microbench.so: random
     gathers at the working sets of one hash level and of the whole table,
-    streaming copy, fp16 MFMA."""
+    streaming copy, streaming read, fp16 MFMA."""
     from paper_2312_11841_amd import microbench as mb
     eb = 2 if cfg.table_dtype == "f16" else 4
     entry = cfg.F * eb
@@ -65,7 +65,14 @@ def measured_rooflines(cfg):
         r = mb.gather(size, 4 if entry <= 4 else (8 if entry <= 8 else 16), 0, iters=128)
         out["gather_random_lane_loads_per_s"][name] = {"bytes": size,
                                                        "value": round(r["lane_loads_per_s"])}
-    out["copy_GBps"] = round(mb.copy(1 << 30)["GBps"], 1)
+    # streaming rates peak at a few blocks per CU (more blocks contend for
+    # DRAM pages): the best of a short sweep, with the block count it took
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for name, fn, per_cu in (("copy", mb.copy, (2, 3, 4)), ("read", mb.read, (1, 1.5, 2, 3))):
+        best = max((fn(1 << 30, blocks=int(k * cus)) for k in per_cu), key=lambda r: r["GBps"])
+        out[f"{name}_GBps"] = round(best["GBps"], 1)
+        out[f"{name}_blocks"] = int(best.get("blocks") or 0)
     out["mfma_f16_TFLOPs"] = round(mb.mfma()["TFLOPs"], 1)
     return out
 

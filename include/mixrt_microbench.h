@@ -29,6 +29,11 @@ int mixrt_mb_gather(const void *table, uint64_t table_bytes, int width, int load
  * grid-stride loop over blocks x 256 threads. */
 int mixrt_mb_copy(const void *src, void *dst, uint64_t bytes, int blocks, void *stream);
 
+/* Streaming read of `bytes` (a multiple of 16) from src with a grid-stride
+ * loop over blocks x 256 threads, four 16-byte loads per thread in flight;
+ * sink: device uint32 [blocks*256] (written, keeps the loads live). */
+int mixrt_mb_read(const void *src, uint64_t bytes, int blocks, uint32_t *sink, void *stream);
+
 /* iters x 8 independent fp16 16x16x32 MFMAs per wave; blocks x 256 threads;
  * out: device float [blocks*256]. */
 int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);

@@ -3,7 +3,8 @@
 //   - gather: random or coalesced loads of 4/8/16 bytes per lane from a
 //     table of a given size (the access pattern of hash-grid lookups), which
 //     measures the achievable gather rate by working set (L1/L2/MALL/HBM);
-//   - copy:   a streaming copy (HBM bandwidth);
+//   - copy:   a streaming copy (HBM bandwidth, reads and writes);
+//   - read:   a streaming read (HBM read bandwidth, the hot path's mix);
 //   - mfma:   a dependent-free fp16 16x16x32 MFMA loop (matrix-core peak).
 // Entry points launch on the given stream and return hipError_t codes; the
 // caller times them with events on that stream.
@@ -78,6 +79,28 @@ __global__ __launch_bounds__(kBlock) void copy_kernel(const uint4 *__restrict__ 
         dst[i] = src[i];
 }
 
+// Grid-stride read of n 16-byte elements, four independent loads per thread
+// in flight per iteration; each thread writes one word (the XOR of what it
+// read) so the loads stay live.
+__global__ __launch_bounds__(kBlock) void read_kernel(const uint4 *__restrict__ src, uint64_t n,
+                                                      uint32_t *__restrict__ sink)
+{
+    const uint64_t stride = (uint64_t)gridDim.x * kBlock;
+    uint64_t i = (uint64_t)blockIdx.x * kBlock + threadIdx.x;
+    uint32_t acc = 0;
+    for (; i + 3 * stride < n; i += 4 * stride) {
+        const uint4 a = src[i], b = src[i + stride], c = src[i + 2 * stride],
+                    d = src[i + 3 * stride];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w ^ b.x ^ b.y ^ b.z ^ b.w ^ c.x ^ c.y ^ c.z ^ c.w ^ d.x ^ d.y ^
+               d.z ^ d.w;
+    }
+    for (; i < n; i += stride) {
+        const uint4 a = src[i];
+        acc ^= a.x ^ a.y ^ a.z ^ a.w;
+    }
+    sink[(uint64_t)blockIdx.x * kBlock + threadIdx.x] = acc;
+}
+
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -142,6 +165,14 @@ int mixrt_mb_copy(const void *src, void *dst, uint64_t bytes, int blocks, void *
     if (!src || !dst || (bytes & 15) || blocks < 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream,
                        (const uint4 *)src, (uint4 *)dst, bytes / 16);
+    return hipGetLastError();
+}
+
+int mixrt_mb_read(const void *src, uint64_t bytes, int blocks, uint32_t *sink, void *stream)
+{
+    if (!src || !sink || (bytes & 15) || blocks < 1) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(read_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream,
+                       (const uint4 *)src, bytes / 16, sink);
     return hipGetLastError();
 }
 

@@ -22,6 +22,7 @@ typedef uint64_t u64a4 __attribute__((aligned(4)));
 typedef unsigned __int128 u128a8 __attribute__((aligned(8)));
 
 __device__ __forceinline__ h2 word_h2(uint32_t w) { return __builtin_bit_cast(h2, w); }
+__device__ __forceinline__ uint32_t h2_word(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 
 constexpr int kMaxViews = 16;
 constexpr int kMaxLevels = 32;
@@ -618,11 +619,12 @@ __device__ __forceinline__ void hash_group(const GridParams &gp, int l0, float x
 //   mfma_f32_16x16x16_f16  A: row c, k = 4g..4g+3;  B: column c, k = 4g..4g+3
 //   D (both):              column c, rows 4g..4g+3
 //
-// Every MFMA here starts from a zero accumulator and the partial products of
-// the K chunks are summed on the VALU: no MFMA reads another MFMA's result as
-// its C operand.  With this compiler, chains that fed a 16x16x32 result into
-// a 16x16x16 accumulate (with a different destination register) read a stale
-// accumulator on gfx950; the zero-C form has no such dependency.
+// The 32-deep K chunks of a tile accumulate in place (16x16x32 into
+// 16x16x32, the same registers as C and D).  A 16-deep remainder starts from
+// a zero accumulator and is added on the VALU: with this compiler, chains that
+// fed a 16x16x32 result into a 16x16x16 accumulate (with a different
+// destination register) read a stale accumulator on gfx950, while in-place
+// 16x16x32 chains and zero-C products were exact.
 // --------------------------------------------------------------------------
 
 // Input slot -> neuron for a layer fed from the previous layer's registers.
@@ -696,7 +698,7 @@ __device__ __forceinline__ f4 mfma_tile(const AL &A, int mt, const h8 *b32, h4 b
         acc = __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
 #pragma unroll
     for (int ch = 1; ch < NC; ++ch)
-        acc += __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], zero, 0, 0, 0);
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(A.a32[mt][ch], b32[ch], acc, 0, 0, 0);
     if (NC > 0 && R16)
         acc += __builtin_amdgcn_mfma_f32_16x16x16f16(A.a16[mt], b16, zero, 0, 0, 0);
     return acc;
@@ -709,17 +711,20 @@ __device__ __forceinline__ void layer_from_regs(const LayerA<KIN, MOUT, true> &A
     constexpr int NC = LayerA<KIN, MOUT, true>::NC, R16 = LayerA<KIN, MOUT, true>::R16;
     h8 b32[NC > 0 ? NC : 1];
     h4 b16 = {};
+    // Each packed pair is one 32-bit register already in operand order, so
+    // the operands are assembled whole (element-wise construction costs
+    // shifts, ORs and permutes per half).
 #pragma unroll
     for (int ch = 0; ch < NC; ++ch) {
         const f4 lo = in.acc[2 * ch], hi = in.acc[2 * ch + 1];
-        const h2 p0 = relu_pack(lo[0], lo[1]), p1 = relu_pack(lo[2], lo[3]);
-        const h2 p2 = relu_pack(hi[0], hi[1]), p3 = relu_pack(hi[2], hi[3]);
-        b32[ch] = h8{p0.x, p0.y, p1.x, p1.y, p2.x, p2.y, p3.x, p3.y};
+        const uint4 w = {h2_word(relu_pack(lo[0], lo[1])), h2_word(relu_pack(lo[2], lo[3])),
+                         h2_word(relu_pack(hi[0], hi[1])), h2_word(relu_pack(hi[2], hi[3]))};
+        b32[ch] = __builtin_bit_cast(h8, w);
     }
     if (R16) {
-        const h2 p0 = relu_pack(in.acc[0][0], in.acc[0][1]);
-        const h2 p1 = relu_pack(in.acc[0][2], in.acc[0][3]);
-        b16 = h4{p0.x, p0.y, p1.x, p1.y};
+        const uint2 w = {h2_word(relu_pack(in.acc[0][0], in.acc[0][1])),
+                         h2_word(relu_pack(in.acc[0][2], in.acc[0][3]))};
+        b16 = __builtin_bit_cast(h4, w);
     }
 #pragma unroll
     for (int mt = 0; mt < Act<MOUT>::MT; ++mt)

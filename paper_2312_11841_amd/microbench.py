@@ -1,5 +1,6 @@
 """Roofline microbenchmarks (libmixrt_microbench.so): achievable gather rate by
-working-set size, streaming-copy bandwidth and fp16 MFMA throughput on the
+working-set size, streaming-copy and streaming-read bandwidth and fp16 MFMA
+throughput on the
 current GPU.  These calibrate the rendering kernel's measured bounds; they
 are not part of the rendering path."""
 from __future__ import annotations
@@ -22,10 +23,12 @@ def lib():
         L.mixrt_mb_gather.argtypes = [P, C.c_uint64, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                       P, P]
         L.mixrt_mb_copy.argtypes = [P, P, C.c_uint64, C.c_int, P]
+        L.mixrt_mb_read.argtypes = [P, C.c_uint64, C.c_int, P, P]
         L.mixrt_mb_mfma.argtypes = [C.c_int, C.c_int, P, P]
         IP = C.POINTER(C.c_int)
         L.mixrt_mb_device_info.argtypes = [C.c_int, IP, IP, IP, IP, C.c_char_p, C.c_int]
-        for f in (L.mixrt_mb_gather, L.mixrt_mb_copy, L.mixrt_mb_mfma, L.mixrt_mb_device_info):
+        for f in (L.mixrt_mb_gather, L.mixrt_mb_copy, L.mixrt_mb_read, L.mixrt_mb_mfma,
+                  L.mixrt_mb_device_info):
             f.restype = C.c_int
         _lib = L
     return _lib
@@ -85,7 +88,23 @@ def copy(bytes_: int = 1 << 30, blocks: int | None = None):
         _check(lib().mixrt_mb_copy(src.data_ptr(), dst.data_ptr(), bytes_, blocks, s.cuda_stream))
 
     t = _timed(launch)
-    return {"bytes": bytes_, "seconds": t, "GBps": 2 * bytes_ / t / 1e9}
+    return {"bytes": bytes_, "blocks": blocks, "seconds": t, "GBps": 2 * bytes_ / t / 1e9}
+
+
+def read(bytes_: int = 1 << 30, blocks: int | None = None):
+    """Streaming read of bytes_; returns the read bandwidth."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = blocks or cus * 8
+    src = torch.empty(bytes_, dtype=torch.uint8, device="cuda").fill_(1)
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+
+    def launch(s):
+        _check(lib().mixrt_mb_read(src.data_ptr(), bytes_, blocks, sink.data_ptr(),
+                                   s.cuda_stream))
+
+    t = _timed(launch)
+    return {"bytes": bytes_, "blocks": blocks, "seconds": t, "GBps": bytes_ / t / 1e9}
 
 
 def mfma(iters: int = 4096, blocks: int | None = None):

@@ -35,6 +35,25 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) <= exported
 
 
+def test_microbench_library_exports_every_declared_symbol():
+    from paper_2312_11841_amd import microbench
+    text = open(os.path.join(ROOT, "include", "mixrt_microbench.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    declared = sorted(set(re.findall(r"\b(mixrt_mb_\w+)\s*\(", text)))
+    assert declared
+    L = microbench.lib()
+    for name in declared:
+        assert getattr(L, name).argtypes is not None, name   # bound with a signature
+    out = subprocess.run(["nm", "-D", "--defined-only", microbench.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r" T (mixrt_mb_\w+)", out))
+    assert set(declared) <= exported
+
+
+def test_every_header_is_checked():
+    assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["mixrt.h", "mixrt_microbench.h"]
+
+
 def test_struct_layout_matches_header():
     structs = {"mixrt_create_info": mixrt.CreateInfo, "mixrt_gbuffer": mixrt.GBuffer,
                "mixrt_camera": mixrt.Camera, "mixrt_disp_tex": mixrt.DispTex,
