@@ -206,10 +206,12 @@ def time_workload(cfg, steps, warmup):
 
 
 def paper_tables(steps, warmup):
-    """Tab. 3 and Tab. 6 of the paper re-run on this GPU, plus a level sweep."""
+    """Tab. 3 and Tab. 6 of the paper re-run on this GPU, plus level and
+    table-size sweeps."""
     from paper_2312_11841_amd import synth
     rows = []
-    for cfg in synth.TABLE3 + synth.LEVEL_SWEEP + [synth.PAPER720P, synth.PAPER720P_NOVDD]:
+    for cfg in (synth.TABLE3 + synth.LEVEL_SWEEP + synth.SIZE_SWEEP +
+                [synth.PAPER720P, synth.PAPER720P_NOVDD]):
         if any(r["workload"] == cfg.name for r in rows):
             continue
         ms = time_workload(cfg, steps, warmup)

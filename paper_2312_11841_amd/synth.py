@@ -189,6 +189,8 @@ def table3_config(L: int, log2_T: int, mlp: bool) -> SceneConfig:
 TABLE3 = [table3_config(8, 17, True), table3_config(8, 17, False), table3_config(1, 17, False),
           table3_config(8, 5, False), table3_config(8, 22, False)]
 LEVEL_SWEEP = [table3_config(L, 17, False) for L in (1, 2, 4, 8, 16)]
+# Table size at L = 8: Tab. 3's 2^5, 2^17 and 2^22, and the deployed 2^21.
+SIZE_SWEEP = [table3_config(8, t, False) for t in (5, 17, 21, 22)]
 
 # The whole pipeline including geometry: a seeded 499,712-triangle mesh (a
 # perturbed-sphere room of radius 6 with 24 perturbed spheres and 16 boxes,
@@ -205,7 +207,7 @@ TINY64_MESH = TINY64_DENSE.replace(
 CONFIGS = {c.name: c for c in (TINY64, TINY64_DENSE, VIEW720P, VIEW720P_DENSE,
                                BATCH8X1080P, DEPLOYED720P, PAPER720P, PAPER720P_NOVDD,
                                TINY64_VEC3, TINY64_U8, TINY64_NODISP, MESH720P, TINY64_MESH,
-                               *TABLE3, *LEVEL_SWEEP)}
+                               *TABLE3, *LEVEL_SWEEP, *SIZE_SWEEP)}
 
 
 # --- scene container ----------------------------------------------------------

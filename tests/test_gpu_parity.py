@@ -233,6 +233,9 @@ FRAME_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.VIEW720P_D
               synth.DEPLOYED720P, synth.PAPER720P, synth.PAPER720P_NOVDD, synth.TINY64_VEC3,
               synth.TINY64_U8, synth.TINY64_NODISP, *synth.TABLE3,
               synth.TINY64_DENSE.replace(name="tiny64_nomlp", widths=(16,), seed=16)]
+# the level and table-size sweeps' remaining points
+FRAME_CFGS += list({c.name: c for c in synth.LEVEL_SWEEP + synth.SIZE_SWEEP
+                    if c.name not in {f.name for f in FRAME_CFGS}}.values())
 
 
 @pytest.mark.parametrize("cfg", FRAME_CFGS, ids=lambda c: c.name)
