@@ -131,6 +131,14 @@ def test_validate_accepts_every_workload(cfg):
     assert rc == mixrt.MIXRT_OK, msg
 
 
+def test_validate_accepts_every_random_sweep_config():
+    from randcfg import SEEDS, random_config
+    for seed in SEEDS:
+        cfg = random_config(seed)
+        rc, msg = _Desc(cfg).validate()
+        assert rc == mixrt.MIXRT_OK, (cfg, msg)
+
+
 BAD = [
     ("gbuf.views", lambda d: setattr(d.gbuf, "views", 0), mixrt.MIXRT_EINVAL),
     ("gbuf.views max", lambda d: setattr(d.gbuf, "views", 17), mixrt.MIXRT_EINVAL),

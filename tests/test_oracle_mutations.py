@@ -154,12 +154,27 @@ def _pins_against(name, work):
 
 @pytest.fixture(scope="module")
 def outcomes(tmp_path_factory):
-    # every planted mistake is built and checked once, several at a time
+    """name -> (exit status, output).  In a single process every planted
+    mistake is built and checked up front, several at a time; under
+    pytest-xdist the workers already run in parallel, so each checks only the
+    mistakes of the tests it is given."""
     work = str(tmp_path_factory.mktemp("mutants"))
+    if os.environ.get("PYTEST_XDIST_WORKER"):
+        return _Lazy(work)
     workers = max(1, min(8, os.cpu_count() or 1))
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
         names = sorted(MUTATIONS)
         return dict(zip(names, ex.map(lambda n: _pins_against(n, work), names)))
+
+
+class _Lazy(dict):
+    def __init__(self, work):
+        super().__init__()
+        self.work = work
+
+    def __missing__(self, name):
+        self[name] = _pins_against(name, self.work)
+        return self[name]
 
 
 @pytest.mark.parametrize("name", sorted(MUTATIONS))
