@@ -262,7 +262,7 @@ def raycast_pixels(cams, W: int, H: int, mesh, pix, threads: int = 1):
     ambiguous [n] bool)."""
     cams = _c(cams, np.float32).reshape(-1, 16)
     pos, fc = _c(mesh.positions, np.float32), _c(mesh.faces, np.int32)
-    uv = _c(mesh.uv, np.float32)
+    uv = None if mesh.uv is None else _c(mesh.uv, np.float32)   # NULL: no texture coordinates
     pix = _c(pix, np.int64).reshape(-1)
     g0, n = np.zeros((pix.size, 4)), np.zeros((pix.size, 3))
     tri, amb = np.zeros(pix.size, np.int64), np.zeros(pix.size, np.int32)

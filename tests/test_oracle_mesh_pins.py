@@ -225,6 +225,24 @@ def test_raycast_pixels_of_a_wall():
     np.testing.assert_array_equal(tri[hit] == 0, p[hit, 1] < p[hit, 0])
 
 
+def test_raycast_pixels_without_uv_gives_zero_uv():
+    """A mesh without texture coordinates: hits keep t and the normal, uv is 0."""
+    W, H = 6, 5
+    cam = np.zeros(16, np.float32)
+    cam[:12] = np.concatenate([np.eye(3), np.zeros((3, 1))], 1).reshape(-1)
+    cam[12] = 60.0
+    pos = np.array([[-9, -9, -3], [9, -9, -3], [0, 9, -3]], np.float32)
+    mesh = synth.Mesh(positions=pos, faces=TRI, uv=None)
+    g0, nrm, tri, _ = O.raycast_pixels(cam[None], W, H, mesh, np.arange(W * H))
+    assert np.all(tri == 0)
+    assert np.all(g0[:, 1:] == 0)
+    with_uv = synth.Mesh(positions=pos, faces=TRI, uv=np.ones((3, 2), np.float32))
+    g0u, nrmu, _, _ = O.raycast_pixels(cam[None], W, H, with_uv, np.arange(W * H))
+    np.testing.assert_array_equal(g0[:, 0], g0u[:, 0])
+    np.testing.assert_array_equal(nrm, nrmu)
+    np.testing.assert_allclose(g0u[:, 1:3], 1.0, atol=1e-12)
+
+
 def test_raycast_pixels_minimum_hit_distance():
     """The G-buffer takes hits beyond t = 1e-4 only: a wall 2e-3 in front of
     the camera is hit by every pixel, one 5e-5 in front by none."""
