@@ -34,6 +34,14 @@ BUILT = [
 SEEDS = list(range(1000, 1048))
 
 
+def _random_rotation(rng: np.random.Generator) -> np.ndarray:
+    """A uniformly random rotation matrix (from a normalised Gaussian quaternion)."""
+    w, x, y, z = (q := rng.normal(size=4)) / np.linalg.norm(q)
+    return np.array([[1 - 2 * (y * y + z * z), 2 * (x * y - w * z), 2 * (x * z + w * y)],
+                     [2 * (x * y + w * z), 1 - 2 * (x * x + z * z), 2 * (y * z - w * x)],
+                     [2 * (x * z - w * y), 2 * (y * z + w * x), 1 - 2 * (x * x + y * y)]])
+
+
 def random_config(seed: int) -> synth.SceneConfig:
     rng = np.random.default_rng(seed)
     tex, F, f16, m_in, hid, nhid = BUILT[seed % len(BUILT)]
@@ -73,14 +81,53 @@ def random_scene(cfg: synth.SceneConfig) -> synth.Scene:
     sc = synth.make_scene(cfg)
     rng = np.random.default_rng(cfg.seed + 7919)
     for v in range(cfg.views):
-        q = rng.normal(size=4)
-        w, x, y, z = q / np.linalg.norm(q)
-        R = np.array([[1 - 2 * (y * y + z * z), 2 * (x * y - w * z), 2 * (x * z + w * y)],
-                      [2 * (x * y + w * z), 1 - 2 * (x * x + z * z), 2 * (y * z - w * x)],
-                      [2 * (x * z - w * y), 2 * (y * z + w * x), 1 - 2 * (x * x + y * y)]])
+        R = _random_rotation(rng)
         o = rng.uniform(-1.0, 1.0, 3)
         sc.cams[v, :12] = np.concatenate([R, o[:, None]], axis=1).reshape(-1).astype(np.float32)
     flat = sc.g0.reshape(-1, 4)
     miss = rng.random(flat.shape[0]) < 0.05
     flat[miss, 0] = rng.choice(np.array([-1.0, 0.0, np.nan, np.inf], np.float32), miss.sum())
     return sc
+
+
+# --- random triangle soups for the geometry stage --------------------------
+
+MESH_SEEDS = list(range(2000, 2024))
+
+
+def random_soup(seed: int):
+    """A seeded triangle soup mixing small, sliver, huge, near-camera and
+    degenerate (a repeated vertex) triangles, with or without uv, and the
+    cameras, image size and grid options to view it with."""
+    rng = np.random.default_rng(seed)
+    n = int(np.exp(rng.uniform(0.0, np.log(3000.0))))
+    kinds = rng.choice(5, n, p=[0.55, 0.15, 0.1, 0.1, 0.1])
+    tris = np.zeros((n, 3, 3))
+    for t in range(n):
+        c = rng.uniform(-4.0, 4.0, 3)
+        if kinds[t] == 0:                               # small
+            tris[t] = c + rng.normal(0.0, rng.uniform(0.01, 0.3), (3, 3))
+        elif kinds[t] == 1:                             # sliver: one short edge
+            a, b = c, c + rng.normal(0.0, 0.5, 3)
+            tris[t] = [a, b, b + rng.normal(0.0, 1e-3, 3)]
+        elif kinds[t] == 2:                             # huge
+            tris[t] = c + rng.normal(0.0, rng.uniform(5.0, 40.0), (3, 3))
+        elif kinds[t] == 3:                             # close to the cameras
+            tris[t] = rng.normal(0.0, rng.uniform(0.02, 0.3), 3) + rng.normal(0.0, 0.1, (3, 3))
+        else:                                           # degenerate
+            tris[t] = c + rng.normal(0.0, 0.3, (3, 3))
+            tris[t, 2] = tris[t, 0]
+    positions = tris.reshape(-1, 3).astype(np.float32)
+    faces = np.arange(3 * n, dtype=np.int32).reshape(n, 3)
+    uv = rng.uniform(0.0, 1.0, (3 * n, 2)).astype(np.float32) if rng.random() < 0.8 else None
+    mesh = synth.Mesh(positions=positions, faces=faces, uv=uv)
+    views = int(rng.integers(1, 4))
+    cams = np.zeros((views, 16), np.float32)
+    for v in range(views):
+        R = _random_rotation(rng)
+        cams[v, :12] = np.concatenate([R, rng.normal(0.0, 0.05, (3, 1))], 1).reshape(-1)
+        cams[v, 12] = rng.uniform(30.0, 120.0)
+    W, H = int(rng.integers(1, 49)), int(rng.integers(1, 49))
+    grid_res = tuple(int(g) for g in rng.integers(1, 24, 3)) if rng.random() < 0.3 else (0, 0, 0)
+    cells_per_face = float(rng.choice([0.0, 0.5, 2.0, 8.0, 32.0]))
+    return mesh, cams, W, H, grid_res, cells_per_face

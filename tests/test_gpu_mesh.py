@@ -7,13 +7,17 @@ Bars, for pixels the oracle does not flag as ambiguous (a hit within the
 rounding reach of an edge, another triangle within it in depth, or a near
 miss; grazing rays widen that reach):
   - triangle index and hit/miss: bit-exact;
-  - t: |dt| <= 1e-5 t / |cos|.  The fp32 ray direction carries about 2e-7
-    relative error, which moves the hit by t 2e-7 / |cos| along the ray, and
-    the fp32 Moller-Trumbore solve adds a few ulp times a condition number
-    of about 1 / (|cos| sin(corner angle)); 1e-5 leaves a 10x margin;
-  - uv: |duv| <= 1e-4 spread / |cos| + 1e-6, spread = the largest uv
-    difference between the triangle's corners (barycentric error of the
-    moved hit point times the uv range it scales);
+  - t: |dt| <= (1e-5 t + 1e-6 D S) / |cos|.  The fp32 ray direction carries
+    about 2e-7 relative error, which moves the hit by t 2e-7 / |cos| along
+    the ray; the fp32 Moller-Trumbore solve forms t from products of
+    vectors of length ~D (D = the farthest vertex's distance from the
+    camera), so it adds a few ulp of D times the condition number S / |cos|
+    (S = L_max^2 / (2 area), about 1 / sin of the smallest corner angle);
+    both coefficients leave a 10x margin or more;
+  - uv: |duv| <= spread (1e-4 + 1e-6 D S / L_max) / |cos| + 1e-6, spread =
+    the largest uv difference between the triangle's corners (the
+    barycentric error of the moved hit point, ~ulp(D) S / L_max, times the
+    uv range it scales); exactly 0 for a mesh without uv;
   - normal: 1e-4 absolute (edges are differenced in fp32 on the GPU).
 Ambiguous pixels: the GPU's triangle must be one the oracle also finds hit or
 nearly hit, at the same distance, no farther than the nearest hit's reach;
@@ -104,12 +108,27 @@ def _check_gbuffer(mesh, cams, W, H, g0, g1, pix, label, max_amb=0.01):
                       for v, ii, jj in zip(view, i, j)])
         cos = np.abs(np.einsum("ij,ij->i", d, ref_n[hit]))
         inv_cos = 1.0 / np.maximum(cos, 1e-3)
-        terr = np.abs(got0[hit, 0] - ref_g0[hit, 0]) / ref_g0[hit, 0]
-        assert np.all(terr <= 1e-5 * inv_cos), terr.max()
-        corners = mesh.uv.astype(np.float64)[mesh.faces[ref_tri[hit]]]      # [n, 3, 2]
-        spread = (corners.max(1) - corners.min(1)).max(1)
+        # conditioning of the fp32 solve: the vertices' distance from the
+        # camera, the longest edge and the triangle's shape L_max^2 / (2 area)
+        P = mesh.positions.astype(np.float64)[mesh.faces[ref_tri[hit]]]    # [n, 3, 3]
+        origin = np.asarray(cams, np.float64).reshape(-1, 16)[view][:, [3, 7, 11]]
+        dist = np.linalg.norm(P - origin[:, None, :], axis=2).max(1)
+        edges = np.stack([P[:, 1] - P[:, 0], P[:, 2] - P[:, 1], P[:, 0] - P[:, 2]], 1)
+        l_max = np.linalg.norm(edges, axis=2).max(1)
+        area = 0.5 * np.linalg.norm(np.cross(edges[:, 0], -edges[:, 2]), axis=1)
+        shape = l_max ** 2 / (2.0 * area)
+        t_ref = ref_g0[hit, 0]
+        dt = np.abs(got0[hit, 0] - t_ref)
+        assert np.all(dt <= (1e-5 * t_ref + 1e-6 * dist * shape) * inv_cos), (dt / t_ref).max()
+        terr = dt / t_ref
         uerr = np.abs(got0[hit, 1:3] - ref_g0[hit, 1:3]).max(1)
-        assert np.all(uerr <= 1e-4 * spread * inv_cos + 1e-6), uerr.max()
+        if mesh.uv is None:
+            assert np.all(got0[hit, 1:3] == 0)
+        else:
+            corners = mesh.uv.astype(np.float64)[mesh.faces[ref_tri[hit]]]      # [n, 3, 2]
+            spread = (corners.max(1) - corners.min(1)).max(1)
+            bar = spread * (1e-4 + 1e-6 * dist * shape / l_max) * inv_cos + 1e-6
+            assert np.all(uerr <= bar), uerr.max()
         assert np.all(got0[hit, 3] == 0)
         nerr = np.abs(got1[hit, :3] - ref_n[hit]).max()
         assert nerr <= 1e-4, nerr
@@ -127,8 +146,13 @@ def _check_gbuffer(mesh, cams, W, H, g0, g1, pix, label, max_amb=0.01):
         assert sol is not None
         t, b1, b2, c = sol
         g = max(1.0, 0.1 / max(abs(c), 1e-12))
+        P = mesh.positions.astype(np.float64)[mesh.faces[int(gid[q])]]
+        dist = np.linalg.norm(P - o, axis=1).max()
+        e = np.stack([P[1] - P[0], P[2] - P[1], P[0] - P[2]])
+        shape = (np.linalg.norm(e, axis=1).max() ** 2
+                 / np.linalg.norm(np.cross(e[0], -e[2])))
         assert min(b1, b2, 1 - b1 - b2) > -4e-4 * g
-        assert abs(got0[q, 0] - t) <= 1e-5 * t * g
+        assert abs(got0[q, 0] - t) <= (1e-5 * t + 1e-6 * dist * shape) * g
         if ref_tri[q] >= 0:
             assert t <= ref_g0[q, 0] * (1 + 2e-4 * g)
 
