@@ -179,13 +179,19 @@ def make_sampling(K: int, delta: float, t_term: float) -> Sampling:
 
 
 def make_grid(table, N_min: int, N_max: int) -> HashGrid:
+    """Descriptor of a device table [L][T][F]; it holds a reference to the
+    tensor, so the memory it points at lives as long as the descriptor."""
     L, T, F = table.shape
-    return HashGrid(L, int(T).bit_length() - 1, F, int(N_min), int(N_max),
-                    _dtype_code(table), _ptr(table))
+    g = HashGrid(L, int(T).bit_length() - 1, F, int(N_min), int(N_max),
+                 _dtype_code(table), _ptr(table))
+    g._keep = table
+    return g
 
 
 def make_mlp(weights, widths, view_sh_dim: int) -> Mlp:
+    """Descriptor of device weights; it holds a reference to the tensor."""
     m = Mlp()
+    m._keep = weights
     m.n_layers = len(widths) - 1
     for i, w in enumerate(widths):
         m.width[i] = int(w)

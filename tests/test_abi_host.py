@@ -131,6 +131,23 @@ def test_validate_accepts_every_workload(cfg):
     assert rc == mixrt.MIXRT_OK, msg
 
 
+def test_descriptors_keep_their_tensors_alive():
+    """A grid or MLP descriptor made from a tensor holds the tensor: the
+    device memory it points at cannot be freed and reused while it lives."""
+    import gc
+    import weakref
+    torch = pytest.importorskip("torch")
+    t = torch.zeros((2, 16, 2), dtype=torch.float16)
+    w = torch.zeros(16 * 16 + 16 * 4, dtype=torch.float16)
+    rt, rw = weakref.ref(t), weakref.ref(w)
+    g = mixrt.make_grid(t, 4, 8)
+    m = mixrt.make_mlp(w, (16, 16, 4), 0)
+    del t, w
+    gc.collect()
+    assert rt() is not None and g.data == rt().data_ptr()
+    assert rw() is not None and m.data == rw().data_ptr()
+
+
 def test_validate_accepts_every_random_sweep_config():
     from randcfg import SEEDS, random_config
     for seed in SEEDS:

@@ -37,3 +37,34 @@ def test_random_workload_matches_oracle(R, seed):
     err = np.abs(got - ref).max()
     print(f"  max |gpu - oracle| = {err:.3e} over {cfg.rays} px", flush=True)
     assert err <= FRAME_TOL + cfg.t_term
+
+
+@pytest.mark.parametrize("seed", list(range(3000, 3024)))
+def test_random_grid_hash_encode_bit_exact(R, seed):
+    """The hash stage alone on random grids: L, T, F, table dtype and level
+    resolutions (dense and hashed levels, N up to 65,536) drawn at random,
+    queried at random and adversarial positions; corners and table indices
+    bit-exact, weights and features within the stage bars."""
+    import torch
+    from test_gpu_parity import _adversarial_x
+    rng = np.random.default_rng(seed)
+    L, F = int(rng.integers(1, 33)), int(rng.choice([2, 4]))
+    f16 = bool(rng.random() < 0.5)
+    log2_T = int(rng.integers(4, 21))
+    while L * (1 << log2_T) * F * 4 > 64 << 20:
+        log2_T -= 1
+    n_min = int(rng.integers(1, 65))
+    n_max = int(min(65536, n_min * np.exp(rng.uniform(0.0, np.log(4096.0)))))
+    print("grid", seed, L, log2_T, F, "f16" if f16 else "f32", n_min, n_max, flush=True)
+    table = rng.uniform(-1.0, 1.0, (L, 1 << log2_T, F)).astype(np.float16 if f16 else np.float32)
+    N = oracle.level_resolutions(L, n_min, n_max)
+    x = _adversarial_x(N, rng, 3000 + seed % 61)
+    tt = torch.from_numpy(table).cuda()
+    grid = mixrt.make_grid(tt, n_min, n_max)
+    got = R.hash_encode(grid, torch.from_numpy(x).cuda())
+    R.sync()
+    corner, idx, w, feat = oracle.hash_encode(x, table, n_min, n_max)
+    assert np.array_equal(got["corner"].cpu().numpy(), corner)
+    assert np.array_equal(got["idx"].cpu().numpy().view(np.uint32), idx)
+    assert np.abs(got["w"].cpu().numpy() - w).max() <= 1e-6
+    assert np.abs(got["feat"].cpu().numpy() - feat).max() <= 1e-5
