@@ -292,10 +292,12 @@ def cpu_model() -> str:
 
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--workload", default="view720p")
+    ap.add_argument("--gpus", type=int, default=1, help="GPUs (one: the only count measured)")
+    ap.add_argument("--steps", type=int, default=100, help="timed steps")
+    ap.add_argument("--warmup", type=int, default=10, help="untimed warm-up steps")
+    from paper_2312_11841_amd import synth as _synth
+    ap.add_argument("--workload", default="view720p", choices=sorted(_synth.CONFIGS),
+                    metavar="WORKLOAD", help="one of: " + ", ".join(sorted(_synth.CONFIGS)))
     ap.add_argument("--geometry", choices=("raster", "raycast"), default="raster",
                     help="mesh workloads: how each step computes the G-buffer")
     ap.add_argument("--cpu-budget", type=float, default=10.0,
@@ -312,7 +314,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU; --gpus {args.gpus} is not supported "
-              "(the path shards by view with no per-frame collective; see the design notes)",
+              "(the path would shard by view, with no per-frame collective)",
               file=sys.stderr)
         sys.exit(2)
 
