@@ -253,6 +253,42 @@ def test_frame_parity(R, cfg):
     assert np.all(np.isfinite(got))
 
 
+def _index_table(L, T, F):
+    """fp32 table whose entries depend on every bit of their index (an integer
+    hash of it, in [-0.5, 0.5)), cheap to build at 2^26 entries."""
+    h = np.arange(L * T * F, dtype=np.uint32)
+    h *= np.uint32(2654435761)                      # wraps modulo 2^32
+    h >>= np.uint32(8)
+    out = h.view(np.int32).astype(np.float32)       # 0 .. 2^24 - 1, exact
+    out *= np.float32(1.0 / (1 << 24))
+    out -= np.float32(0.5)
+    return out.reshape(L, T, F)
+
+
+@pytest.mark.parametrize("L,log2_T,F,n_min,n_max", [(32, 14, 2, 2, 2048), (2, 26, 2, 4096, 4096)],
+                         ids=["max_levels", "max_table"])
+def test_frame_at_the_largest_grids(R, L, log2_T, F, n_min, n_max):
+    """The largest level count (32, dense and hashed levels) and the largest
+    table (2^26 entries per level, two hashed levels; the table values depend
+    on every index bit), with the MLP removed."""
+    cfg = synth.TINY64_DENSE.replace(name=f"grid_L{L}_T{log2_T}", H=24, W=40, L=L, F=F,
+                                     log2_T=min(log2_T, 14), N_min=n_min, N_max=n_max,
+                                     widths=(L * F,), seed=17)
+    sc = synth.make_scene(cfg)
+    if log2_T > 14:
+        sc.cfg = cfg.replace(log2_T=log2_T, disp="none")
+        sc.table = _index_table(L, 1 << log2_T, F)
+    say("largest grid", sc.cfg.name, sc.table.shape, sc.table.dtype)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got = R.render(ds).cpu().numpy()
+    R.sync()
+    ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays), threads=oracle.max_threads())
+    err = np.abs(got - ref).max()
+    say(f"  max |gpu - oracle| = {err:.3e}")
+    assert err <= FRAME_TOL
+    del ds
+
+
 def test_frame_is_deterministic(R):
     sc, ds = scene_of(synth.VIEW720P_DENSE)
     a = R.render(ds).clone()
