@@ -38,7 +38,7 @@ extern "C" {
 enum mixrt_status {
     MIXRT_OK = 0,
     MIXRT_EINVAL = -1,        /* null pointer, bad size or inconsistent shape */
-    MIXRT_ENOMEM = -2,        /* device allocation failed */
+    MIXRT_ENOMEM = -2,        /* device (or, building a mesh, host) allocation failed */
     MIXRT_EDEVICE = -3,       /* HIP runtime error (launch or device failure) */
     MIXRT_EUNSUPPORTED = -4   /* valid request outside what this build serves */
 };
@@ -282,8 +282,9 @@ int mixrt_mesh_plan(const mixrt_mesh_desc *desc, mixrt_mesh_info *info, char *ms
  * per-triangle texture coordinates, and the triangle records once more in
  * triangle order (for mixrt_rasterize).  The mesh owns this device memory; the copies are
  * synchronous, so desc's arrays may be released on return.  *out is NULL on
- * failure (MIXRT_EINVAL for a bad descriptor, MIXRT_ENOMEM if the device
- * memory cannot be allocated). */
+ * failure (MIXRT_EINVAL for a bad descriptor, MIXRT_ENOMEM if the host
+ * arrays of the build or the device memory cannot be allocated,
+ * MIXRT_EUNSUPPORTED if the lists would reach 2^31 entries). */
 int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **out);
 
 /* Sizes of a created mesh (host only). */

@@ -355,7 +355,13 @@ int mixrt_mesh_plan(const mixrt_mesh_desc *desc, mixrt_mesh_info *info, char *ms
     if (msg && cap) msg[0] = 0;
     mixrt::MeshGridHost g;
     char buf[512] = "";
-    int rc = mixrt::build_mesh_grid(desc, false, g, buf, sizeof buf);
+    int rc;
+    try {
+        rc = mixrt::build_mesh_grid(desc, false, g, buf, sizeof buf);
+    } catch (const std::bad_alloc &) {
+        rc = MIXRT_ENOMEM;
+        snprintf(buf, sizeof buf, "host allocation for the mesh grid failed");
+    }
     if (rc) {
         if (msg && cap) snprintf(msg, cap, "%s", buf);
         return fail(nullptr, rc, "%s", buf);
@@ -382,7 +388,13 @@ int mixrt_mesh_create(mixrt_ctx *ctx, const mixrt_mesh_desc *desc, mixrt_mesh **
     *out = nullptr;
     mixrt::MeshGridHost g;
     char buf[512] = "";
-    int rc = mixrt::build_mesh_grid(desc, true, g, buf, sizeof buf);
+    int rc;
+    try {
+        // the grid's lists can reach 2^31 entries (48 bytes each) on the host
+        rc = mixrt::build_mesh_grid(desc, true, g, buf, sizeof buf);
+    } catch (const std::bad_alloc &) {
+        return fail(ctx, MIXRT_ENOMEM, "host allocation for the mesh grid failed");
+    }
     if (rc) return fail(ctx, rc, "%s", buf);
     if ((rc = bind_device(ctx))) return rc;
     const int64_t cells = (int64_t)g.n[0] * g.n[1] * g.n[2];
