@@ -57,50 +57,117 @@ __global__ __launch_bounds__(kBlock) void hash_encode_kernel(GridParams gp, cons
     }
 }
 
-template <int IN, int HID, int NHID>
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"   // M0 is clobbered on purpose
+// One 16-byte chunk per lane straight from global memory into LDS
+// (global_load_lds_dwordx4): lane l's chunk lands at lds + 16 l.  M0 is set
+// in the same statement; nothing else in this kernel uses it.
+__device__ __forceinline__ void lds_load16(const void *g, uint32_t lds)
+{
+    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(
+                     __builtin_amdgcn_readfirstlane(lds)),
+                 "v"(g)
+                 : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// A 16-byte vector store, issued as assembly like the loads above.
+__device__ __forceinline__ void store16(void *g, f4 v)
+{
+    asm volatile("global_store_dwordx4 %0, %1, off" ::"v"(g), "v"(v) : "memory");
+}
+
+// Wait until at most N vector-memory operations (loads and stores) of this
+// wave are outstanding; they complete in issue order.
+template <int N>
+__device__ __forceinline__ void wait_vm()
+{
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+
+// wait_vm<n> for a wave-uniform n in 0..N
+template <int N>
+__device__ __forceinline__ void wait_vm_upto(int n)
+{
+    if constexpr (N == 0) {
+        wait_vm<0>();
+    } else {
+        if (n >= N)
+            wait_vm<N>();
+        else
+            wait_vm_upto<N - 1>(n);
+    }
+}
+
+// Persistent: weights are loaded once per wave, then 64-row tiles.  A tile's
+// rows are one contiguous block of 64 * CH 16-byte chunks, copied to LDS in
+// CH coalesced loads, DEPTH tiles ahead of the one being computed.
+//
+// The loads and stores of the tile loop are issued as assembly, so that the
+// compiler, which sees no memory operation of its own there, places no wait
+// of its own: its form of the LDS loads waits for every outstanding vector
+// operation before any LDS read, and before inline assembly it drains its
+// pending stores; either would serialise the pipelining.  The waits are
+// counted instead.  Every tile issues exactly CH loads (the chunks of rows
+// past n are read from the last row, and their outputs never stored) and
+// every tile but the last overall, which is then also the last of its wave,
+// is full and issues exactly kStores stores.  After the loads of tile k come
+// the stores of the min(k, DEPTH) tiles before it and the loads of the tiles
+// after it that are already in flight, and that is the count to wait for.
+constexpr int kStores = 4;   // one per 16-row sub-tile, by lanes 0..15
+
+template <int IN, int HID, int NHID, int DEPTH>
 __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict__ weights,
                                                      const _Float16 *__restrict__ in, int64_t n,
                                                      float4 *__restrict__ out4)
 {
-    static_assert(IN % 8 == 0, "rows are staged in 16-byte chunks");
-    constexpr int LD = IN + 8;
-    constexpr int CH = IN / 8;   // 16-byte chunks per row, and per lane per tile
-    __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][kWave * LD];
+    static_assert(IN % 8 == 0, "rows are moved in 16-byte chunks");
+    static_assert(DEPTH >= 1 && DEPTH <= 2, "tiles in flight");
+    constexpr int CH = IN / 8;   // 16-byte chunks per row; a tile is CH 1-KiB loads
+    constexpr int NB = DEPTH + 1;
+    static_assert(DEPTH * (CH + kStores) <= 63, "vmcnt range");
+    // NB tile buffers per wave, rows of IN halves back to back
+    __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][NB][kWave * IN];
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = threadIdx.x / kWave;
-    _Float16 *rows = s_rows[wv];
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     MlpWeights<IN, HID, NHID> Wt;
     Wt.load(weights, lane);
-    // Persistent: weights are loaded once per wave, then 64-row tiles.  A
-    // tile's rows are one contiguous block of 64 * CH chunks; lane l reads
-    // chunks l, l + 64, ... (coalesced) and writes each into its row in LDS.
-    // (Fetching the next tile into registers during the current one costs
-    // a wave per SIMD of occupancy and was slower.)
     const int64_t n_tiles = (n + kWave - 1) / kWave;
     const int64_t total = (int64_t)gridDim.x * kWavesPerBlock;
+    const int64_t first = (int64_t)blockIdx.x * kWavesPerBlock + wv;
+    if (first >= n_tiles) return;
+    const int count = (int)((n_tiles - 1 - first) / total) + 1;   // tiles of this wave
+    const int64_t last_chunk = n * CH - 1;
+    const h8 *chunks = (const h8 *)in;
     const int c = lane & 15, g = lane >> 4;
-    for (int64_t tile = (int64_t)blockIdx.x * kWavesPerBlock + wv; tile < n_tiles; tile += total) {
-        const int64_t base = tile * kWave;
-        const h8 *src = (const h8 *)(in + base * IN);
-        h8 buf[CH];
+    auto issue = [&](int k) {
+        const int64_t base = (first + (int64_t)k * total) * kWave * CH;
+        const uint32_t lds = (uint32_t)(uintptr_t)s_rows[wv][k % NB];
 #pragma unroll
         for (int e = 0; e < CH; ++e) {
-            const int q = lane + kWave * e;
-            buf[e] = base + q / CH < n ? src[q] : h8{};   // rows past n are zeros
+            const int64_t q = base + lane + kWave * e;
+            lds_load16(chunks + (q < last_chunk ? q : last_chunk), lds + 1024u * (uint32_t)e);
         }
+    };
+    for (int k = 0; k < DEPTH && k < count; ++k) issue(k);
+    for (int k = 0; k < count; ++k) {
+        if (k + DEPTH < count) issue(k + DEPTH);
+        const int ahead = count - 1 - k < DEPTH ? count - 1 - k : DEPTH;
+        const int stored = k < DEPTH ? k : DEPTH;
+        wait_vm_upto<DEPTH *(CH + kStores)>(ahead * CH + stored * kStores);
+        const _Float16 *rows = s_rows[wv][k % NB];
+        const int64_t base = (first + (int64_t)k * total) * kWave;
 #pragma unroll
-        for (int e = 0; e < CH; ++e) {
-            const int q = lane + kWave * e;
-            *(h8 *)(rows + (q / CH) * LD + (q % CH) * 8) = buf[e];
-        }
-        wave_lds_sync();
         for (int nt = 0; nt < 4; ++nt) {
-            const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
+            const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * IN, IN, lane);
             const int64_t s = base + nt * 16 + c;
-            if (g == 0 && s < n) out4[s] = mlp_activate(o);
+            if (g == 0 && s < n) {
+                const float4 a = mlp_activate(o);
+                store16(out4 + s, f4{a.x, a.y, a.z, a.w});
+            }
         }
-        wave_lds_sync();
     }
+    wait_vm<0>();
 }
 
 // The MLP removed: inputs summed per component (input i feeds output i mod 4).
@@ -181,6 +248,9 @@ hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const floa
     return hipGetLastError();
 }
 
+// Tiles each wave has in flight beyond the one it computes
+constexpr int kMlpDepth = 2;
+
 hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const _Float16 *x,
                       int64_t n, float4 *out4, int cus, hipStream_t stream)
 {
@@ -193,7 +263,7 @@ hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const 
     const int64_t want = ((n + kWave - 1) / kWave + kWavesPerBlock - 1) / kWavesPerBlock;
 #define X(d, e, f)                                                                           \
     if (in == d && hid == e && nhid == f) {                                                  \
-        auto fn = mlp_kernel<d, e, f>;                                                       \
+        auto fn = mlp_kernel<d, e, f, kMlpDepth>;                                            \
         static std::atomic<int> per_cu{0};                                                   \
         const int64_t resident = (int64_t)blocks_per_cu((const void *)fn, per_cu) * cus;     \
         const int64_t blocks = want < resident ? want : resident;                            \
