@@ -155,6 +155,25 @@ def _ptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
 
 
+def _require(t, name: str, dtypes, numel: int, device: int):
+    """Check a tensor whose device pointer is handed to the library: on the
+    renderer's GPU, contiguous, of an accepted dtype and at least numel
+    elements.  The library only sees a pointer, so a wrong buffer would be
+    read or written out of bounds on the GPU."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if t.device.type != "cuda" or t.device.index != device:
+        raise ValueError(f"{name}: on {t.device}, expected cuda:{device}")
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected one of {dtypes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: not contiguous")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, needs {numel}")
+    return t
+
+
 # --- descriptors from scene data -------------------------------------------------
 
 _DT = {"float32": MIXRT_F32, "float16": MIXRT_F16, "uint8": MIXRT_U8}
@@ -341,6 +360,7 @@ class Renderer:
         import torch
         if out is None:
             out = torch.empty((ds.rays, 4), dtype=torch.float32, device=ds.g0.device)
+        _require(out, "out", (torch.float32,), 4 * ds.rays, self.device)
         self._check(lib().mixrt_render(self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
                                        C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp),
                                        _ptr(out)))
@@ -365,6 +385,9 @@ class Renderer:
             out = (torch.empty((views, H, W, 4), dtype=torch.float32, device=dev),
                    torch.empty((views, H, W, 4), dtype=torch.float32, device=dev) if g1 else None)
         g0t, g1t = out
+        _require(g0t, "out[0]", (torch.float32,), views * H * W * 4, self.device)
+        if g1t is not None:
+            _require(g1t, "out[1]", (torch.float32,), views * H * W * 4, self.device)
         self._check(fn(self._h, mesh._h, views, W, H, cam_arr, _ptr(g0t), _ptr(g1t)))
         return g0t, g1t
 
@@ -383,6 +406,7 @@ class Renderer:
         import torch
         n = x.shape[0]
         L, F = grid.L, grid.F
+        _require(x, "x", (torch.float32,), 3 * n, self.device)
         dev = x.device
         out = {
             "corner": torch.empty((n, L, 3), dtype=torch.int32, device=dev) if "corner" in want else None,
@@ -398,6 +422,7 @@ class Renderer:
     def mlp(self, mlp: Mlp, x_f16):
         import torch
         n = x_f16.shape[0]
+        _require(x_f16, "x_f16", (torch.float16, torch.int16), n * mlp.width[0], self.device)
         out = torch.empty((n, 4), dtype=torch.float32, device=x_f16.device)
         self._check(lib().mixrt_debug_mlp(self._h, C.byref(mlp), _ptr(x_f16), n, _ptr(out)))
         return out
@@ -405,6 +430,7 @@ class Renderer:
     def composite(self, srgb, smp: Sampling, bg):
         import torch
         rays = srgb.shape[0]
+        _require(srgb, "srgb", (torch.float32,), rays * smp.K * 4, self.device)
         out = torch.empty((rays, 4), dtype=torch.float32, device=srgb.device)
         bgc = (C.c_float * 3)(*[float(b) for b in bg])
         self._check(lib().mixrt_debug_composite(self._h, _ptr(srgb), rays, C.byref(smp), bgc,

@@ -313,3 +313,12 @@ def test_mesh_plan_rejects_null_and_tiny():
     d = mixrt.MeshDesc(2, 1, 0, 0, None, (C.c_int32 * 3)(0, 0, 0), 0.0)
     assert mixrt.lib().mixrt_mesh_plan(C.byref(d), None, None, 0) == mixrt.MIXRT_EINVAL
     assert b"n_vertices" in mixrt.lib().mixrt_thread_error()
+
+
+def test_binding_checks_buffers_it_passes_as_pointers():
+    """The binding refuses a buffer the library would reach out of bounds."""
+    torch = pytest.importorskip("torch")
+    with pytest.raises(ValueError, match="on cpu"):
+        mixrt._require(torch.zeros(8), "out", (torch.float32,), 8, 0)
+    with pytest.raises(TypeError):
+        mixrt._require(np.zeros(8, np.float32), "out", (torch.float32,), 8, 0)

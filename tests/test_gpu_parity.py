@@ -390,3 +390,26 @@ def test_render_rejects_bad_calls(R):
         rc = mixrt.lib().mixrt_render(R._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
                                       C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp), None)
         R._check(rc)
+
+
+def test_binding_rejects_wrong_buffers_before_any_launch(R):
+    """Buffers the library would only see as pointers are checked in the
+    binding: too small, wrong dtype, not contiguous or on the CPU."""
+    sc, ds = scene_of(synth.TINY64)
+    small = torch.empty((ds.rays - 1, 4), dtype=torch.float32, device="cuda:0")
+    with pytest.raises(ValueError, match="elements"):
+        R.render(ds, small)
+    with pytest.raises(ValueError, match="dtype"):
+        R.render(ds, torch.empty((ds.rays, 4), dtype=torch.float16, device="cuda:0"))
+    with pytest.raises(ValueError, match="on cpu"):
+        R.render(ds, torch.empty((ds.rays, 4), dtype=torch.float32))
+    strided = torch.empty((ds.rays, 8), dtype=torch.float32, device="cuda:0")[:, ::2]
+    with pytest.raises(ValueError, match="contiguous"):
+        R.render(ds, strided)
+    x = torch.zeros((100, 2), dtype=torch.float32, device="cuda:0")
+    with pytest.raises(ValueError, match="elements"):
+        R.hash_encode(ds.grid, x)
+    with pytest.raises(ValueError, match="dtype"):
+        R.mlp(ds.mlp, torch.zeros((64, ds.mlp.width[0]), dtype=torch.float32, device="cuda:0"))
+    with pytest.raises(ValueError, match="elements"):
+        R.composite(torch.zeros((10, ds.smp.K, 3), device="cuda:0"), ds.smp, (0, 0, 0))
