@@ -82,7 +82,10 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     __shared__ int s_hit[kWavesPerBlock][kWave];
 
     const int lane = threadIdx.x & (kWave - 1);
-    const int wv = threadIdx.x / kWave;
+    // wave-uniform, so that the tile, its view and its camera live in scalar
+    // registers (a lane-dependent view index makes the compiler keep every
+    // camera in registers and select among them)
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     _Float16 *rows = s_rows[wv];
 
     // NHID = 0: the MLP removed; the level features are summed per component
@@ -100,7 +103,6 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     const int k = lane - r_loc * K;
     const int L = gp.L;
     const int n_dense = gp.n_dense;
-    const uint32_t hw = (uint32_t)rp.H * (uint32_t)rp.W;
 
     for (int tile = gw; tile < ts.n_tiles; tile += total) {
         // the tile's pixel block, and ray r of it at (r % RW, r / RW)
@@ -108,6 +110,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         const int ty = rem / ts.tiles_x, tx = rem - ty * ts.tiles_x;
         const int i0 = tx * ts.RW, j0 = ty * ts.RH;
         const int ray_base = (view * rp.H + j0) * rp.W + i0;
+        const CamK &cam = rp.cams[view];
         auto ray_of = [&](int r, bool &in) {
             const int dy = r / ts.RW, dx = r - dy * ts.RW;
             in = r < R && i0 + dx < rp.W && j0 + dy < rp.H;
@@ -120,7 +123,8 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         bool hit = false;
         Ray ry = {};
         if (valid) {
-            ry = pixel_ray(rp, ray);
+            const int dy = r_loc / ts.RW, dx = r_loc - dy * ts.RW;
+            ry = camera_ray(cam, rp.W, rp.H, (uint32_t)(i0 + dx), (uint32_t)(j0 + dy));
             hit = sample_position<TK>(rp, ry, rp.g0[ray], k, x0, x1, x2);
         }
         // --- hash encoding, features to LDS as fp16: dense levels first (pair
@@ -180,7 +184,6 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
                 Composite cp;
                 for (int kk = 0; kk < K; ++kk)
                     if (!cp.add(s_out[wv][lane * K + kk], rp.delta, rp.t_term)) break;
-                const CamK &cam = rp.cams[(uint32_t)ray_c / hw];
                 out[ray_c] = cp.finish(cam.bg[0], cam.bg[1], cam.bg[2]);
             }
         }
