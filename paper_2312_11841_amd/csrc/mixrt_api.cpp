@@ -304,6 +304,8 @@ void fill_grid_params(mixrt::GridParams &gp, const mixrt_hash_grid *g)
     const uint64_t T = 1ull << g->log2_T;
     for (int l = 0; l < g->L; ++l) {
         gp.N[l] = (uint32_t)N[l];
+        gp.Nf[l] = (float)N[l];
+        gp.Ntop[l] = (float)(N[l] - 1);
         const uint64_t side = (uint64_t)N[l] + 1;
         if (side * side * side <= T) {
             gp.dense_mask |= 1u << l;

@@ -58,6 +58,8 @@ struct GridParams {
     uint32_t dense_mask;    // bit l: level l indexes its vertices densely
     int32_t n_dense;        // dense levels form the prefix 0..n_dense-1
     uint32_t N[kMaxLevels];
+    float Nf[kMaxLevels];   // N as float, and N - 1 (exact: N <= 2^20), so
+    float Ntop[kMaxLevels]; // that no lane converts them
 };
 
 // --------------------------------------------------------------------------
@@ -502,38 +504,56 @@ struct TablePair<4, false> {
 constexpr uint32_t kPrimeY = 2654435761u;
 constexpr uint32_t kPrimeZ = 805459861u;
 
-// Voxel, fractional position and the 8 corner indices of one query at one
-// level.  Corner b has offset (b & 1, b >> 1 & 1, b >> 2 & 1).
+// Voxel, fractional position and the 8 corner entries of one query at one
+// level, as byte offsets into the level's table for entries of EB bytes.
+// Corner b has offset (b & 1, b >> 1 & 1, b >> 2 & 1).
 struct LevelSetup {
-    int32_t c[3];
+    float cf[3];       // voxel corner c0 (integral values)
     float fr[3];
-    uint32_t idx[8];
+    uint32_t off[8];   // entry index times EB
 };
 
-__device__ __forceinline__ void level_setup(uint32_t N, bool dense, uint32_t T_mask, float x0,
+// IN_UNIT: the query is known to lie in [0, 1]^3 (the render path clamps it
+// there), so only the upper clamp of the voxel is needed.  Otherwise a
+// coordinate below 0 or NaN takes voxel 0, as the oracle does.
+//
+// The byte offsets are computed directly: shifting left distributes over
+// XOR and AND, so (h & (T - 1)) EB for a hash h = x ^ y pY ^ z pZ (mod 2^32)
+// equals (x EB ^ y (pY EB) ^ z (pZ EB)) & ((T - 1) EB) with the products
+// taken mod 2^32 (T EB <= 2^30), and a dense index scales term by term.
+template <uint32_t EB, bool IN_UNIT>
+__device__ __forceinline__ void level_setup(const GridParams &gp, int l, bool dense, float x0,
                                             float x1, float x2, LevelSetup &s)
 {
-    const float Nf = (float)N;
+    static_assert(EB == 4 || EB == 8 || EB == 16, "entry size");
+    const uint32_t N = gp.N[l], T_mask = gp.T_mask;
+    const float Nf = gp.Nf[l], top = gp.Ntop[l];
     const float p[3] = {__fmul_rn(x0, Nf), __fmul_rn(x1, Nf), __fmul_rn(x2, Nf)};
-    const int32_t top = (int32_t)N - 1;
+    uint32_t c[3];
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
-        s.c[a] = min(max((int32_t)floorf(p[a]), 0), top);
-        s.fr[a] = p[a] - (float)s.c[a];
+        // floor(min(p, N - 1)) = min(floor(p), N - 1) since N - 1 is integral
+        s.cf[a] = floorf(IN_UNIT ? fminf(p[a], top) : fminf(fmaxf(p[a], 0.0f), top));
+        c[a] = (uint32_t)s.cf[a];
+        s.fr[a] = p[a] - s.cf[a];
     }
     if (dense) {
         const uint32_t s1 = N + 1u, s2 = s1 * s1;
-        const uint32_t base = (uint32_t)s.c[0] + (uint32_t)s.c[1] * s1 + (uint32_t)s.c[2] * s2;
+        const uint32_t base = c[0] * EB + c[1] * (s1 * EB) + c[2] * (s2 * EB);
 #pragma unroll
         for (int b = 0; b < 8; ++b)
-            s.idx[b] = base + (uint32_t)(b & 1) + ((b & 2) ? s1 : 0u) + ((b & 4) ? s2 : 0u);
+            s.off[b] = base + ((b & 1) ? EB : 0u) + ((b & 2) ? s1 * EB : 0u) +
+                       ((b & 4) ? s2 * EB : 0u);
     } else {
-        const uint32_t hy0 = (uint32_t)s.c[1] * kPrimeY, hy1 = hy0 + kPrimeY;
-        const uint32_t hz0 = (uint32_t)s.c[2] * kPrimeZ, hz1 = hz0 + kPrimeZ;
+        constexpr uint32_t pY = kPrimeY * EB, pZ = kPrimeZ * EB;   // mod 2^32
+        const uint32_t mask = T_mask * EB;
+        const uint32_t hx0 = c[0] * EB, hx1 = hx0 + EB;
+        const uint32_t hy0 = c[1] * pY, hy1 = hy0 + pY;
+        const uint32_t hz0 = c[2] * pZ, hz1 = hz0 + pZ;
 #pragma unroll
         for (int b = 0; b < 8; ++b)
-            s.idx[b] = (((uint32_t)s.c[0] + (uint32_t)(b & 1)) ^ ((b & 2) ? hy1 : hy0) ^
-                        ((b & 4) ? hz1 : hz0)) & T_mask;
+            s.off[b] = (((b & 1) ? hx1 : hx0) ^ ((b & 2) ? hy1 : hy0) ^ ((b & 4) ? hz1 : hz0)) &
+                       mask;
     }
 }
 
@@ -552,15 +572,14 @@ __device__ __forceinline__ void level_fetch(const void *table_l, const LevelSetu
                                             float (*v)[F])
 {
     const char *t = (const char *)table_l;
-    constexpr uint32_t eb = TableEntry<F, F16>::kBytes;
     if (DENSE) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-            TablePair<F, F16>::load(t, s.idx[2 * q] * eb, v[2 * q], v[2 * q + 1]);
+            TablePair<F, F16>::load(t, s.off[2 * q], v[2 * q], v[2 * q + 1]);
     } else {
 #pragma unroll
         for (int b = 0; b < 8; ++b)
-            TableEntry<F, F16>::load(t, s.idx[b] * eb, v[b]);
+            TableEntry<F, F16>::load(t, s.off[b], v[b]);
     }
 }
 
@@ -597,7 +616,7 @@ __device__ __forceinline__ void hash_group(const GridParams &gp, int l0, float x
     float v[G][8][F];
 #pragma unroll
     for (int g = 0; g < G; ++g)
-        level_setup(gp.N[l0 + g], DENSE, gp.T_mask, x0, x1, x2, s[g]);
+        level_setup<TableEntry<F, F16>::kBytes, true>(gp, l0 + g, DENSE, x0, x1, x2, s[g]);
 #pragma unroll
     for (int g = 0; g < G; ++g)
         level_fetch<F, F16, DENSE>(level_base(gp, l0 + g, F, F16), s[g], v[g]);

@@ -34,11 +34,14 @@ __global__ __launch_bounds__(kBlock) void hash_encode_kernel(GridParams gp, cons
     if (s >= n) return;
     const float x0 = x[3 * s], x1 = x[3 * s + 1], x2 = x[3 * s + 2];
     for (int l = 0; l < gp.L; ++l) {
-        // the render kernel's arithmetic, one level at a time
+        // the render kernel's arithmetic, one level at a time (the render
+        // kernel's queries lie in [0, 1]^3; here a coordinate outside it is
+        // clamped to the grid)
         LevelSetup st;
         float v[8][F], f[F];
         const bool dense = l < gp.n_dense;
-        level_setup(gp.N[l], dense, gp.T_mask, x0, x1, x2, st);
+        constexpr uint32_t eb = TableEntry<F, TF16>::kBytes;
+        level_setup<eb, false>(gp, l, dense, x0, x1, x2, st);
         const void *base = level_base(gp, l, F, TF16);
         if (dense)
             level_fetch<F, TF16, true>(base, st, v);
@@ -47,9 +50,9 @@ __global__ __launch_bounds__(kBlock) void hash_encode_kernel(GridParams gp, cons
         level_accumulate<F>(st, v, f);
         const int64_t sl = s * gp.L + l;
         if (out_corner)
-            for (int a = 0; a < 3; ++a) out_corner[sl * 3 + a] = st.c[a];
+            for (int a = 0; a < 3; ++a) out_corner[sl * 3 + a] = (int32_t)st.cf[a];
         if (out_idx)
-            for (int b = 0; b < 8; ++b) out_idx[sl * 8 + b] = st.idx[b];
+            for (int b = 0; b < 8; ++b) out_idx[sl * 8 + b] = st.off[b] / eb;
         if (out_w)
             for (int b = 0; b < 8; ++b) out_w[sl * 8 + b] = corner_weight(st, b);
         if (out_feat)
