@@ -24,6 +24,7 @@ struct mixrt_ctx {
     hipStream_t stream = nullptr;
     uint32_t flags = 0;
     int cus = 0;
+    int64_t l2_bytes = 0;
     std::string err;
 };
 
@@ -602,6 +603,7 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     ctx->stream = (hipStream_t)ci->hip_stream;
     ctx->flags = ci->flags;
     ctx->cus = prop.multiProcessorCount;
+    ctx->l2_bytes = prop.l2CacheSize;
     *out = ctx;
     return MIXRT_OK;
 }
@@ -650,6 +652,7 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
     L.hid = hid;
     L.nhid = nhid;
     L.cus = ctx->cus;
+    L.l2_bytes = ctx->l2_bytes;
     return finish_launch(ctx, mixrt::launch_render(L, ctx->stream), "render");
 }
 

@@ -56,6 +56,7 @@ struct RenderLaunch {
     bool tf16;
     int F, in, hid, nhid;
     int cus;
+    int64_t l2_bytes;   // L2 of one XCD
 };
 
 bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid);

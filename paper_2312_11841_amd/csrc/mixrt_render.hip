@@ -224,6 +224,25 @@ bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nh
     return false;
 }
 
+// Persistent blocks per CU for a frame, given the most that fit (`resident`).
+// More waves hide more latency when the gathers of a wave hit the same cache
+// lines: several samples per ray, spaced finer than the cells of at least
+// half the levels, on levels whose table fits one XCD's L2.  When the gathers
+// scatter instead (one or two samples per ray, widely spaced samples, or
+// levels larger than the L2), 2 blocks per CU keep more of each wave's lines
+// in the caches and run faster than the full occupancy.  The count changes
+// only which wave renders which tile, never a result.
+static int render_blocks_per_cu(const RenderLaunch &L, int resident)
+{
+    const float spacing = 0.25f * L.rp.delta;   // in grid units inside the unit ball
+    int shared = 0;   // levels whose cells are at least one sample spacing wide
+    for (int l = 0; l < L.gp.L; ++l)
+        if ((float)L.gp.N[l] * spacing <= 1.0f) ++shared;
+    const int64_t level_bytes = ((int64_t)L.gp.T_mask + 1) * L.F * (L.tf16 ? 2 : 4);
+    const bool coherent = L.rp.K >= 4 && 2 * shared >= L.gp.L && level_bytes <= L.l2_bytes;
+    return coherent || resident < 2 ? resident : 2;
+}
+
 hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
 {
     const int R = kWave / L.rp.K;
@@ -235,7 +254,8 @@ hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
         auto fn = render_kernel<a, b, c, d, e, f>;                                             \
         static std::atomic<int> per_cu{0};                                                     \
         /* blocks resident on the whole device */                                              \
-        int64_t blocks = (int64_t)blocks_per_cu((const void *)fn, per_cu) * L.cus;             \
+        int64_t blocks =                                                                       \
+            (int64_t)render_blocks_per_cu(L, blocks_per_cu((const void *)fn, per_cu)) * L.cus; \
         if (want < blocks) blocks = want;                                                      \
         if (blocks > 8) blocks -= blocks % 8;                                                  \
         if (blocks < 1) blocks = 1;                                                            \
