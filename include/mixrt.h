@@ -62,8 +62,16 @@ enum mixrt_disp_mode {
 
 /* Context creation flags. */
 enum mixrt_flags {
-    MIXRT_FLAG_SYNC_CHECK = 1u   /* synchronise after each call and report
+    MIXRT_FLAG_SYNC_CHECK = 1u,  /* synchronise after each call and report
                                     device errors as MIXRT_EDEVICE */
+    /* Persistent blocks of the render kernel per CU.  By default a frame runs
+     * every block that fits when a wave's gathers share cache lines (at least
+     * 4 samples per ray, spaced finer than the cells of half the levels, on
+     * levels whose table fits one XCD's L2) and 2 blocks per CU otherwise.
+     * These force one choice (setting both is MIXRT_EINVAL); the choice
+     * changes speed only, never a result. */
+    MIXRT_FLAG_BLOCKS_FULL = 2u,
+    MIXRT_FLAG_BLOCKS_TWO = 4u
 };
 
 #define MIXRT_MAX_VIEWS 16

@@ -584,6 +584,11 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     if (!out) return fail(nullptr, MIXRT_EINVAL, "out is NULL");
     *out = nullptr;
     if (!ci) return fail(nullptr, MIXRT_EINVAL, "create_info is NULL");
+    constexpr uint32_t known = MIXRT_FLAG_SYNC_CHECK | MIXRT_FLAG_BLOCKS_FULL | MIXRT_FLAG_BLOCKS_TWO;
+    if (ci->flags & ~known)
+        return fail(nullptr, MIXRT_EINVAL, "unknown flags 0x%x", ci->flags & ~known);
+    if ((ci->flags & MIXRT_FLAG_BLOCKS_FULL) && (ci->flags & MIXRT_FLAG_BLOCKS_TWO))
+        return fail(nullptr, MIXRT_EINVAL, "MIXRT_FLAG_BLOCKS_FULL and MIXRT_FLAG_BLOCKS_TWO together");
     int n = 0;
     hipError_t e = hipGetDeviceCount(&n);
     if (e != hipSuccess || n == 0)
@@ -653,6 +658,7 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
     L.nhid = nhid;
     L.cus = ctx->cus;
     L.l2_bytes = ctx->l2_bytes;
+    L.blocks_mode = (ctx->flags & MIXRT_FLAG_BLOCKS_FULL) ? 1 : (ctx->flags & MIXRT_FLAG_BLOCKS_TWO) ? 2 : 0;
     return finish_launch(ctx, mixrt::launch_render(L, ctx->stream), "render");
 }
 

@@ -57,6 +57,7 @@ struct RenderLaunch {
     int F, in, hid, nhid;
     int cus;
     int64_t l2_bytes;   // L2 of one XCD
+    int blocks_mode;    // 0: by the gathers' line sharing, 1: all that fit, 2: two per CU
 };
 
 bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid);

@@ -234,6 +234,8 @@ bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nh
 // only which wave renders which tile, never a result.
 static int render_blocks_per_cu(const RenderLaunch &L, int resident)
 {
+    if (L.blocks_mode == 1) return resident;
+    if (L.blocks_mode == 2) return resident < 2 ? resident : 2;
     const float spacing = 0.25f * L.rp.delta;   // in grid units inside the unit ball
     int shared = 0;   // levels whose cells are at least one sample spacing wide
     for (int l = 0; l < L.gp.L; ++l)

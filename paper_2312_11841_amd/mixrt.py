@@ -25,6 +25,8 @@ MIXRT_F32, MIXRT_F16, MIXRT_U8 = 0, 1, 2
 MIXRT_DISP_ALONG_RAY, MIXRT_DISP_SH_VEC3, MIXRT_DISP_NONE = 0, 1, 2
 _DISP = {"ray": MIXRT_DISP_ALONG_RAY, "vec3": MIXRT_DISP_SH_VEC3, "none": MIXRT_DISP_NONE}
 MIXRT_FLAG_SYNC_CHECK = 1
+MIXRT_FLAG_BLOCKS_FULL, MIXRT_FLAG_BLOCKS_TWO = 2, 4
+_BLOCKS = {None: 0, "full": MIXRT_FLAG_BLOCKS_FULL, "two": MIXRT_FLAG_BLOCKS_TWO}
 MAX_VIEWS, MAX_LEVELS, MAX_LAYERS = 16, 32, 8
 
 # Every symbol include/mixrt.h declares.
@@ -323,14 +325,16 @@ class DeviceMesh:
 class Renderer:
     """One mixrt context bound to a device and a HIP stream."""
 
-    def __init__(self, device: int = 0, stream=None, sync_check: bool = False):
+    def __init__(self, device: int = 0, stream=None, sync_check: bool = False, blocks=None):
+        """blocks: None (the library's choice), "full" or "two": the render
+        kernel's persistent blocks per CU (speed only, never a result)."""
         import torch
         self.device = device
         if stream is None:
             stream = torch.cuda.current_stream(device)
         self.stream = stream
         ci = CreateInfo(device, C.c_void_p(int(stream.cuda_stream)),
-                        MIXRT_FLAG_SYNC_CHECK if sync_check else 0)
+                        (MIXRT_FLAG_SYNC_CHECK if sync_check else 0) | _BLOCKS[blocks])
         h = C.c_void_p()
         rc = lib().mixrt_create(C.byref(h), C.byref(ci))
         if rc != MIXRT_OK:

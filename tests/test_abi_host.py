@@ -322,3 +322,21 @@ def test_binding_checks_buffers_it_passes_as_pointers():
         mixrt._require(torch.zeros(8), "out", (torch.float32,), 8, 0)
     with pytest.raises(TypeError):
         mixrt._require(np.zeros(8, np.float32), "out", (torch.float32,), 8, 0)
+
+
+@pytest.mark.parametrize("flags", [8, 1 << 31, mixrt.MIXRT_FLAG_BLOCKS_FULL | mixrt.MIXRT_FLAG_BLOCKS_TWO])
+def test_create_rejects_bad_flags_before_touching_a_device(flags):
+    """Unknown flag bits, or both block-count flags, are MIXRT_EINVAL (checked
+    on the host, so this runs without a GPU)."""
+    h = C.c_void_p()
+    ci = mixrt.CreateInfo(0, None, flags)
+    assert mixrt.lib().mixrt_create(C.byref(h), C.byref(ci)) == mixrt.MIXRT_EINVAL
+    assert not h.value
+    assert "flag" in mixrt.lib().mixrt_thread_error().decode().lower()
+
+
+def test_flag_values_match_header():
+    text = open(os.path.join(ROOT, "include", "mixrt.h")).read()
+    for name in ("MIXRT_FLAG_SYNC_CHECK", "MIXRT_FLAG_BLOCKS_FULL", "MIXRT_FLAG_BLOCKS_TWO"):
+        m = re.search(rf"{name}\s*=\s*(\d+)u", text)
+        assert m and int(m.group(1)) == getattr(mixrt, name), name

@@ -413,3 +413,19 @@ def test_binding_rejects_wrong_buffers_before_any_launch(R):
         R.mlp(ds.mlp, torch.zeros((64, ds.mlp.width[0]), dtype=torch.float32, device="cuda:0"))
     with pytest.raises(ValueError, match="elements"):
         R.composite(torch.zeros((10, ds.smp.K, 3), device="cuda:0"), ds.smp, (0, 0, 0))
+
+
+def test_frame_does_not_depend_on_blocks_per_cu():
+    """The persistent grid's size changes which wave renders a tile, never a
+    pixel: view720p (coherent, full occupancy by default) and view720p_dense
+    (scattered, 2 blocks per CU by default) rendered both ways, bit for bit."""
+    for cfg in (synth.VIEW720P, synth.VIEW720P_DENSE):
+        say("blocks per CU", cfg.name)
+        sc = synth.make_scene(cfg)
+        ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+        outs = []
+        for blocks in ("full", "two", None):
+            r = mixrt.Renderer(0, blocks=blocks)
+            outs.append(r.render(ds).cpu().numpy())
+            r.close()
+        assert np.array_equal(outs[0], outs[1]) and np.array_equal(outs[0], outs[2])
