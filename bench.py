@@ -448,6 +448,9 @@ def main():
             "algorithmic_bytes_per_launch": total_bytes,
             "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
                                            "ray": work["per_ray_bytes"]},
+            "note": "achieved counts every table entry a sample gathers; samples that share "
+                    "cache lines are served by the L1 and L2, so it can exceed the HBM peak "
+                    "on coherent frames; traffic is what reached HBM and the Infinity Cache",
         },
         "hash_encode_GBps": round(work["hash_bytes"] / rsec / 1e9, 1),
         "hash_lane_loads_per_s": round(cfg.samples * cfg.L * 8 / rsec),
