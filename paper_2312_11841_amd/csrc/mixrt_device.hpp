@@ -528,7 +528,14 @@ __device__ __forceinline__ void level_setup(const GridParams &gp, int l, bool de
     static_assert(EB == 4 || EB == 8 || EB == 16, "entry size");
     const uint32_t N = gp.N[l], T_mask = gp.T_mask;
     const float Nf = gp.Nf[l], top = gp.Ntop[l];
-    const float p[3] = {__fmul_rn(x0, Nf), __fmul_rn(x1, Nf), __fmul_rn(x2, Nf)};
+    // p = x N rounded once to fp32, as the oracle takes it.  The empty asm
+    // keeps the compiler from fusing the product into p - c0 (which would
+    // skip that rounding); with it, p - c0 is exact (c0 <= p < c0 + 1), so the
+    // fractions equal the oracle's.
+    float p[3] = {x0 * Nf, x1 * Nf, x2 * Nf};
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+        asm("" : "+v"(p[a]));
     uint32_t c[3];
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
