@@ -256,8 +256,11 @@ hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const floa
     return hipGetLastError();
 }
 
-// Tiles each wave has in flight beyond the one it computes
-constexpr int kMlpDepth = 2;
+// Tiles each wave has in flight beyond the one it computes.  One tile ahead
+// leaves room in LDS for 3 blocks per CU (2 at two ahead) and, with the
+// non-temporal loads and stores, runs about 2.5% faster (0.157 against 0.161
+// ms for 7.37M rows of 48).
+constexpr int kMlpDepth = 1;
 
 hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const _Float16 *x,
                       int64_t n, float4 *out4, int cus, hipStream_t stream)
