@@ -440,7 +440,10 @@ int orc_mlp(int64_t n, const double *in, int n_layers, const int32_t *widths,
 
 /* srgb [rays][K][4] = (sigma, r, g, b); bg [rays][3].  The transmittance of
  * sample k is exp(-sum_{j<k} sigma_j delta); the transmittance left after the
- * last sample weights the background.  out [rays][4] = (rgb, alpha). */
+ * last sample weights the background.  out [rays][4] = (rgb, alpha).
+ * A sample's optical depth sigma_k delta is 0 when delta = 0: an interval of
+ * zero length absorbs nothing, whatever the density (this also defines the
+ * product for a density that overflowed to infinity). */
 void orc_composite(int64_t rays, int K, const double *srgb, double delta, const double *bg,
                    double *out)
 {
@@ -450,10 +453,11 @@ void orc_composite(int64_t rays, int K, const double *srgb, double delta, const 
         double optical = 0.0;  /* sum_{j<k} sigma_j delta */
         for (int k = 0; k < K; ++k) {
             double T = exp(-optical);
-            double alpha = 1.0 - exp(-s[4 * k] * delta);
+            double tau = delta > 0.0 ? s[4 * k] * delta : 0.0;
+            double alpha = 1.0 - exp(-tau);
             for (int ch = 0; ch < 3; ++ch)
                 c[ch] += T * alpha * s[4 * k + 1 + ch];
-            optical += s[4 * k] * delta;
+            optical += tau;
         }
         double Tend = exp(-optical);
         for (int ch = 0; ch < 3; ++ch)

@@ -835,13 +835,17 @@ __device__ __forceinline__ float4 mlp_activate(f4 o)
 // Eq. 1 front to back: alpha_k = 1 - exp(-sigma_k delta), the running
 // transmittance excludes sample k, the remaining transmittance weights the
 // background, and a ray stops once its transmittance is below t_term.
+// A zero-length interval (delta = 0) has zero optical depth whatever sigma
+// is: sigma delta is taken through max(., 0), which turns the inf * 0 of an
+// overflowed density into 0 and leaves every other product unchanged
+// (sigma = exp(.) >= 0).
 // --------------------------------------------------------------------------
 struct Composite {
     float r = 0.0f, g = 0.0f, b = 0.0f, T = 1.0f;
 
     __device__ __forceinline__ bool add(float4 s, float delta, float t_term)
     {
-        const float alpha = 1.0f - fast_exp(-s.x * delta);
+        const float alpha = 1.0f - fast_exp(-fmaxf(s.x * delta, 0.0f));
         const float w = T * alpha;
         r += w * s.y;
         g += w * s.z;

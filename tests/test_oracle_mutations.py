@@ -19,8 +19,8 @@ MUTATIONS = {
                       "side * (uint64_t)v[2] + side * side * (uint64_t)v[1]"),
     "uv_swap": ("double a = u * R - 0.5, b = v * R - 0.5;", "double a = v * R - 0.5, b = u * R - 0.5;"),
     "no_half_texel": ("double a = u * R - 0.5, b = v * R - 0.5;", "double a = u * R, b = v * R;"),
-    "inclusive_T": ("double T = exp(-optical);\n            double alpha",
-                    "double T = exp(-optical - s[4 * k] * delta);\n            double alpha"),
+    "inclusive_T": ("double T = exp(-optical);\n            double tau",
+                    "double T = exp(-optical - s[4 * k] * delta);\n            double tau"),
     "weight_flip": ("wt *= bit ? fr[a] : 1.0 - fr[a];", "wt *= bit ? 1.0 - fr[a] : fr[a];"),
     "sh_sign": ("return sqrt(2.0) * k * p * sin((double)am * phi);",
                 "return -sqrt(2.0) * k * p * sin((double)am * phi);"),
@@ -60,8 +60,10 @@ MUTATIONS = {
     "no_near_miss": ("fmin(fmin(b1, b2), 1.0 - b1 - b2) > -eps_b * g)", "fmin(fmin(b1, b2), 1.0 - b1 - b2) > 0.0)"),
     'fr_from_c': ('fr[a] = (double)pos[a] - (double)c0[a];',
         'fr[a] = (double)pos[a] - (double)c;'),
-    'alpha_no_delta': ('double alpha = 1.0 - exp(-s[4 * k] * delta);',
-        'double alpha = 1.0 - exp(-s[4 * k]);'),
+    'alpha_no_delta': ('double tau = delta > 0.0 ? s[4 * k] * delta : 0.0;',
+        'double tau = delta > 0.0 ? s[4 * k] : 0.0;'),
+    'zero_delta_not_special': ('double tau = delta > 0.0 ? s[4 * k] * delta : 0.0;',
+        'double tau = s[4 * k] * delta;'),
     'sigma_relu': ('out4[4 * s + 0] = exp(o[0]);',
         'out4[4 * s + 0] = o[0] > 0.0 ? o[0] : 0.0;'),
     'sigmoid_sign': ('out4[4 * s + c] = 1.0 / (1.0 + exp(-o[c]));',
@@ -110,8 +112,8 @@ MUTATIONS = {
         'v = ldexp((double)(mant + 1024), expo - 24);'),
     'nomlp_mod': ('o[i % 4] += in[s * widths[0] + i];',
         'o[(i / (widths[0] / 4)) % 4] += in[s * widths[0] + i];'),
-    'composite_T_update': ('double T = exp(-optical);\n            double alpha',
-        'double T = exp(-0.5 * optical);\n            double alpha'),
+    'composite_T_update': ('double T = exp(-optical);\n            double tau',
+        'double T = exp(-0.5 * optical);\n            double tau'),
     'b2_margin_missing': ('*ambiguous = best_i >= 0 && fmin(fmin(bb1, bb2), 1.0 - bb1 - bb2) < eps_b * graze(bcos);',
         '*ambiguous = best_i >= 0 && fmin(bb1, 1.0 - bb1 - bb2) < eps_b * graze(bcos);'),
     'no_edge_flag': ('*ambiguous = best_i >= 0 && fmin(fmin(bb1, bb2), 1.0 - bb1 - bb2) < eps_b * graze(bcos);',

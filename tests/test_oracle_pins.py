@@ -458,6 +458,24 @@ def test_zero_density_returns_background():
     assert np.allclose(out[:, :3], bg, atol=1e-15) and np.all(out[:, 3] == 0)
 
 
+def test_zero_length_interval_absorbs_nothing():
+    """Eq. 1 with delta = 0: every alpha is 1 - exp(0) = 0, so the pixel is the
+    background with alpha 0, also for a density that overflowed to infinity
+    (whose product with 0 is otherwise undefined)."""
+    rng = np.random.default_rng(12)
+    s = rng.uniform(0, 1, (6, 5, 4))
+    s[..., 0] = rng.exponential(3.0, (6, 5))
+    s[0, :, 0] = np.inf
+    s[1, 2, 0] = np.inf
+    bg = rng.uniform(0, 1, (6, 3))
+    out = oracle.composite(s, 0.0, bg)
+    assert np.all(np.isfinite(out))
+    assert np.array_equal(out[:, :3], bg) and np.all(out[:, 3] == 0)
+    # and with delta > 0 an infinite density is one opaque sample
+    out = oracle.composite(s[:1], 0.1, bg[:1])
+    assert np.allclose(out[0], list(s[0, 0, 1:]) + [1.0], atol=0)
+
+
 def test_compositing_weights_telescope_and_two_sample_form():
     rng = np.random.default_rng(11)
     K = 8
