@@ -32,7 +32,8 @@ MAX_VIEWS, MAX_LEVELS, MAX_LAYERS = 16, 32, 8
 # Every symbol include/mixrt.h declares.
 EXPORTS = (
     "mixrt_create", "mixrt_destroy", "mixrt_sync", "mixrt_validate",
-    "mixrt_level_resolutions", "mixrt_render", "mixrt_debug_ray_setup",
+    "mixrt_level_resolutions", "mixrt_render", "mixrt_render_launch_shape",
+    "mixrt_debug_phase_cycles", "mixrt_debug_ray_setup",
     "mixrt_debug_hash_encode", "mixrt_debug_mlp", "mixrt_debug_composite",
     "mixrt_mesh_plan", "mixrt_mesh_create", "mixrt_mesh_get_info", "mixrt_mesh_destroy",
     "mixrt_raycast", "mixrt_rasterize",
@@ -54,7 +55,8 @@ class MixrtError(RuntimeError):
 # --- descriptor structs (field order and types as in mixrt.h) ------------------
 
 class CreateInfo(C.Structure):
-    _fields_ = [("device", C.c_int32), ("hip_stream", C.c_void_p), ("flags", C.c_uint32)]
+    _fields_ = [("device", C.c_int32), ("hip_stream", C.c_void_p), ("flags", C.c_uint32),
+                ("tile_stripe", C.c_int32)]
 
 
 class GBuffer(C.Structure):
@@ -98,18 +100,25 @@ class MeshInfo(C.Structure):
                 ("n_faces", C.c_int64), ("n_refs", C.c_int64), ("device_bytes", C.c_int64)]
 
 
-_lib = None
+_libs = {}
 
 
-def lib():
-    """Load libmixrt.so, or raise MixrtUnavailable (no fallback path exists)."""
-    global _lib
-    if _lib is None:
-        if not os.path.exists(LIB_PATH):
+def variant_path(variant=None) -> str:
+    """Path of libmixrt.so, or of one of its profiling builds ("timer",
+    "split_nodisp", "split_nohash", "split_nomlp"; see build.py)."""
+    return LIB_PATH if variant is None else os.path.join(_PKG, f"libmixrt_{variant}.so")
+
+
+def lib(variant=None):
+    """Load libmixrt.so (or a profiling build of it), or raise
+    MixrtUnavailable (no fallback path exists)."""
+    path = variant_path(variant)
+    if path not in _libs:
+        if not os.path.exists(path):
             raise MixrtUnavailable(
-                f"{LIB_PATH} is missing: build it with `python __graft_entry__.py` "
+                f"{path} is missing: build it with `python __graft_entry__.py` "
                 "or `python paper_2312_11841_amd/build.py`")
-        L = C.CDLL(LIB_PATH)
+        L = C.CDLL(path)
         P, I64 = C.c_void_p, C.c_int64
         sig = {
             "mixrt_create": (C.c_int, [C.POINTER(C.c_void_p), C.POINTER(CreateInfo)]),
@@ -123,6 +132,11 @@ def lib():
             "mixrt_render": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                        C.POINTER(DispTex), C.POINTER(HashGrid), C.POINTER(Mlp),
                                        C.POINTER(Sampling), P]),
+            "mixrt_render_launch_shape": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
+                                                    C.POINTER(DispTex), C.POINTER(HashGrid),
+                                                    C.POINTER(Mlp), C.POINTER(Sampling),
+                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
+            "mixrt_debug_phase_cycles": (C.c_int, [P, P, C.c_int]),
             "mixrt_debug_ray_setup": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                 C.POINTER(DispTex), C.POINTER(Sampling), P, P]),
             "mixrt_debug_hash_encode": (C.c_int, [P, C.POINTER(HashGrid), P, I64, P, P, P, P]),
@@ -145,8 +159,8 @@ def lib():
             f = getattr(L, name)
             f.restype = res
             f.argtypes = args
-        _lib = L
-    return _lib
+        _libs[path] = L
+    return _libs[path]
 
 
 def status_string(status: int) -> str:
@@ -157,22 +171,23 @@ def _ptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
 
 
-def _require(t, name: str, dtypes, numel: int, device: int):
-    """Check a tensor whose device pointer is handed to the library: on the
-    renderer's GPU, contiguous, of an accepted dtype and at least numel
-    elements.  The library only sees a pointer, so a wrong buffer would be
-    read or written out of bounds on the GPU."""
+def _require(t, name: str, dtypes, numel: int, device):
+    """Check a tensor whose device pointer is handed to the library: of an
+    accepted dtype, contiguous, at least numel elements, and on GPU `device`
+    (any GPU when device is None).  The library only sees a pointer, so a
+    wrong buffer would be read or written out of bounds on the GPU."""
     import torch
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
-    if t.device.type != "cuda" or t.device.index != device:
-        raise ValueError(f"{name}: on {t.device}, expected cuda:{device}")
     if t.dtype not in dtypes:
         raise ValueError(f"{name}: dtype {t.dtype}, expected one of {dtypes}")
     if not t.is_contiguous():
         raise ValueError(f"{name}: not contiguous")
     if t.numel() < numel:
         raise ValueError(f"{name}: {t.numel()} elements, needs {numel}")
+    if t.device.type != "cuda" or (device is not None and t.device.index != device):
+        want = "a GPU" if device is None else f"cuda:{device}"
+        raise ValueError(f"{name}: on {t.device}, expected {want}")
     return t
 
 
@@ -200,17 +215,37 @@ def make_sampling(K: int, delta: float, t_term: float) -> Sampling:
 
 
 def make_grid(table, N_min: int, N_max: int) -> HashGrid:
-    """Descriptor of a device table [L][T][F]; it holds a reference to the
-    tensor, so the memory it points at lives as long as the descriptor."""
-    L, T, F = table.shape
-    g = HashGrid(L, int(T).bit_length() - 1, F, int(N_min), int(N_max),
+    """Descriptor of a device table [L][T][F] (T a power of two, fp32 or
+    fp16, contiguous, on a GPU); it holds a reference to the tensor, so the
+    memory it points at lives as long as the descriptor."""
+    import torch
+    if not isinstance(table, torch.Tensor) or table.dim() != 3:
+        raise ValueError("table: expected a 3-d torch.Tensor [L][T][F]")
+    L, T, F = (int(n) for n in table.shape)
+    if T < 1 or T & (T - 1):
+        raise ValueError(f"table: T={T} entries per level is not a power of two")
+    _require(table, "table", (torch.float32, torch.float16), L * T * F, None)
+    g = HashGrid(L, T.bit_length() - 1, F, int(N_min), int(N_max),
                  _dtype_code(table), _ptr(table))
     g._keep = table
     return g
 
 
+def mlp_weight_count(widths) -> int:
+    """fp16 weights of an MLP with these layer widths (no biases)."""
+    return sum(int(a) * int(b) for a, b in zip(widths[:-1], widths[1:]))
+
+
 def make_mlp(weights, widths, view_sh_dim: int) -> Mlp:
-    """Descriptor of device weights; it holds a reference to the tensor."""
+    """Descriptor of device weights (fp16, or their bits as int16; every
+    layer's [in][out] matrix concatenated, contiguous, on a GPU); it holds a
+    reference to the tensor."""
+    import torch
+    if len(widths) < 1 or len(widths) > MAX_LAYERS + 1:
+        raise ValueError(f"widths: {len(widths)} entries, expected 1..{MAX_LAYERS + 1}")
+    n = mlp_weight_count(widths)
+    if n > 0 or weights is not None:
+        _require(weights, "weights", (torch.float16, torch.int16), n, None)
     m = Mlp()
     m._keep = weights
     m.n_layers = len(widths) - 1
@@ -265,6 +300,40 @@ class DeviceScene:
         return cls(g0, tex, scale, table, weights, make_cameras(scene.cams), gbuf, disp, grid,
                    mlp, smp, cfg.rays)
 
+    def check(self, device: int):
+        """Every buffer the descriptors point at, against the sizes the
+        descriptors declare, before a launch reads it (the library sees only
+        pointers)."""
+        import torch
+        g = self.gbuf
+        if g.g0 != _ptr(self.g0):
+            raise ValueError("gbuf.g0 does not point at this scene's g0 tensor")
+        _require(self.g0, "g0", (torch.float32,), 4 * g.views * g.H * g.W, device)
+        d = self.disp
+        if d.mode != MIXRT_DISP_NONE:
+            tdt = {MIXRT_F32: (torch.float32,), MIXRT_F16: (torch.float16,),
+                   MIXRT_U8: (torch.uint8,)}.get(d.dtype, ())
+            used = d.V if d.mode == MIXRT_DISP_ALONG_RAY else 3 * (d.sh_degree + 1) ** 2
+            chans = d.C if d.C > 0 else used
+            if d.data != _ptr(self.tex):
+                raise ValueError("disp.data does not point at this scene's texture")
+            _require(self.tex, "tex", tdt, d.R * d.R * chans, device)
+            if d.mode == MIXRT_DISP_SH_VEC3:
+                if self.scale is None or d.scale != _ptr(self.scale):
+                    raise ValueError("disp.scale does not point at this scene's scale map")
+                _require(self.scale, "scale", tdt, d.R * d.R, device)
+        gr = self.grid
+        if gr.data != _ptr(self.table):
+            raise ValueError("grid.data does not point at this scene's table")
+        _require(self.table, "table", (torch.float32, torch.float16),
+                 gr.L * (1 << gr.log2_T) * gr.F, device)
+        widths = [self.mlp.width[i] for i in range(self.mlp.n_layers + 1)]
+        if mlp_weight_count(widths):
+            if self.mlp.data != _ptr(self.weights):
+                raise ValueError("mlp.data does not point at this scene's weights")
+            _require(self.weights, "weights", (torch.float16, torch.int16),
+                     mlp_weight_count(widths), device)
+
 
 # --- meshes (the geometry stage) ---------------------------------------------------
 
@@ -301,16 +370,17 @@ class DeviceMesh:
     def __init__(self, renderer: "Renderer", mesh, grid_res=(0, 0, 0), cells_per_face=0.0):
         d, _keep = make_mesh_desc(mesh.positions, mesh.faces, getattr(mesh, "uv", None),
                                   grid_res, cells_per_face)
+        self._L = renderer._L
         h = C.c_void_p()
-        renderer._check(lib().mixrt_mesh_create(renderer._h, C.byref(d), C.byref(h)))
+        renderer._check(self._L.mixrt_mesh_create(renderer._h, C.byref(d), C.byref(h)))
         self._h = h
         info = MeshInfo()
-        lib().mixrt_mesh_get_info(h, C.byref(info))
+        self._L.mixrt_mesh_get_info(h, C.byref(info))
         self.info = _info_dict(info)
 
     def close(self):
         if getattr(self, "_h", None):
-            lib().mixrt_mesh_destroy(self._h)
+            self._L.mixrt_mesh_destroy(self._h)
             self._h = None
 
     def __del__(self):
@@ -325,29 +395,35 @@ class DeviceMesh:
 class Renderer:
     """One mixrt context bound to a device and a HIP stream."""
 
-    def __init__(self, device: int = 0, stream=None, sync_check: bool = False, blocks=None):
+    def __init__(self, device: int = 0, stream=None, sync_check: bool = False, blocks=None,
+                 tile_stripe: int = 0, variant=None):
         """blocks: None (the library's choice), "full" or "two": the render
-        kernel's persistent blocks per CU (speed only, never a result)."""
+        kernel's persistent blocks per CU; tile_stripe: 0 (the library's
+        choice), > 0 stripes of that many tiles, < 0 row-major (the order in
+        which waves take tiles).  Both change speed only, never a result.
+        variant: None (libmixrt.so) or a profiling build (see lib())."""
         import torch
         self.device = device
         if stream is None:
             stream = torch.cuda.current_stream(device)
         self.stream = stream
         ci = CreateInfo(device, C.c_void_p(int(stream.cuda_stream)),
-                        (MIXRT_FLAG_SYNC_CHECK if sync_check else 0) | _BLOCKS[blocks])
+                        (MIXRT_FLAG_SYNC_CHECK if sync_check else 0) | _BLOCKS[blocks],
+                        int(tile_stripe))
+        self._L = lib(variant)
         h = C.c_void_p()
-        rc = lib().mixrt_create(C.byref(h), C.byref(ci))
+        rc = self._L.mixrt_create(C.byref(h), C.byref(ci))
         if rc != MIXRT_OK:
-            raise MixrtError(rc, lib().mixrt_thread_error().decode())
+            raise MixrtError(rc, self._L.mixrt_thread_error().decode())
         self._h = h
 
     def _check(self, rc: int):
         if rc != MIXRT_OK:
-            raise MixrtError(rc, lib().mixrt_last_error(self._h).decode())
+            raise MixrtError(rc, self._L.mixrt_last_error(self._h).decode())
 
     def close(self):
         if getattr(self, "_h", None):
-            lib().mixrt_destroy(self._h)
+            self._L.mixrt_destroy(self._h)
             self._h = None
 
     def __del__(self):
@@ -357,28 +433,47 @@ class Renderer:
             pass
 
     def sync(self):
-        self._check(lib().mixrt_sync(self._h))
+        self._check(self._L.mixrt_sync(self._h))
 
     # -- the hot path
     def render(self, ds: DeviceScene, out=None):
         import torch
         if out is None:
-            out = torch.empty((ds.rays, 4), dtype=torch.float32, device=ds.g0.device)
+            out = torch.empty((ds.rays, 4), dtype=torch.float32,
+                              device=torch.device("cuda", self.device))
         _require(out, "out", (torch.float32,), 4 * ds.rays, self.device)
-        self._check(lib().mixrt_render(self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
+        ds.check(self.device)
+        self._check(self._L.mixrt_render(self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
                                        C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp),
                                        _ptr(out)))
         return out
+
+    def phase_cycles(self, reset: bool = False):
+        """The phase-timer build's counters (see mixrt_debug_phase_cycles):
+        {"setup", "hash", "mlp", "composite": shader clocks summed over
+        waves, "tiles", "waves"}."""
+        out = (C.c_uint64 * 8)()
+        self._check(self._L.mixrt_debug_phase_cycles(self._h, out, int(reset)))
+        names = ("setup", "hash", "mlp", "composite", "tiles", "waves")
+        return {n: int(out[i]) for i, n in enumerate(names)}
+
+    def launch_shape(self, ds: DeviceScene):
+        """(blocks, tile stripe) that render(ds) launches."""
+        b, st = C.c_int32(), C.c_int32()
+        self._check(self._L.mixrt_render_launch_shape(
+            self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp), C.byref(ds.grid),
+            C.byref(ds.mlp), C.byref(ds.smp), C.byref(b), C.byref(st)))
+        return b.value, st.value
 
     # -- geometry
     def raycast(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):
         """G-buffer of views x H x W pixels by ray casting the mesh's grid:
         (g0, g1) device float [views, H, W, 4] (g1 None unless asked for)."""
-        return self._gbuffer(lib().mixrt_raycast, mesh, cams, W, H, g1, out)
+        return self._gbuffer(self._L.mixrt_raycast, mesh, cams, W, H, g1, out)
 
     def rasterize(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):
         """The same G-buffer by rasterising the mesh (visibility buffer)."""
-        return self._gbuffer(lib().mixrt_rasterize, mesh, cams, W, H, g1, out)
+        return self._gbuffer(self._L.mixrt_rasterize, mesh, cams, W, H, g1, out)
 
     def _gbuffer(self, fn, mesh, cams, W, H, g1, out):
         import torch
@@ -398,10 +493,11 @@ class Renderer:
     # -- stage entry points
     def ray_setup(self, ds: DeviceScene):
         import torch
+        ds.check(self.device)
         K = ds.smp.K
         x = torch.empty((ds.rays, K, 3), dtype=torch.float32, device=ds.g0.device)
         hit = torch.empty((ds.rays,), dtype=torch.int32, device=ds.g0.device)
-        self._check(lib().mixrt_debug_ray_setup(self._h, C.byref(ds.gbuf), ds.cams,
+        self._check(self._L.mixrt_debug_ray_setup(self._h, C.byref(ds.gbuf), ds.cams,
                                                 C.byref(ds.disp), C.byref(ds.smp), _ptr(x),
                                                 _ptr(hit)))
         return x, hit
@@ -418,7 +514,7 @@ class Renderer:
             "w": torch.empty((n, L, 8), dtype=torch.float32, device=dev) if "w" in want else None,
             "feat": torch.empty((n, L * F), dtype=torch.float32, device=dev) if "feat" in want else None,
         }
-        self._check(lib().mixrt_debug_hash_encode(
+        self._check(self._L.mixrt_debug_hash_encode(
             self._h, C.byref(grid), _ptr(x), n, _ptr(out["corner"]), _ptr(out["idx"]),
             _ptr(out["w"]), _ptr(out["feat"])))
         return out
@@ -428,7 +524,7 @@ class Renderer:
         n = x_f16.shape[0]
         _require(x_f16, "x_f16", (torch.float16, torch.int16), n * mlp.width[0], self.device)
         out = torch.empty((n, 4), dtype=torch.float32, device=x_f16.device)
-        self._check(lib().mixrt_debug_mlp(self._h, C.byref(mlp), _ptr(x_f16), n, _ptr(out)))
+        self._check(self._L.mixrt_debug_mlp(self._h, C.byref(mlp), _ptr(x_f16), n, _ptr(out)))
         return out
 
     def composite(self, srgb, smp: Sampling, bg):
@@ -437,7 +533,7 @@ class Renderer:
         _require(srgb, "srgb", (torch.float32,), rays * smp.K * 4, self.device)
         out = torch.empty((rays, 4), dtype=torch.float32, device=srgb.device)
         bgc = (C.c_float * 3)(*[float(b) for b in bg])
-        self._check(lib().mixrt_debug_composite(self._h, _ptr(srgb), rays, C.byref(smp), bgc,
+        self._check(self._L.mixrt_debug_composite(self._h, _ptr(srgb), rays, C.byref(smp), bgc,
                                                 _ptr(out)))
         return out
 

@@ -35,6 +35,16 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) <= exported
 
 
+@pytest.mark.parametrize("variant", ["timer", "split_nodisp", "split_nohash", "split_nomlp"])
+def test_profiling_builds_export_the_same_symbols(variant):
+    """The profiling builds (the render kernel compiled with one -D option)
+    are drop-in replacements of libmixrt.so for the binding."""
+    L = mixrt.lib(variant)
+    for name in _declared_functions():
+        assert hasattr(L, name), name
+    assert L is not mixrt.lib()
+
+
 def test_microbench_library_exports_every_declared_symbol():
     from paper_2312_11841_amd import microbench
     text = open(os.path.join(ROOT, "include", "mixrt_microbench.h")).read()
@@ -131,21 +141,36 @@ def test_validate_accepts_every_workload(cfg):
     assert rc == mixrt.MIXRT_OK, msg
 
 
-def test_descriptors_keep_their_tensors_alive():
-    """A grid or MLP descriptor made from a tensor holds the tensor: the
-    device memory it points at cannot be freed and reused while it lives."""
-    import gc
-    import weakref
+def test_descriptor_makers_refuse_wrong_buffers():
+    """make_grid and make_mlp check the tensor behind the pointer they hand to
+    the library (dtype, layout, size, on a GPU) before any descriptor exists:
+    the library cannot see sizes, so a short or host buffer would be read out
+    of bounds on the GPU."""
     torch = pytest.importorskip("torch")
-    t = torch.zeros((2, 16, 2), dtype=torch.float16)
-    w = torch.zeros(16 * 16 + 16 * 4, dtype=torch.float16)
-    rt, rw = weakref.ref(t), weakref.ref(w)
-    g = mixrt.make_grid(t, 4, 8)
-    m = mixrt.make_mlp(w, (16, 16, 4), 0)
-    del t, w
-    gc.collect()
-    assert rt() is not None and g.data == rt().data_ptr()
-    assert rw() is not None and m.data == rw().data_ptr()
+    with pytest.raises(ValueError, match="dtype"):
+        mixrt.make_grid(torch.zeros((2, 16, 2), dtype=torch.float64), 4, 8)
+    with pytest.raises(ValueError, match="power of two"):
+        mixrt.make_grid(torch.zeros((2, 24, 2), dtype=torch.float16), 4, 8)
+    with pytest.raises(ValueError, match="3-d"):
+        mixrt.make_grid(torch.zeros((32, 2), dtype=torch.float16), 4, 8)
+    with pytest.raises(ValueError, match="contiguous"):
+        mixrt.make_grid(torch.zeros((2, 2, 16), dtype=torch.float16).transpose(1, 2), 4, 8)
+    with pytest.raises(ValueError, match="expected a GPU"):
+        mixrt.make_grid(torch.zeros((2, 16, 2), dtype=torch.float16), 4, 8)
+    w_ok = 16 * 16 + 16 * 4
+    with pytest.raises(ValueError, match="elements"):
+        mixrt.make_mlp(torch.zeros(w_ok - 1, dtype=torch.float16), (16, 16, 4), 0)
+    with pytest.raises(ValueError, match="dtype"):
+        mixrt.make_mlp(torch.zeros(w_ok, dtype=torch.float32), (16, 16, 4), 0)
+    with pytest.raises(ValueError, match="contiguous"):
+        mixrt.make_mlp(torch.zeros(2 * w_ok, dtype=torch.float16)[::2], (16, 16, 4), 0)
+    with pytest.raises(ValueError, match="expected a GPU"):
+        mixrt.make_mlp(torch.zeros(w_ok, dtype=torch.float16), (16, 16, 4), 0)
+    with pytest.raises(TypeError):
+        mixrt.make_mlp(None, (16, 16, 4), 0)
+    # the MLP removed has no weights to check
+    m = mixrt.make_mlp(None, (16,), 0)
+    assert m.n_layers == 0 and m.data is None
 
 
 def test_validate_accepts_every_random_sweep_config():

@@ -375,6 +375,28 @@ def test_miss_pixels_are_background(R):
     assert np.abs(got - ref).max() <= FRAME_TOL
 
 
+@pytest.mark.parametrize("delta", [0.0, 0.5])
+def test_overflowing_density(R, delta):
+    """Density heads large enough that fp32 exp overflows to inf on the GPU
+    (o0 > 88.7) for part of the samples: with delta = 0 every pixel is the
+    background with alpha 0 (a zero-length interval absorbs nothing); with
+    delta > 0 such a sample is opaque.  No NaN either way."""
+    cfg = synth.TINY64_DENSE.replace(name=f"overflow_d{delta}", delta=delta, seed=18)
+    sc = synth.make_scene(cfg)
+    sc.weights[-1][:, 0] = np.float16(40.0)   # sigma column of the head
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got = R.render(ds).cpu().numpy()
+    R.sync()
+    assert np.all(np.isfinite(got))
+    ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays), threads=oracle.max_threads())
+    err = np.abs(got - ref).max()
+    say(f"  delta {delta}: max |gpu - oracle| = {err:.3e}")
+    assert err <= FRAME_TOL
+    if delta == 0.0:
+        bg = np.array(list(cfg.bg) + [0.0], np.float32)
+        assert np.array_equal(got, np.tile(bg, (cfg.rays, 1)))
+
+
 def test_render_rejects_bad_calls(R):
     sc, ds = scene_of(synth.TINY64)
     bad = mixrt.make_sampling(65, 0.01, 1e-4)
@@ -413,6 +435,42 @@ def test_binding_rejects_wrong_buffers_before_any_launch(R):
         R.mlp(ds.mlp, torch.zeros((64, ds.mlp.width[0]), dtype=torch.float32, device="cuda:0"))
     with pytest.raises(ValueError, match="elements"):
         R.composite(torch.zeros((10, ds.smp.K, 3), device="cuda:0"), ds.smp, (0, 0, 0))
+
+
+def test_descriptors_keep_their_tensors_alive():
+    """A grid or MLP descriptor made from a tensor holds the tensor: the
+    device memory it points at cannot be freed and reused while it lives."""
+    import gc
+    import weakref
+    t = torch.zeros((2, 16, 2), dtype=torch.float16, device="cuda:0")
+    w = torch.zeros(16 * 16 + 16 * 4, dtype=torch.float16, device="cuda:0")
+    rt, rw = weakref.ref(t), weakref.ref(w)
+    g = mixrt.make_grid(t, 4, 8)
+    m = mixrt.make_mlp(w, (16, 16, 4), 0)
+    del t, w
+    gc.collect()
+    assert rt() is not None and g.data == rt().data_ptr()
+    assert rw() is not None and m.data == rw().data_ptr()
+
+
+def test_render_checks_the_scene_buffers(R):
+    """Scene tensors that no longer match their descriptors (replaced by a
+    shorter one, or moved to the host) are refused before the launch."""
+    import dataclasses
+    sc, ds = scene_of(synth.TINY64)
+    short = dataclasses.replace(ds, table=ds.table[:1].contiguous())
+    short.grid = mixrt.HashGrid(ds.grid.L, ds.grid.log2_T, ds.grid.F, ds.grid.N_min,
+                                ds.grid.N_max, ds.grid.dtype, short.table.data_ptr())
+    with pytest.raises(ValueError, match="table: .* elements"):
+        R.render(short)
+    host = dataclasses.replace(ds, g0=ds.g0.cpu())
+    with pytest.raises(ValueError, match="does not point"):
+        R.render(host)
+    small_tex = dataclasses.replace(ds, tex=ds.tex[:2].contiguous())
+    small_tex.disp = mixrt.DispTex.from_buffer_copy(ds.disp)
+    small_tex.disp.data = small_tex.tex.data_ptr()
+    with pytest.raises(ValueError, match="tex: .* elements"):
+        R.render(small_tex)
 
 
 def test_frame_does_not_depend_on_blocks_per_cu():
