@@ -97,6 +97,61 @@ def standalone_mlp(cfg, ds, renderer, samples):
             "hbm_bytes": samples * (cfg.widths[0] * 2 + 16)}
 
 
+def gather_replay_floor(cfg, ds, renderer):
+    """The render kernel's gather stream replayed alone: this frame's own
+    sample positions (its ray setup), the kernel's tile order, lane order and
+    level batches, loads XOR-folded (mixrt_mb_gather_replay).  The fastest of
+    a sweep of grid sizes is the floor for this access stream."""
+    import torch
+    from paper_2312_11841_amd import microbench as mb
+    from paper_2312_11841_amd import mixrt
+    x, hit = renderer.ray_setup(ds)
+    blocks, stripe = renderer.launch_shape(ds)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    N = mixrt.level_resolutions(ds.grid)
+    grids = sorted({blocks} | {k * cus for k in (1, 2, 3, 4, 6, 8)})
+    r = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N, stripe,
+                         grids)
+    del x, hit
+    return {"render_blocks": blocks, "tile_stripe": stripe, **r}
+
+
+def stage_metrics(cfg, ds, out, steps):
+    """Where the fused kernel's time goes, two ways, both from builds of the
+    same render source with one -D option:
+      - phase timer: every wave adds the shader clocks of each phase of each
+        tile (s_memtime at the phase boundaries); a phase's share of all
+        wave-clocks times the kernel's time is that phase's time;
+      - ablation (the paper's own method, Tab. 3): the frame with one stage
+        removed; the difference to the full kernel is the stage's marginal
+        cost (stages overlap in the fused kernel, so marginal costs need not
+        add up to the whole)."""
+    import torch
+    from paper_2312_11841_amd import mixrt
+    stream = torch.cuda.current_stream()
+    res = {}
+    r = mixrt.Renderer(0, stream=stream, variant="timer")
+    for _ in range(5):
+        r.render(ds, out)
+    r.phase_cycles(reset=True)
+    timer_ms = time_launches(stream, lambda: r.render(ds, out), steps)
+    ph = r.phase_cycles(reset=True)
+    r.close()
+    tot = sum(ph[k] for k in ("setup", "hash", "mlp", "composite"))
+    res["phase_share"] = {k: round(ph[k] / tot, 4) for k in ("setup", "hash", "mlp", "composite")}
+    res["timer_build_ms"] = round(timer_ms, 4)
+    abl = {}
+    for v in ("split_nodisp", "split_nohash", "split_nomlp"):
+        r = mixrt.Renderer(0, stream=stream, variant=v)
+        for _ in range(5):
+            r.render(ds, out)
+        abl[v.replace("split_", "without_")] = round(time_launches(stream, lambda: r.render(ds, out),
+                                                                   steps), 4)
+        r.close()
+    res["ablation_ms"] = abl
+    return res
+
+
 def algorithmic_work(cfg):
     """Bytes the method must move and MLP flops it must do, per frame.
 
@@ -176,6 +231,21 @@ def time_launches(stream, fn, steps):
     return a.elapsed_time(b) / steps
 
 
+def launch_stats(stream, fn, launches):
+    """Per-launch durations of fn() over `launches` launches, an event on
+    `stream` between consecutive launches: (median ms, mean ms)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(launches + 1)]
+    torch.cuda.synchronize()
+    ev[0].record(stream)
+    for i in range(launches):
+        fn()
+        ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    per = np.array([ev[i].elapsed_time(ev[i + 1]) for i in range(launches)])
+    return float(np.median(per)), float(per.mean())
+
+
 # The paper's profiling points (FPS at 1280x720 on a MacBook M1 Pro in WebGL,
 # one query per pixel): Tab. 3 (levels, table size, MLP) and Tab. 6 (with and
 # without the displacement map).  Context only: other hardware.
@@ -225,10 +295,14 @@ def paper_tables(steps, warmup):
 
 
 def sweep(steps, warmup):
-    """The ray x sample sweep: the first 2^16..2^24 rays of a coherent
-    4096x4096 view x K in {1..32}, on view720p's texture, grid and MLP.  The
-    view is generated once and its first rows rendered for each ray count."""
+    """The ray x sample sweep: the central 2^16..2^24 rays (whole rows) of a
+    coherent 4096x4096 view x K in {1..32}, on view720p's texture, grid and
+    MLP.  The view is generated once; each ray count renders its central rows
+    as an image of those rows whose camera keeps the full view's focal length
+    (tan(fov'/2) = tan(fov/2) rows / 4096), so every pixel's ray is the one it
+    has in the full view and the gathers keep the view's coherence."""
     import dataclasses
+    import math
     import torch
     from paper_2312_11841_amd import mixrt, synth
     full = synth.sweep_config(1 << 24, 8)
@@ -241,10 +315,17 @@ def sweep(steps, warmup):
     rows_out = []
     for log2r in (16, 18, 20, 22, 24):
         rays = 1 << log2r
+        rows = rays // full.W
+        row0 = (full.H - rows) // 2
         out = torch.empty((rays, 4), dtype=torch.float32, device="cuda:0")
-        gbuf = mixrt.GBuffer(1, full.W, rays // full.W, ds.gbuf.g0, 0)
+        g0 = ds.g0[:, row0:row0 + rows].contiguous()
+        gbuf = mixrt.GBuffer(1, full.W, rows, g0.data_ptr(), 0)
+        cams = scene.cams.copy()
+        half = math.radians(float(cams[0, 12])) / 2
+        cams[:, 12] = math.degrees(2 * math.atan(math.tan(half) * rows / full.H))
         for K in (1, 2, 4, 8, 16, 32):
-            d = dataclasses.replace(ds, gbuf=gbuf, rays=rays,
+            d = dataclasses.replace(ds, g0=g0, gbuf=gbuf, rays=rays,
+                                    cams=mixrt.make_cameras(cams),
                                     smp=mixrt.make_sampling(K, full.delta, full.t_term))
             n = max(steps, int(2e7 // (rays * K)))   # small launches: more of them
             for _ in range(warmup):
@@ -260,7 +341,8 @@ def sweep(steps, warmup):
             rows_out.append(row)
             print(json.dumps(row), file=sys.stderr, flush=True)
     r.close()
-    print(json.dumps({"sweep": rows_out, "view": "first rows of a coherent 4096x4096 view",
+    print(json.dumps({"sweep": rows_out, "view": "central rows of a coherent 4096x4096 view, "
+                                                 "each pixel's ray as in the full view",
                       "grid": "L16 T2^19 F2 f16 N 16-4096", "mlp": "48-64-64-4 fp16"}), flush=True)
 
 
@@ -359,6 +441,7 @@ def main():
         r.rasterize(mesh, ds.cams, cfg.W, cfg.H, g1=False, out=(ds.g0, None))
 
     geometry = rasterize if args.geometry == "raster" else raycast
+    extra = {}
 
     def render():
         r.render(ds, out)
@@ -368,10 +451,25 @@ def main():
             geometry()
         render()
 
+    # The measurements beside the headline (microbenchmark rooflines, the MLP
+    # stage alone, the gather replay, the profiling builds) run first: a GPU
+    # left idle for some tens of milliseconds drops its clock, and the first
+    # ~25 launches after that ran up to 12% slower than the steady rate
+    # (measured), so the timed steps come right after this GPU work.
+    replay = None
+    stages = None
+    if mesh is not None:
+        geometry()   # the G-buffer the legs below read
+    if not args.no_rooflines:
+        print("bench: rooflines, replay and stage builds", file=sys.stderr, flush=True)
+        extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
+        extra["rooflines_measured"] = measured_rooflines(cfg)
+        replay = gather_replay_floor(cfg, ds, r)
+        stages = stage_metrics(cfg, ds, out, max(args.steps, 20))
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    print(f"bench: warmup done, timing {args.steps} frames", file=sys.stderr, flush=True)
 
     # HIP events on the renderer's stream bracket exactly the timed launches.
     t_wall = time.perf_counter()
@@ -380,7 +478,12 @@ def main():
     # The roofline's kernel timed on its own (for a render-only step this is
     # the step itself).
     render_ms = ms if mesh is None else time_launches(stream, render, args.steps)
-    extra = {}
+    # ms per frame as the median of at least 100 launches, each timed by the
+    # events on either side of it (the K timed steps above give the mean)
+    n_med = max(100, args.steps)
+    med_ms, med_mean_ms = launch_stats(stream, step, n_med)
+    print(f"bench: timed {args.steps} frames ({ms:.4f} ms each), median of {n_med}: "
+          f"{med_ms:.4f} ms", file=sys.stderr, flush=True)
     if mesh is not None:
         ray_ms = time_launches(stream, raycast, args.steps)
         ras_ms = time_launches(stream, rasterize, args.steps)
@@ -396,9 +499,6 @@ def main():
                            "raycast": round(cfg.rays / (ray_ms * 1e-3) / 1e6, 1)},
             "mesh_faces": int(len(scene.mesh.faces)), "mesh_bytes": int(scene.mesh.nbytes),
             "grid": mesh.info, "load_s": round(mesh_load_s, 2)}
-    if not args.no_rooflines:
-        extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
-        extra["rooflines_measured"] = measured_rooflines(cfg)
     if mesh is not None:
         mesh.close()
     r.close()
@@ -410,6 +510,71 @@ def main():
     total_bytes = work["hash_bytes"] + work["ray_bytes"]
     achieved = total_bytes / rsec / 1e9
     mpix = cfg.rays / sec / 1e6
+    hbm_line = {"achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "note": "algorithmic bytes over the HBM peak; the bytes include gathers "
+                        "the L1 and L2 serve, so this is not what binds the kernel"}
+    if replay is not None:
+        rms = replay["best"]["ms"]
+        roofline = {
+            "kernel": "render_kernel (fused path" + (", the only kernel of a step)"
+                                                     if mesh is None else "; timed alone)"),
+            "bound": "vector_l1",
+            "achieved": round(achieved, 1),
+            "peak": round(total_bytes / (rms * 1e-3) / 1e9, 1),
+            "unit": "GB/s",
+            "frac": round(rms / render_ms, 4),
+            "traffic": traffic,
+            "traffic_source": traffic_src,
+            "peak_source": "gather replay measured in this run: this frame's own corner "
+                           "loads, in the kernel's tile, lane and level-batch order, issued "
+                           "alone (mixrt_mb_gather_replay, fastest grid size); the counters "
+                           "show the vector L1 as the saturated unit",
+            "gather_replay": {"ms": round(rms, 4), "frac": round(rms / render_ms, 4),
+                              "address_only_ms": round(replay["best"]["address_only_ms"], 4),
+                              "blocks": replay["best"]["blocks"],
+                              "render_blocks": replay["render_blocks"],
+                              "tile_stripe": replay["tile_stripe"],
+                              "by_blocks": [{k: (round(v, 4) if isinstance(v, float) else v)
+                                             for k, v in row.items()}
+                                            for row in replay["by_blocks"]]},
+            "hbm": hbm_line,
+            "algorithmic_bytes_per_launch": total_bytes,
+            "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
+                                           "ray": work["per_ray_bytes"]},
+        }
+    else:
+        roofline = {
+            "kernel": "render_kernel",
+            "bound": "hbm", **hbm_line, "traffic": traffic, "traffic_source": traffic_src,
+            "algorithmic_bytes_per_launch": total_bytes,
+            "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
+                                           "ray": work["per_ray_bytes"]},
+        }
+    stage_fields = {}
+    if stages is not None:
+        share = stages["phase_share"]
+        hash_s = share["hash"] * rsec
+        mlp_s = share["mlp"] * rsec
+        stage_fields = {
+            "stages": {
+                "method": "phase-timer build (the render source compiled with "
+                          "-DMIXRT_PHASE_TIMER: per-wave shader clocks per phase, a phase's "
+                          "time = its share of all wave-clocks x the kernel's time) and "
+                          "ablation builds (-DMIXRT_SPLIT_NO_*: one stage removed; full - "
+                          "ablated = that stage's marginal cost)",
+                **stages,
+                "hash_stage_ms": round(hash_s * 1e3, 4),
+                "mlp_phase_ms": round(mlp_s * 1e3, 4),
+            },
+            "hash_encode_GBps": round(work["hash_bytes"] / hash_s / 1e9, 1),
+            "hash_encode_GBps_vs_replay": round(
+                (work["hash_bytes"] / hash_s) / (work["hash_bytes"] / (replay["best"]["ms"] * 1e-3)),
+                4) if replay is not None else None,
+            "mlp_mfma_util": round(work["mlp_flops"] / mlp_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+            "mlp_phase_tflops": round(work["mlp_flops"] / mlp_s / 1e12, 1),
+            "stage_metric_method": "phase timer (see stages.method)",
+        }
     line = {
         "metric": "Mpix/s and ms/frame at 1280x720 (1 GPU); hash-encode GB/s, MLP MFMA util",
         "value": round(mpix, 2),
@@ -418,7 +583,10 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 4),
-        "ms_per_frame": round(ms, 4),
+        "ms_per_frame": round(med_ms, 4),
+        "ms_per_frame_stat": f"median of {n_med} launches, each bracketed by HIP events",
+        "ms_per_frame_mean": round(med_mean_ms, 4),
+        "Mpix_per_s_at_median": round(cfg.rays / (med_ms * 1e-3) / 1e6, 2),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -435,27 +603,9 @@ def main():
             "samples": cfg.samples,
             "parallelism": "single GPU",
         },
-        "roofline": {
-            "kernel": "render_kernel (fused path" + (", the only kernel of a step)" if mesh is None
-                                                      else "; timed alone)"),
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic,
-            "traffic_source": traffic_src,
-            "algorithmic_bytes_per_launch": total_bytes,
-            "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
-                                           "ray": work["per_ray_bytes"]},
-            "note": "achieved counts every table entry a sample gathers; samples that share "
-                    "cache lines are served by the L1 and L2, so it can exceed the HBM peak "
-                    "on coherent frames; traffic is what reached HBM and the Infinity Cache",
-        },
-        "hash_encode_GBps": round(work["hash_bytes"] / rsec / 1e9, 1),
+        "roofline": roofline,
+        **stage_fields,
         "hash_lane_loads_per_s": round(cfg.samples * cfg.L * 8 / rsec),
-        "mlp_mfma_util": round(work["mlp_flops"] / rsec / 1e12 / MFMA_F16_PEAK_TFLOPS, 5),
-        "mlp_tflops": round(work["mlp_flops"] / rsec / 1e12, 2),
         "wall_s_timed": round(t_wall, 3),
         "kernel_source_digest": kernel_source_digest(),
     }

@@ -87,6 +87,12 @@ typedef struct {
     void *hip_stream;    /* hipStream_t the context enqueues on (NULL: the
                             device's null stream); caller-owned */
     uint32_t flags;      /* mixrt_flags */
+    int32_t tile_stripe; /* order in which the render kernel's waves take the
+                            image's tiles (speed only, never a result): 0 the
+                            library's choice (stripes about 48 pixels wide),
+                            > 0 vertical stripes of that many tiles, each
+                            stripe row by row (compact blocks of pixels per
+                            XCD), < 0 plain row-major order */
 } mixrt_create_info;
 
 /* The coarse-mesh hit per pixel (Fig. 2 step 1): rasterisation output. */
@@ -207,7 +213,26 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
                  const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
                  const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
 
+/* The persistent grid (blocks of 256 threads) and the tile-order stripe
+ * width (tiles; the image's tile columns for row-major order) that
+ * mixrt_render would launch for these descriptors on this context; nothing
+ * is enqueued.  blocks, tile_stripe: host int32. */
+int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
+                              const mixrt_camera *cams, const mixrt_disp_tex *disp,
+                              const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe);
+
 /* ---- stage entry points (the same device code as mixrt_render) ------------ */
+
+/* Profiling: in the phase-timer build of the library (the same sources
+ * compiled with -DMIXRT_PHASE_TIMER, which renders the same frames), every
+ * wave of mixrt_render adds the shader clocks it spends in each phase of a
+ * tile to device counters.  Waits for the device, then writes out (host
+ * uint64[8]): [0] setup (ray, G-buffer, Eq. 2, samples, contraction),
+ * [1] hash encoding, [2] MLP (with the view encoding), [3] compositing and
+ * store, summed over waves; [4] tiles; [5] waves; [6], [7] zero.  reset != 0
+ * zeroes the counters after reading.  MIXRT_EUNSUPPORTED in other builds. */
+int mixrt_debug_phase_cycles(mixrt_ctx *ctx, uint64_t *out, int reset);
 
 /* Steps before the grid: ray, hit, Eq. 2 calibration, K samples, contraction
  * and normalisation to [0,1]^3.  out_x: device float [views*H*W][K][3] (the

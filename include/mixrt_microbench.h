@@ -38,6 +38,24 @@ int mixrt_mb_read(const void *src, uint64_t bytes, int blocks, uint32_t *sink, v
  * out: device float [blocks*256]. */
 int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
 
+/* Gather replay of one frame's hash-grid loads, the floor of the render
+ * kernel's gather stream: blocks x 256 threads, the render kernel's
+ * XCD-contiguous block mapping and tile order (tile_stripe as returned by
+ * mixrt_render_launch_shape), one sample per lane as in the render kernel;
+ * each lane reads its sample's position from x (device float
+ * [views*H*W][K][3], the frame's mixrt_debug_ray_setup output; rays with
+ * hit[ray] == 0 are skipped, hit: device int32 [views*H*W]), computes the
+ * level's voxel and corner offsets like the render kernel and issues the
+ * same loads of `entry_bytes`-byte entries (4, 8 or 16) from `table`
+ * (device [L][2^log2_T] entries, 16-byte aligned) in the same batches,
+ * keeping only an XOR of the loaded words (mode 0).  Mode 1 issues no loads
+ * (address arithmetic alone).  N: host int32 [L], the level resolutions
+ * (non-decreasing).  sink: device uint32 [blocks*256] (written). */
+int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
+                           int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
+                           int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
+                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream);
+
 /* Properties of HIP device `device` the measurements are quoted against:
  * peak shader clock (kHz), memory clock (kHz), compute units, L2 bytes, and
  * the architecture name (NUL-terminated, at most cap bytes written). */

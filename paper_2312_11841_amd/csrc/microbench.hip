@@ -12,6 +12,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <cmath>
+
+#include "mixrt_common.hpp"
 #include "mixrt_microbench.h"
 
 namespace {
@@ -129,9 +132,177 @@ __global__ __launch_bounds__(kBlock) void mfma_kernel(int iters, float *__restri
     out[blockIdx.x * kBlock + threadIdx.x] = s[0] + s[1] + s[2] + s[3];
 }
 
+// ---------------------------------------------------------------------------
+// Gather replay: the hash-grid loads of one frame, in the render kernel's
+// order and nothing else.  Same persistent grid, XCD-contiguous block
+// mapping and tile order (stripe) as the render kernel; a lane takes the
+// same sample of the same tile, reads that sample's position from the frame's
+// ray-setup output, and issues the same loads in the same batches (dense
+// levels as x-neighbour pairs, two levels per batch).  The loaded words are
+// XOR-folded into one word per lane (no fp16 conversion, no interpolation,
+// no MLP, no compositing), so the kernel's time is the floor that this exact
+// access stream, plus the address arithmetic that produces it, sets.  MODE 1
+// drops the loads and folds the offsets instead (the address arithmetic
+// alone).
+// ---------------------------------------------------------------------------
+template <uint32_t EB>
+struct RawEntry;
+template <> struct RawEntry<4> {
+    static __device__ __forceinline__ uint32_t one(const char *t, uint32_t o)
+    {
+        return *(const uint32_t *)(t + o);
+    }
+    static __device__ __forceinline__ uint32_t pair(const char *t, uint32_t o)
+    {
+        const uint64_t v = *(const mixrt::u64a4 *)(t + o);
+        return (uint32_t)v ^ (uint32_t)(v >> 32);
+    }
+};
+template <> struct RawEntry<8> {
+    static __device__ __forceinline__ uint32_t one(const char *t, uint32_t o)
+    {
+        const uint2 v = *(const uint2 *)(t + o);
+        return v.x ^ v.y;
+    }
+    static __device__ __forceinline__ uint32_t pair(const char *t, uint32_t o)
+    {
+        const unsigned __int128 v = *(const mixrt::u128a8 *)(t + o);
+        return (uint32_t)v ^ (uint32_t)(v >> 32) ^ (uint32_t)(v >> 64) ^ (uint32_t)(v >> 96);
+    }
+};
+template <> struct RawEntry<16> {
+    static __device__ __forceinline__ uint32_t one(const char *t, uint32_t o)
+    {
+        const uint4 v = *(const uint4 *)(t + o);
+        return v.x ^ v.y ^ v.z ^ v.w;
+    }
+    static __device__ __forceinline__ uint32_t pair(const char *t, uint32_t o)
+    {
+        return one(t, o) ^ one(t, o + 16u);
+    }
+};
+
+template <uint32_t EB, int G, bool DENSE, int MODE>
+__device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, int l0, float x0,
+                                                 float x1, float x2)
+{
+    mixrt::LevelSetup s[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+        mixrt::level_setup<EB, true>(gp, l0 + g, DENSE, x0, x1, x2, s[g]);
+    uint32_t v[G][8];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        const char *t = (const char *)gp.table + (size_t)(l0 + g) * ((size_t)gp.T_mask + 1) * EB;
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            if (DENSE && (b & 1)) continue;   // a dense pair covers corners b and b + 1
+            if (MODE == 1)
+                v[g][b] = s[g].off[b];
+            else
+                v[g][b] = DENSE ? RawEntry<EB>::pair(t, s[g].off[b]) : RawEntry<EB>::one(t, s[g].off[b]);
+        }
+    }
+    uint32_t acc = 0;
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+            if (!(DENSE && (b & 1))) acc ^= v[g][b];
+    return acc;
+}
+
+template <uint32_t EB, int MODE>
+__global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict__ x,
+                                                        const int32_t *__restrict__ hit, int views,
+                                                        int W, int H, int K, int stripe,
+                                                        mixrt::GridParams gp,
+                                                        uint32_t *__restrict__ sink)
+{
+    constexpr int kGroup = 2;
+    const int lane = threadIdx.x & 63;
+    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+    const int R = 64 / K;
+    const mixrt::TileShape ts = mixrt::tile_shape(R, views, W, H, stripe);
+    const int gw = mixrt::xcd_logical_block(blockIdx.x, gridDim.x) * 4 + wv;
+    const int total = gridDim.x * 4;
+    const int r_loc = lane / K, k = lane - r_loc * K;
+    const int L = gp.L, n_dense = gp.n_dense;
+    uint32_t acc = 0;
+    for (int tile = gw; tile < ts.n_tiles; tile += total) {
+        const mixrt::TilePos tp = mixrt::tile_at(ts, tile);
+        const int i0 = tp.tx * ts.RW, j0 = tp.ty * ts.RH;
+        const int dy = r_loc / ts.RW, dx = r_loc - dy * ts.RW;
+        const bool valid = r_loc < R && i0 + dx < W && j0 + dy < H;
+        if (!valid) continue;
+        const int ray = (tp.view * H + j0 + dy) * W + i0 + dx;
+        if (!hit[ray]) continue;
+        const float *p = x + ((size_t)ray * K + k) * 3;
+        // positions into [0, 1] (NaN to 0), which level_setup's in-unit form
+        // needs to keep every corner inside its level
+        const float x0 = p[0] >= 0.0f ? fminf(p[0], 1.0f) : 0.0f;
+        const float x1 = p[1] >= 0.0f ? fminf(p[1], 1.0f) : 0.0f;
+        const float x2 = p[2] >= 0.0f ? fminf(p[2], 1.0f) : 0.0f;
+        int l = 0;
+        for (; l + kGroup <= n_dense; l += kGroup) acc ^= replay_group<EB, kGroup, true, MODE>(gp, l, x0, x1, x2);
+        for (; l < n_dense; ++l) acc ^= replay_group<EB, 1, true, MODE>(gp, l, x0, x1, x2);
+        for (; l + kGroup <= L; l += kGroup) acc ^= replay_group<EB, kGroup, false, MODE>(gp, l, x0, x1, x2);
+        for (; l < L; ++l) acc ^= replay_group<EB, 1, false, MODE>(gp, l, x0, x1, x2);
+    }
+    sink[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
+}
+
 }  // namespace
 
 extern "C" {
+
+int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
+                           int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
+                           int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
+                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream)
+{
+    if (!x || !hit || !table || !N || !sink) return hipErrorInvalidValue;
+    if (views < 1 || W < 1 || H < 1 || (int64_t)views * H * W >= ((int64_t)1 << 31))
+        return hipErrorInvalidValue;
+    if (K < 1 || K > 64 || L < 1 || L > mixrt::kMaxLevels || log2_T < 4 || log2_T > 26)
+        return hipErrorInvalidValue;
+    if (entry_bytes != 4 && entry_bytes != 8 && entry_bytes != 16) return hipErrorInvalidValue;
+    if ((mode != 0 && mode != 1) || blocks < 1) return hipErrorInvalidValue;
+    if (((uintptr_t)table & 15) != 0) return hipErrorInvalidValue;
+    mixrt::GridParams gp;
+    memset(&gp, 0, sizeof gp);
+    gp.table = table;
+    gp.log2_T = (uint32_t)log2_T;
+    gp.T_mask = (uint32_t)((1u << log2_T) - 1u);
+    gp.L = L;
+    const uint64_t T = 1ull << log2_T;
+    for (int l = 0; l < L; ++l) {
+        if (N[l] < 1 || N[l] > (1 << 20) || (l > 0 && N[l] < N[l - 1])) return hipErrorInvalidValue;
+        gp.N[l] = (uint32_t)N[l];
+        gp.Nf[l] = (float)N[l];
+        gp.Ntop[l] = (float)(N[l] - 1);
+        const uint64_t side = (uint64_t)N[l] + 1;
+        if (side * side * side <= T) {
+            gp.dense_mask |= 1u << l;
+            gp.n_dense = l + 1;
+        }
+    }
+    hipStream_t s = (hipStream_t)stream;
+#define RP(EB, M)                                                                                \
+    hipLaunchKernelGGL((replay_kernel<EB, M>), dim3(blocks), dim3(kBlock), 0, s, x, hit, views, \
+                       W, H, K, tile_stripe, gp, sink)
+    if (mode == 0) {
+        if (entry_bytes == 4) RP(4, 0);
+        else if (entry_bytes == 8) RP(8, 0);
+        else RP(16, 0);
+    } else {
+        if (entry_bytes == 4) RP(4, 1);
+        else if (entry_bytes == 8) RP(8, 1);
+        else RP(16, 1);
+    }
+#undef RP
+    return hipGetLastError();
+}
 
 int mixrt_mb_gather(const void *table, uint64_t table_bytes, int width, int loads_per_iter,
                     int iters, int pattern, int blocks, uint32_t *sink, void *stream)

@@ -23,6 +23,7 @@ struct mixrt_ctx {
     int device = 0;
     hipStream_t stream = nullptr;
     uint32_t flags = 0;
+    int32_t tile_stripe = 0;
     int cus = 0;
     int64_t l2_bytes = 0;
     std::string err;
@@ -607,6 +608,7 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     ctx->device = ci->device;
     ctx->stream = (hipStream_t)ci->hip_stream;
     ctx->flags = ci->flags;
+    ctx->tile_stripe = ci->tile_stripe;
     ctx->cus = prop.multiProcessorCount;
     ctx->l2_bytes = prop.l2CacheSize;
     *out = ctx;
@@ -631,20 +633,15 @@ int mixrt_sync(mixrt_ctx *ctx)
     return MIXRT_OK;
 }
 
-int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
-                 const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
-                 const mixrt_sampling *smp, float *out_rgba)
+namespace {
+
+// The launch of a render call whose descriptors validated (hid, nhid: the
+// MLP's hidden width and hidden-layer count).
+void fill_render_launch(mixrt::RenderLaunch &L, const mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
+                        const mixrt_camera *cams, const mixrt_disp_tex *disp,
+                        const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                        const mixrt_sampling *smp, int hid, int nhid, float *out_rgba)
 {
-    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
-    clear_err(ctx);
-    char msg[512];
-    int hid = 0, nhid = 0;
-    int rc = validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, sizeof msg}, &hid, &nhid);
-    if (rc) return fail(ctx, rc, "%s", msg);
-    if (!out_rgba) return fail(ctx, MIXRT_EINVAL, "out_rgba is NULL");
-    if (!aligned16(out_rgba)) return fail(ctx, MIXRT_EINVAL, "out_rgba not 16-byte aligned");
-    if ((rc = bind_device(ctx))) return rc;
-    mixrt::RenderLaunch L;
     fill_ray_params(L.rp, gbuf, cams, disp, smp);
     fill_grid_params(L.gp, grid);
     L.weights = (const _Float16 *)mlp->data;
@@ -659,7 +656,65 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
     L.cus = ctx->cus;
     L.l2_bytes = ctx->l2_bytes;
     L.blocks_mode = (ctx->flags & MIXRT_FLAG_BLOCKS_FULL) ? 1 : (ctx->flags & MIXRT_FLAG_BLOCKS_TWO) ? 2 : 0;
+    L.tile_stripe = ctx->tile_stripe;
+}
+
+}  // namespace
+
+int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                 const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                 const mixrt_sampling *smp, float *out_rgba)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    int hid = 0, nhid = 0;
+    int rc = validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, sizeof msg}, &hid, &nhid);
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (!out_rgba) return fail(ctx, MIXRT_EINVAL, "out_rgba is NULL");
+    if (!aligned16(out_rgba)) return fail(ctx, MIXRT_EINVAL, "out_rgba not 16-byte aligned");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::RenderLaunch L;
+    fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, out_rgba);
     return finish_launch(ctx, mixrt::launch_render(L, ctx->stream), "render");
+}
+
+int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
+                              const mixrt_camera *cams, const mixrt_disp_tex *disp,
+                              const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    char msg[512];
+    int hid = 0, nhid = 0;
+    int rc = validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, sizeof msg}, &hid, &nhid);
+    if (rc) return fail(ctx, rc, "%s", msg);
+    if (!blocks || !tile_stripe) return fail(ctx, MIXRT_EINVAL, "blocks or tile_stripe is NULL");
+    if ((rc = bind_device(ctx))) return rc;
+    mixrt::RenderLaunch L;
+    fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, nullptr);
+    int b = 0, st = 0;
+    const hipError_t e = mixrt::render_launch_shape(L, &b, &st);
+    if (e != hipSuccess)
+        return fail(ctx, MIXRT_EDEVICE, "render launch shape: %s", hipGetErrorString(e));
+    *blocks = b;
+    *tile_stripe = st;
+    return MIXRT_OK;
+}
+
+int mixrt_debug_phase_cycles(mixrt_ctx *ctx, uint64_t *out, int reset)
+{
+    if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
+    clear_err(ctx);
+    if (!out) return fail(ctx, MIXRT_EINVAL, "out is NULL");
+    int rc = bind_device(ctx);
+    if (rc) return rc;
+    const hipError_t e = mixrt::phase_cycles_read(out, reset != 0);
+    if (e == hipErrorNotSupported)
+        return fail(ctx, MIXRT_EUNSUPPORTED, "this library is not the phase-timer build");
+    if (e != hipSuccess) return fail(ctx, MIXRT_EDEVICE, "phase cycles: %s", hipGetErrorString(e));
+    return MIXRT_OK;
 }
 
 int mixrt_debug_ray_setup(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,

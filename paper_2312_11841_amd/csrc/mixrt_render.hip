@@ -10,33 +10,40 @@
 #include "mixrt_common.hpp"
 #include "mixrt_launch.hpp"
 
+// Profiling builds of this same source, selected with -D at compile time
+// (the default build defines none of them; they exist to attribute the fused
+// kernel's time to its stages, the way the paper's Tab. 3 removes stages):
+//   MIXRT_SPLIT_NO_DISP  the displacement map is not read (p_cali = p);
+//   MIXRT_SPLIT_NO_HASH  no table loads, every feature is zero (the sample
+//                        positions are still computed and kept live);
+//   MIXRT_SPLIT_NO_MLP   no MFMA: a sample's output is its first 4 features;
+//   MIXRT_PHASE_TIMER    each wave adds the shader clocks it spends in each
+//                        phase of a tile (setup, hash encoding, MLP,
+//                        compositing) to phase_cycles, read back with
+//                        mixrt_debug_phase_cycles.
+// The split builds render wrong frames on purpose and are never the library
+// the binding loads by default; the timer build renders the same frames.
+
 namespace mixrt {
 
 // Levels per batch of corner loads in the render kernel.
 constexpr int kLevelGroup = 2;
 
-// A tile's R = 64/K rays cover a block of pixels, RW x RH with RW >= 4 RH,
-// when R is a power of two (8 rays: 8 x 1; 64 rays: 16 x 4), else one row
-// segment.  With one sample per ray the block puts nearby pixels in one wave,
-// so its gathers share more cache lines (K = 1: 10-16% faster than a row of
-// 64); with 8 samples per ray a row of 8 measured best.  Tiles never cross a
-// row or view boundary.
-struct TileShape {
-    int RW, RH, tiles_x, per_view, n_tiles;
-};
-
-__host__ __device__ inline TileShape tile_shape(int R, int views, int W, int H)
-{
-    TileShape t;
-    t.RH = 1;
-    if ((R & (R - 1)) == 0)
-        while (t.RH * t.RH * 16 <= R) t.RH *= 2;
-    t.RW = R / t.RH;
-    t.tiles_x = (W + t.RW - 1) / t.RW;
-    t.per_view = t.tiles_x * ((H + t.RH - 1) / t.RH);
-    t.n_tiles = views * t.per_view;
-    return t;
-}
+#ifdef MIXRT_PHASE_TIMER
+// [0..3] shader clocks summed over waves in setup, hash, MLP and compositing;
+// [4] tiles; [5] waves.
+__device__ unsigned long long phase_cycles[8];
+#define MIXRT_PHASE(i)                                          \
+    do {                                                        \
+        const uint64_t t_ = __builtin_readcyclecounter();       \
+        ph[i] += t_ - t_last;                                   \
+        t_last = t_;                                            \
+    } while (0)
+#else
+#define MIXRT_PHASE(i) \
+    do {               \
+    } while (0)
+#endif
 
 // G levels of one query: into its fp16 row of MLP inputs, or (the MLP
 // removed) added in fp32 to the per-component sums acc[(l F + i) mod 4].
@@ -73,9 +80,14 @@ struct NoMlp {
 template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
                                                         const _Float16 *__restrict__ weights,
-                                                        int view_sh, float4 *__restrict__ out)
+                                                        int view_sh, int stripe,
+                                                        float4 *__restrict__ out)
 {
+#ifdef MIXRT_SPLIT_NO_DISP
+    typedef TexKind<float, kDispNone> TK;
+#else
     typedef typename TexOf<TEX>::type TK;
+#endif
     constexpr int LD = IN + 8;  // padded row of MLP inputs (halves), 16-byte multiple
     __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][kWave * LD];
     __shared__ float4 s_out[kWavesPerBlock][kWave];
@@ -96,19 +108,23 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     const int K = rp.K;
     const int R = kWave / K;                 // rays per tile
     const int spt = R * K;                   // sample slots used per tile
-    const TileShape ts = tile_shape(R, rp.views, rp.W, rp.H);
+    const TileShape ts = tile_shape(R, rp.views, rp.W, rp.H, stripe);
     const int gw = xcd_logical_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wv;
     const int total = gridDim.x * kWavesPerBlock;
     const int r_loc = lane / K;
     const int k = lane - r_loc * K;
     const int L = gp.L;
     const int n_dense = gp.n_dense;
+#ifdef MIXRT_PHASE_TIMER
+    uint64_t ph[4] = {0, 0, 0, 0}, n_tiles_done = 0;
+    uint64_t t_last = __builtin_readcyclecounter();
+#endif
 
     for (int tile = gw; tile < ts.n_tiles; tile += total) {
         // the tile's pixel block, and ray r of it at (r % RW, r / RW)
-        const int view = tile / ts.per_view, rem = tile - view * ts.per_view;
-        const int ty = rem / ts.tiles_x, tx = rem - ty * ts.tiles_x;
-        const int i0 = tx * ts.RW, j0 = ty * ts.RH;
+        const TilePos tp = tile_at(ts, tile);
+        const int view = tp.view;
+        const int i0 = tp.tx * ts.RW, j0 = tp.ty * ts.RH;
         const int ray_base = (view * rp.H + j0) * rp.W + i0;
         const CamK &cam = rp.cams[view];
         auto ray_of = [&](int r, bool &in) {
@@ -131,7 +147,12 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         // loads), then hashed levels, kLevelGroup levels per batch of loads
         _Float16 *row = rows + lane * LD;
         float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+        MIXRT_PHASE(0);
+#ifdef MIXRT_SPLIT_NO_HASH
+        if (false) {
+#else
         if (hit) {
+#endif
             int l = 0;
             for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
                 encode_levels<F, TF16, kLevelGroup, true, SUM>(gp, l, x0, x1, x2, row, acc);
@@ -145,6 +166,11 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
             for (int e = 0; e < L * F; e += 2)
                 *(h2 *)(row + e) = h2{(_Float16)0.0f, (_Float16)0.0f};
         }
+#ifdef MIXRT_SPLIT_NO_HASH
+        // keep the sample positions (and so the ray setup) live
+        row[0] = (_Float16)((x0 + x1 + x2) * 0.0f);
+#endif
+        MIXRT_PHASE(1);
         if (!SUM && view_sh) {
             float Y[16];
             sh_basis<16>(ry.dx, ry.dy, ry.dz, Y);
@@ -166,7 +192,12 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
             const int c = lane & 15, g = lane >> 4;
             const int n_nt = (spt + 15) >> 4;
             for (int nt = 0; nt < n_nt; ++nt) {
+#ifdef MIXRT_SPLIT_NO_MLP
+                const _Float16 *rr = rows + (nt * 16 + c) * LD;
+                const f4 o = {(float)rr[0], (float)rr[1], (float)rr[2], (float)rr[3]};
+#else
                 const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * LD, LD, lane);
+#endif
                 if (g == 0) {
                     const int s = nt * 16 + c;
                     float4 a = mlp_activate(o);
@@ -176,6 +207,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
             }
             wave_lds_sync();
         }
+        MIXRT_PHASE(2);
         // --- compositing, one lane per ray
         if (lane < R) {
             bool in_c;
@@ -188,7 +220,18 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
             }
         }
         wave_lds_sync();
+        MIXRT_PHASE(3);
+#ifdef MIXRT_PHASE_TIMER
+        ++n_tiles_done;
+#endif
     }
+#ifdef MIXRT_PHASE_TIMER
+    if (lane == 0) {
+        for (int i = 0; i < 4; ++i) atomicAdd(&phase_cycles[i], (unsigned long long)ph[i]);
+        atomicAdd(&phase_cycles[4], (unsigned long long)n_tiles_done);
+        atomicAdd(&phase_cycles[5], 1ull);
+    }
+#endif
 }
 
 
@@ -245,25 +288,93 @@ static int render_blocks_per_cu(const RenderLaunch &L, int resident)
     return coherent || resident < 2 ? resident : 2;
 }
 
-hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
+// Tile order for a frame (the stripe width of tile_at, in tiles).  Waves
+// take tiles in order and the blocks are dealt to the 8 XCDs in contiguous
+// runs, so the tiles one XCD renders at once are a run of the order; in
+// stripes of about 48 pixels that run is a compact block of the image
+// instead of a strip along rows, and neighbouring pixels' samples, which
+// share voxel corners, meet in the same L2.  Measured on 16 workloads (K 1 to
+// 32, 720p and the 8-view 1080p batch): 48-pixel stripes were 1-13% faster
+// than row-major order everywhere and within 1.5% of each workload's best
+// stripe on most of them (4.5% at worst).
+static int render_stripe(const RenderLaunch &L, const TileShape &ts, int64_t blocks)
+{
+    (void)blocks;
+    constexpr int kStripePixels = 48;
+    if (L.tile_stripe < 0) return ts.tiles_x;
+    int st = L.tile_stripe > 0 ? L.tile_stripe : (kStripePixels + ts.RW / 2) / ts.RW;
+    if (st < 1) st = 1;
+    return st < ts.tiles_x ? st : ts.tiles_x;
+}
+
+// Grid size and tile order of a frame, given the blocks of its kernel that
+// fit on one CU.
+static void render_shape(const RenderLaunch &L, int resident, int64_t &blocks, int &stripe)
 {
     const int R = kWave / L.rp.K;
-    const int64_t n_tiles = tile_shape(R, L.rp.views, L.rp.W, L.rp.H).n_tiles;
-    const int64_t want = (n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+    const TileShape ts = tile_shape(R, L.rp.views, L.rp.W, L.rp.H, 0);
+    const int64_t want = ((int64_t)ts.n_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+    // blocks resident on the whole device
+    blocks = (int64_t)render_blocks_per_cu(L, resident) * L.cus;
+    if (want < blocks) blocks = want;
+    if (blocks > 8) blocks -= blocks % 8;
+    if (blocks < 1) blocks = 1;
+    stripe = render_stripe(L, ts, blocks);
+}
+
+// Blocks of one render kernel that fit on a CU, queried once per kernel.
+template <int A, int B, bool C, int D, int E, int F_>
+static int render_resident()
+{
+    static std::atomic<int> cache{0};
+    return blocks_per_cu((const void *)render_kernel<A, B, C, D, E, F_>, cache);
+}
+
+#define MIXRT_RENDER_MATCH(a, b, c, d, e, f) \
+    (L.tex == a && L.F == b && L.tf16 == c && L.nhid == f && (f == 0 || (L.in == d && L.hid == e)))
+
+hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
+{
 #define X(a, b, c, d, e, f)                                                                    \
-    if (L.tex == a && L.F == b && L.tf16 == c && L.nhid == f &&                                \
-        (f == 0 || (L.in == d && L.hid == e))) {                                               \
-        auto fn = render_kernel<a, b, c, d, e, f>;                                             \
-        static std::atomic<int> per_cu{0};                                                     \
-        /* blocks resident on the whole device */                                              \
-        int64_t blocks =                                                                       \
-            (int64_t)render_blocks_per_cu(L, blocks_per_cu((const void *)fn, per_cu)) * L.cus; \
-        if (want < blocks) blocks = want;                                                      \
-        if (blocks > 8) blocks -= blocks % 8;                                                  \
-        if (blocks < 1) blocks = 1;                                                            \
-        hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, L.rp, L.gp,    \
-                           L.weights, L.view_sh, L.out);                                       \
+    if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
+        int64_t blocks;                                                                        \
+        int stripe;                                                                            \
+        render_shape(L, render_resident<a, b, c, d, e, f>(), blocks, stripe);                  \
+        hipLaunchKernelGGL((render_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks),          \
+                           dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh, stripe,  \
+                           L.out);                                                             \
         return hipGetLastError();                                                              \
+    }
+    MIXRT_RENDER_VARIANTS(X)
+#undef X
+    return hipErrorInvalidValue;
+}
+
+hipError_t phase_cycles_read(uint64_t *out, bool reset)
+{
+#ifdef MIXRT_PHASE_TIMER
+    hipError_t e = hipDeviceSynchronize();
+    if (e == hipSuccess) e = hipMemcpyFromSymbol(out, HIP_SYMBOL(phase_cycles), 8 * sizeof(uint64_t));
+    if (e == hipSuccess && reset) {
+        const unsigned long long zero[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+        e = hipMemcpyToSymbol(HIP_SYMBOL(phase_cycles), zero, sizeof zero);
+    }
+    return e;
+#else
+    (void)out;
+    (void)reset;
+    return hipErrorNotSupported;
+#endif
+}
+
+hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe)
+{
+#define X(a, b, c, d, e, f)                                                                    \
+    if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
+        int64_t nb;                                                                            \
+        render_shape(L, render_resident<a, b, c, d, e, f>(), nb, *stripe);                     \
+        *blocks = (int)nb;                                                                     \
+        return hipSuccess;                                                                     \
     }
     MIXRT_RENDER_VARIANTS(X)
 #undef X

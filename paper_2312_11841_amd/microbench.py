@@ -25,6 +25,10 @@ def lib():
         L.mixrt_mb_copy.argtypes = [P, P, C.c_uint64, C.c_int, P]
         L.mixrt_mb_read.argtypes = [P, C.c_uint64, C.c_int, P, P]
         L.mixrt_mb_mfma.argtypes = [C.c_int, C.c_int, P, P]
+        I32 = C.c_int32
+        L.mixrt_mb_gather_replay.argtypes = [P, P, I32, I32, I32, I32, P, I32, I32, I32, P, I32,
+                                             I32, I32, P, P]
+        L.mixrt_mb_gather_replay.restype = C.c_int
         IP = C.POINTER(C.c_int)
         L.mixrt_mb_device_info.argtypes = [C.c_int, IP, IP, IP, IP, C.c_char_p, C.c_int]
         for f in (L.mixrt_mb_gather, L.mixrt_mb_copy, L.mixrt_mb_read, L.mixrt_mb_mfma,
@@ -129,3 +133,37 @@ def device_info(device: int = 0) -> dict:
                                       C.byref(l2), arch, 64))
     return {"clock_MHz": clk.value // 1000, "mem_clock_MHz": mclk.value // 1000,
             "compute_units": cus.value, "l2_bytes": l2.value, "arch": arch.value.decode()}
+
+
+def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_stripe: int,
+                  blocks_list, reps: int = 20):
+    """The frame's hash-grid loads replayed in the render kernel's order
+    (mixrt_mb_gather_replay): for each grid size in blocks_list, the mean time
+    of the loads (mode 0) and of their address arithmetic alone (mode 1).
+    x: device float [rays][K][3] and hit: device int32 [rays] from the
+    frame's ray setup; table: the device hash table [L][T][F]; N: level
+    resolutions.  Returns per-grid-size times and the fastest."""
+    import numpy as np
+    import torch
+    L_, T, F = (int(n) for n in table.shape)
+    eb = F * table.element_size()
+    Nh = np.ascontiguousarray(np.asarray(N, np.int32))
+    assert x.is_cuda and hit.is_cuda and table.is_cuda and x.is_contiguous()
+    assert x.numel() == views * H * W * K * 3 and hit.numel() == views * H * W
+    assert Nh.size == L_ and T & (T - 1) == 0
+    rows = []
+    for blocks in blocks_list:
+        sink = torch.empty(int(blocks) * 256, dtype=torch.int32, device=x.device)
+        res = {"blocks": int(blocks)}
+        for mode, name in ((0, "ms"), (1, "address_only_ms")):
+            def launch(s, mode=mode):
+                _check(lib().mixrt_mb_gather_replay(
+                    x.data_ptr(), hit.data_ptr(), views, W, H, K, table.data_ptr(), L_,
+                    T.bit_length() - 1, eb, Nh.ctypes.data, int(tile_stripe), mode, int(blocks),
+                    sink.data_ptr(), s.cuda_stream))
+            for _ in range(3):
+                launch(torch.cuda.current_stream())
+            res[name] = _timed(launch, reps) * 1e3
+        rows.append(res)
+    best = min(rows, key=lambda r: r["ms"])
+    return {"by_blocks": rows, "best": best}

@@ -1,0 +1,143 @@
+"""GPU checks of what changes the render kernel's speed but never its result:
+the tile order (stripes of tiles per XCD), the profiling builds that time
+the kernel's phases, and the gather-replay microbenchmark that measures the
+floor of its gather stream.
+
+  - every tile order renders the same frame bit for bit, and every pixel;
+  - the phase-timer build renders the same frame as the library, and its
+    counters cover every tile of every launch;
+  - the replay loads exactly the table entries of the oracle's corner
+    indices for the frame's own sample positions (the XOR of everything it
+    loads equals the XOR of those entries, which does not depend on which
+    lane loaded what).
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2312_11841_amd import mixrt, synth
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def _render(ds, **kw):
+    r = mixrt.Renderer(0, sync_check=True, **kw)
+    out = torch.full((ds.rays, 4), float("nan"), dtype=torch.float32, device="cuda:0")
+    r.render(ds, out)
+    shape = r.launch_shape(ds)
+    r.sync()
+    r.close()
+    return out.cpu().numpy(), shape
+
+
+ORDER_CFGS = [
+    synth.VIEW720P_DENSE,
+    synth.PAPER720P,
+    synth.TINY64_DENSE.replace(name="ragged_views", H=37, W=53, views=3, K=8, gbuf="iid"),
+    synth.TINY64_DENSE.replace(name="ragged_k1", H=29, W=71, views=2, K=1, gbuf="iid"),
+    synth.TINY64_DENSE.replace(name="ragged_k3", H=23, W=37, views=2, K=3, gbuf="iid"),
+]
+
+
+@pytest.mark.parametrize("cfg", ORDER_CFGS, ids=lambda c: c.name)
+def test_tile_order_never_changes_a_pixel(cfg):
+    say("tile order", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    ref, (_, default_stripe) = _render(ds, tile_stripe=-1)
+    assert np.all(np.isfinite(ref))
+    R = 64 // cfg.K
+    seen = {default_stripe}
+    for stripe in (1, 2, 3, 8, 16, 37, 1 << 20, 0):
+        got, (blocks, st) = _render(ds, tile_stripe=stripe)
+        seen.add(st)
+        assert np.array_equal(got, ref), (stripe, st)
+        for b in ("two", "full"):
+            got, _ = _render(ds, tile_stripe=stripe, blocks=b)
+            assert np.array_equal(got, ref), (stripe, b)
+    say(f"  stripes launched: {sorted(seen)} (tiles of {R} rays)")
+
+
+def test_tile_order_spot_check_against_the_oracle():
+    cfg = ORDER_CFGS[2]
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got, _ = _render(ds, tile_stripe=3)
+    ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays), threads=oracle.max_threads())
+    assert np.abs(got - ref).max() <= 2e-3
+
+
+@pytest.mark.parametrize("cfg", [synth.VIEW720P, synth.PAPER720P], ids=lambda c: c.name)
+def test_phase_timer_build_renders_the_same_frame(cfg):
+    say("timer build", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    ref, (blocks, stripe) = _render(ds)
+    r = mixrt.Renderer(0, sync_check=True, variant="timer")
+    r.phase_cycles(reset=True)
+    out = torch.full((ds.rays, 4), float("nan"), dtype=torch.float32, device="cuda:0")
+    for _ in range(3):
+        r.render(ds, out)
+    ph = r.phase_cycles(reset=True)
+    assert r.launch_shape(ds) == (blocks, stripe)
+    r.close()
+    assert np.array_equal(out.cpu().numpy(), ref)
+    R = 64 // cfg.K
+    say("  ", ph)
+    assert ph["waves"] == 3 * blocks * 4
+    assert ph["tiles"] == 3 * ds.rays // R   # whole tiles: W and H are multiples of the tile's
+    assert all(ph[k] > 0 for k in ("setup", "hash", "mlp", "composite"))
+
+
+def test_default_library_has_no_phase_timer():
+    r = mixrt.Renderer(0)
+    with pytest.raises(mixrt.MixrtError) as e:
+        r.phase_cycles()
+    assert e.value.status == mixrt.MIXRT_EUNSUPPORTED
+    r.close()
+
+
+@pytest.mark.parametrize("cfg", [synth.TINY64_DENSE.replace(name="replay_tiny", H=40, W=56),
+                                 synth.VIEW720P.replace(name="replay_720p_rows", rows=48),
+                                 synth.DEPLOYED720P.replace(name="replay_f4", rows=64)],
+                         ids=lambda c: c.name)
+def test_gather_replay_loads_exactly_the_corner_entries(cfg):
+    from paper_2312_11841_amd import microbench as mb
+    say("gather replay", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    r = mixrt.Renderer(0, sync_check=True)
+    x, hit = r.ray_setup(ds)
+    blocks, stripe = r.launch_shape(ds)
+    r.sync()
+    N = np.ascontiguousarray(mixrt.level_resolutions(ds.grid), np.int32)
+    # the XOR over every lane's fold is the XOR over all loaded words,
+    # whichever lane loaded them
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    for grid in (blocks, 2 * cus):
+        for st in (stripe, 1):
+            res = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N,
+                                   st, [grid], reps=1)
+            assert res["best"]["ms"] > 0
+    sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
+    rc = mb.lib().mixrt_mb_gather_replay(
+        x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table.data_ptr(),
+        cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F, N.ctypes.data,
+        stripe, 0, blocks, sink.data_ptr(), None)
+    assert rc == 0
+    torch.cuda.synchronize()
+    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+    xs = x.cpu().numpy().reshape(-1, cfg.K, 3)[hit.cpu().numpy() != 0].reshape(-1, 3)
+    _, idx, _, _ = oracle.hash_encode(xs, sc.table, cfg.N_min, cfg.N_max)
+    words = sc.table.view(np.uint32).reshape(cfg.L, cfg.T, -1)      # an entry's 32-bit words
+    acc = np.uint32(0)
+    for l in range(cfg.L):
+        w = words[l][idx[:, l, :].reshape(-1)]
+        acc ^= np.bitwise_xor.reduce(w.reshape(-1))
+    assert got == acc
+    r.close()
