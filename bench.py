@@ -106,17 +106,17 @@ def gather_replay_floor(cfg, ds, renderer):
     from paper_2312_11841_amd import microbench as mb
     from paper_2312_11841_amd import mixrt
     x, hit = renderer.ray_setup(ds)
-    blocks, stripe = renderer.launch_shape(ds)
+    blocks, stripe, chunk = renderer.launch_shape(ds, chunk=True)
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     N = mixrt.level_resolutions(ds.grid)
     grids = sorted({blocks} | {k * cus for k in (1, 2, 3, 4, 6, 8)})
     r = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N, stripe,
-                         grids)
+                         grids, chunk=chunk)
     del x, hit
-    return {"render_blocks": blocks, "tile_stripe": stripe, **r}
+    return {"render_blocks": blocks, "tile_stripe": stripe, "early_stop_chunk": chunk, **r}
 
 
-def stage_metrics(cfg, ds, out, steps):
+def stage_metrics(cfg, ds, out, steps, chunk=0):
     """Where the fused kernel's time goes, two ways, both from builds of the
     same render source with one -D option:
       - phase timer: every wave adds the shader clocks of each phase of each
@@ -130,19 +130,20 @@ def stage_metrics(cfg, ds, out, steps):
     from paper_2312_11841_amd import mixrt
     stream = torch.cuda.current_stream()
     res = {}
-    r = mixrt.Renderer(0, stream=stream, variant="timer")
+    r = mixrt.Renderer(0, stream=stream, variant="timer", early_stop_chunk=chunk)
     for _ in range(5):
         r.render(ds, out)
     r.phase_cycles(reset=True)
     timer_ms = time_launches(stream, lambda: r.render(ds, out), steps)
     ph = r.phase_cycles(reset=True)
     r.close()
+    res["samples_evaluated_per_frame"] = ph["samples"] // steps
     tot = sum(ph[k] for k in ("setup", "hash", "mlp", "composite"))
     res["phase_share"] = {k: round(ph[k] / tot, 4) for k in ("setup", "hash", "mlp", "composite")}
     res["timer_build_ms"] = round(timer_ms, 4)
     abl = {}
     for v in ("split_nodisp", "split_nohash", "split_nomlp"):
-        r = mixrt.Renderer(0, stream=stream, variant=v)
+        r = mixrt.Renderer(0, stream=stream, variant=v, early_stop_chunk=chunk)
         for _ in range(5):
             r.render(ds, out)
         abl[v.replace("split_", "without_")] = round(time_launches(stream, lambda: r.render(ds, out),
@@ -157,12 +158,17 @@ def algorithmic_work(cfg):
 
     Per sample: the 8 corner entries of every level (L * 8 * F * element size).
     Per ray: the G-buffer record read (16 B: t, u, v, pad), the 4 bilinear
-    texels (4 * V * element size) and the RGBA written (16 B).
+    taps of the channels the displacement form reads (4 * channels * element
+    size, plus the scale map's 4 taps for Eq. 2 as printed) and the RGBA
+    written (16 B).
     MLP: 2 * sum of in*out over layers per sample."""
     eb = 2 if cfg.table_dtype == "f16" else 4
-    xb = 2 if cfg.tex_dtype == "f16" else 4
+    xb = {"f32": 4, "f16": 2, "u8": 1}[cfg.tex_dtype]
     per_sample_hash = cfg.L * 8 * cfg.F * eb
-    per_ray = 16 + 4 * cfg.tex_V * xb + 16
+    # the 4 bilinear taps of the channels the displacement form reads (Eq. 2
+    # as printed also reads the scale map's 4 taps)
+    tex = 4 * cfg.tex_channels * xb + (4 * xb if cfg.disp == "vec3" else 0)
+    per_ray = 16 + tex + 16
     flops_per_sample = 2 * sum(a * b for a, b in zip(cfg.widths[:-1], cfg.widths[1:]))
     return {
         "hash_bytes": cfg.samples * per_sample_hash,
@@ -389,6 +395,9 @@ def main():
                     help="time the paper's Tab. 3 / Tab. 6 profiling points instead")
     ap.add_argument("--no-rooflines", action="store_true",
                     help="skip the microbenchmark rooflines and the standalone MLP leg")
+    ap.add_argument("--early-stop-chunk", type=int, default=0, metavar="C",
+                    help="render in front-to-back rounds of C samples per ray, dropping rays "
+                         "once opaque (0: the library's default, the tile path)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes per step (the "
                          "reference kernel that scales the FETCH_SIZE / WRITE_SIZE counters)")
@@ -426,7 +435,7 @@ def main():
     ds = mixrt.DeviceScene.from_scene(scene, "cuda:0")
     out = torch.empty((cfg.rays, 4), dtype=torch.float32, device="cuda:0")
     stream = torch.cuda.current_stream()
-    r = mixrt.Renderer(0, stream=stream)
+    r = mixrt.Renderer(0, stream=stream, early_stop_chunk=args.early_stop_chunk)
     mesh = None
     if scene.mesh is not None:
         # load time, outside the timed region: grid build on the host + upload
@@ -465,8 +474,9 @@ def main():
         extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
         extra["rooflines_measured"] = measured_rooflines(cfg)
         replay = gather_replay_floor(cfg, ds, r)
-        stages = stage_metrics(cfg, ds, out, max(args.steps, 20))
+        stages = stage_metrics(cfg, ds, out, max(args.steps, 20), args.early_stop_chunk)
 
+    launch = r.launch_shape(ds, chunk=True)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -504,6 +514,14 @@ def main():
     r.close()
 
     work = algorithmic_work(cfg)
+    if stages is not None and stages["samples_evaluated_per_frame"] != cfg.samples:
+        # misses and rays stopped early evaluate no samples: the work the
+        # frame actually has is that of the samples evaluated (counted by
+        # the phase-timer build)
+        ev = stages["samples_evaluated_per_frame"]
+        work["hash_bytes"] = ev * work["per_sample_hash_bytes"]
+        work["mlp_flops"] = ev * work["flops_per_sample"]
+        work["samples_evaluated"] = ev
     traffic, traffic_src = measured_traffic(cfg.name)
     sec = ms * 1e-3
     rsec = render_ms * 1e-3
@@ -531,6 +549,11 @@ def main():
                            "alone (mixrt_mb_gather_replay, fastest grid size); the counters "
                            "show the vector L1 as the saturated unit",
             "gather_replay": {"ms": round(rms, 4), "frac": round(rms / render_ms, 4),
+                              "early_stop_chunk": replay["early_stop_chunk"],
+                              "note": "the render's own order (tile path, or its rounds of "
+                                      "early_stop_chunk samples per ray); rounds are replayed as "
+                                      "they run when no ray stops, so where rays stop the render "
+                                      "gathers fewer samples than the replay",
                               "address_only_ms": round(replay["best"]["address_only_ms"], 4),
                               "blocks": replay["best"]["blocks"],
                               "render_blocks": replay["render_blocks"],
@@ -542,6 +565,7 @@ def main():
             "algorithmic_bytes_per_launch": total_bytes,
             "algorithmic_bytes_per_unit": {"sample": work["per_sample_hash_bytes"],
                                            "ray": work["per_ray_bytes"]},
+            "samples_per_launch": work.get("samples_evaluated", cfg.samples),
         }
     else:
         roofline = {
@@ -602,6 +626,7 @@ def main():
             "rays": cfg.rays,
             "samples": cfg.samples,
             "parallelism": "single GPU",
+            "launch": dict(zip(("blocks", "tile_stripe", "early_stop_chunk"), launch)),
         },
         "roofline": roofline,
         **stage_fields,

@@ -93,6 +93,19 @@ typedef struct {
                             > 0 vertical stripes of that many tiles, each
                             stripe row by row (compact blocks of pixels per
                             XCD), < 0 plain row-major order */
+    int32_t early_stop_chunk; /* how mixrt_render evaluates a ray's samples
+                            (speed only, never a result): > 0 front to back in
+                            rounds of that many samples per ray (rounded down
+                            to a power of two, at most K), a ray stopping once
+                            its transmittance is below t_term; the rays still
+                            running are packed into each round, so a stopped
+                            ray costs no further gathers or MFMA work.  < 0
+                            all K samples of a ray at once (the tile path).
+                            0 the library's choice: the tile path for K < 4, K
+                            not a power of two, or coherent samples on levels
+                            larger than one XCD's L2; otherwise rounds of 4, 2
+                            or 1 as a ray's samples share the voxels of at
+                            least half, a quarter or fewer of the levels */
 } mixrt_create_info;
 
 /* The coarse-mesh hit per pixel (Fig. 2 step 1): rasterisation output. */
@@ -213,14 +226,16 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
                  const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
                  const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
 
-/* The persistent grid (blocks of 256 threads) and the tile-order stripe
- * width (tiles; the image's tile columns for row-major order) that
- * mixrt_render would launch for these descriptors on this context; nothing
- * is enqueued.  blocks, tile_stripe: host int32. */
+/* The persistent grid (blocks of 256 threads), the tile-order stripe width
+ * (tiles; the image's tile columns for row-major order) and the samples per
+ * ray per round (0: all K at once) that mixrt_render would launch for these
+ * descriptors on this context; nothing is enqueued.  blocks, tile_stripe,
+ * chunk: host int32. */
 int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
                               const mixrt_camera *cams, const mixrt_disp_tex *disp,
                               const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
-                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe);
+                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe,
+                              int32_t *chunk);
 
 /* ---- stage entry points (the same device code as mixrt_render) ------------ */
 
@@ -230,7 +245,9 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
  * tile to device counters.  Waits for the device, then writes out (host
  * uint64[8]): [0] setup (ray, G-buffer, Eq. 2, samples, contraction),
  * [1] hash encoding, [2] MLP (with the view encoding), [3] compositing and
- * store, summed over waves; [4] tiles; [5] waves; [6], [7] zero.  reset != 0
+ * store, summed over waves; [4] tiles; [5] waves; [6] samples run through
+ * the hash encoding and MLP (a hit ray's samples, and with early_stop_chunk
+ * only those of rays still running); [7] zero.  reset != 0
  * zeroes the counters after reading.  MIXRT_EUNSUPPORTED in other builds. */
 int mixrt_debug_phase_cycles(mixrt_ctx *ctx, uint64_t *out, int reset);
 

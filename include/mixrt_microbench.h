@@ -49,12 +49,18 @@ int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
  * same loads of `entry_bytes`-byte entries (4, 8 or 16) from `table`
  * (device [L][2^log2_T] entries, 16-byte aligned) in the same batches,
  * keeping only an XOR of the loaded words (mode 0).  Mode 1 issues no loads
- * (address arithmetic alone).  N: host int32 [L], the level resolutions
- * (non-decreasing).  sink: device uint32 [blocks*256] (written). */
+ * (address arithmetic alone).  chunk: 0 replays the tile path (a tile's
+ * K samples of R = 64/K rays per step); > 0 (a power of two dividing 64, at
+ * most K) replays the early-termination path with rounds of chunk samples
+ * as it runs when every ray hits and none stops (runs of K/chunk tiles per
+ * wave, lane s*chunk + j on sample c*chunk + j of the run's ray s in round
+ * c).  N: host int32 [L], the level resolutions (non-decreasing).  sink:
+ * device uint32 [blocks*256] (written). */
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
-                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream);
+                           int32_t chunk, int32_t mode, int32_t blocks, uint32_t *sink,
+                           void *stream);
 
 /* Properties of HIP device `device` the measurements are quoted against:
  * peak shader clock (kHz), memory clock (kHz), compute units, L2 bytes, and

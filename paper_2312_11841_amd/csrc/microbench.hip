@@ -215,7 +215,7 @@ __device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, in
 template <uint32_t EB, int MODE>
 __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict__ x,
                                                         const int32_t *__restrict__ hit, int views,
-                                                        int W, int H, int K, int stripe,
+                                                        int W, int H, int K, int stripe, int C,
                                                         mixrt::GridParams gp,
                                                         uint32_t *__restrict__ sink)
 {
@@ -226,11 +226,24 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
     const mixrt::TileShape ts = mixrt::tile_shape(R, views, W, H, stripe);
     const int gw = mixrt::xcd_logical_block(blockIdx.x, gridDim.x) * 4 + wv;
     const int total = gridDim.x * 4;
-    const int r_loc = lane / K, k = lane - r_loc * K;
     const int L = gp.L, n_dense = gp.n_dense;
+    // C = 0: one tile per step, lane r K + k on sample k of ray r (the tile
+    // path).  C > 0: the early-termination path's order when no ray stops
+    // and every ray hits: runs of B = K/C tiles, one round per C samples,
+    // lane s C + j on sample c C + j of the run's ray s.
+    const int B = C > 0 && K / C > 1 ? K / C : 1;
+    const int rounds = C > 0 ? (K + C - 1) / C : 1;
+    const int Cl = C > 0 ? C : K;
+    const int sl = lane / Cl, j = lane - sl * Cl;
+    const int t_in_run = C > 0 ? sl / R : 0, r_loc = C > 0 ? sl - t_in_run * R : lane / K;
     uint32_t acc = 0;
-    for (int tile = gw; tile < ts.n_tiles; tile += total) {
-        const mixrt::TilePos tp = mixrt::tile_at(ts, tile);
+    for (int64_t run = gw; run * B < ts.n_tiles; run += total)
+    for (int c = 0; c < rounds; ++c) {
+        const int64_t tile64 = run * B + t_in_run;
+        const int k = C > 0 ? c * C + j : lane - r_loc * K;
+        if (t_in_run >= B || tile64 >= ts.n_tiles || k >= K || lane >= (C > 0 ? 64 : R * K))
+            continue;
+        const mixrt::TilePos tp = mixrt::tile_at(ts, (int)tile64);
         const int i0 = tp.tx * ts.RW, j0 = tp.ty * ts.RH;
         const int dy = r_loc / ts.RW, dx = r_loc - dy * ts.RW;
         const bool valid = r_loc < R && i0 + dx < W && j0 + dy < H;
@@ -259,9 +272,12 @@ extern "C" {
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
-                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream)
+                           int32_t chunk, int32_t mode, int32_t blocks, uint32_t *sink,
+                           void *stream)
 {
     if (!x || !hit || !table || !N || !sink) return hipErrorInvalidValue;
+    if (chunk < 0 || chunk > K || (chunk > 0 && (64 % chunk != 0 || (chunk & (chunk - 1)))))
+        return hipErrorInvalidValue;
     if (views < 1 || W < 1 || H < 1 || (int64_t)views * H * W >= ((int64_t)1 << 31))
         return hipErrorInvalidValue;
     if (K < 1 || K > 64 || L < 1 || L > mixrt::kMaxLevels || log2_T < 4 || log2_T > 26)
@@ -290,7 +306,7 @@ int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, in
     hipStream_t s = (hipStream_t)stream;
 #define RP(EB, M)                                                                                \
     hipLaunchKernelGGL((replay_kernel<EB, M>), dim3(blocks), dim3(kBlock), 0, s, x, hit, views, \
-                       W, H, K, tile_stripe, gp, sink)
+                       W, H, K, tile_stripe, chunk, gp, sink)
     if (mode == 0) {
         if (entry_bytes == 4) RP(4, 0);
         else if (entry_bytes == 8) RP(8, 0);

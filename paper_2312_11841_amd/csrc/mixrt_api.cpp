@@ -24,6 +24,7 @@ struct mixrt_ctx {
     hipStream_t stream = nullptr;
     uint32_t flags = 0;
     int32_t tile_stripe = 0;
+    int32_t early_stop_chunk = 0;
     int cus = 0;
     int64_t l2_bytes = 0;
     std::string err;
@@ -609,6 +610,7 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     ctx->stream = (hipStream_t)ci->hip_stream;
     ctx->flags = ci->flags;
     ctx->tile_stripe = ci->tile_stripe;
+    ctx->early_stop_chunk = ci->early_stop_chunk;
     ctx->cus = prop.multiProcessorCount;
     ctx->l2_bytes = prop.l2CacheSize;
     *out = ctx;
@@ -657,6 +659,7 @@ void fill_render_launch(mixrt::RenderLaunch &L, const mixrt_ctx *ctx, const mixr
     L.l2_bytes = ctx->l2_bytes;
     L.blocks_mode = (ctx->flags & MIXRT_FLAG_BLOCKS_FULL) ? 1 : (ctx->flags & MIXRT_FLAG_BLOCKS_TWO) ? 2 : 0;
     L.tile_stripe = ctx->tile_stripe;
+    L.chunk = ctx->early_stop_chunk;
 }
 
 }  // namespace
@@ -682,7 +685,8 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
 int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
                               const mixrt_camera *cams, const mixrt_disp_tex *disp,
                               const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
-                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe)
+                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe,
+                              int32_t *chunk)
 {
     if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
     clear_err(ctx);
@@ -690,16 +694,18 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
     int hid = 0, nhid = 0;
     int rc = validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, sizeof msg}, &hid, &nhid);
     if (rc) return fail(ctx, rc, "%s", msg);
-    if (!blocks || !tile_stripe) return fail(ctx, MIXRT_EINVAL, "blocks or tile_stripe is NULL");
+    if (!blocks || !tile_stripe || !chunk)
+        return fail(ctx, MIXRT_EINVAL, "blocks, tile_stripe or chunk is NULL");
     if ((rc = bind_device(ctx))) return rc;
     mixrt::RenderLaunch L;
     fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, nullptr);
-    int b = 0, st = 0;
-    const hipError_t e = mixrt::render_launch_shape(L, &b, &st);
+    int b = 0, st = 0, ch = 0;
+    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch);
     if (e != hipSuccess)
         return fail(ctx, MIXRT_EDEVICE, "render launch shape: %s", hipGetErrorString(e));
     *blocks = b;
     *tile_stripe = st;
+    *chunk = ch;
     return MIXRT_OK;
 }
 

@@ -361,26 +361,57 @@ __device__ __forceinline__ bool ray8_applies(const RayParams &p)
            (p.K & 7) == 0 && 64 % p.K == 0;
 }
 
+// A hit ray's calibrated frame: P = o + (p_cali - p), so that sample k sits
+// at P + (t + (k - (K-1)/2) delta) d.
+struct RayHit {
+    float px, py, pz;
+    float t;
+};
+
+// Hit test and Eq. 2 calibration of a ray (sub: the lane's index within its
+// ray's 8-lane group when displacement_ray8 serves the call).  Returns false
+// for a miss.
+template <typename TK>
+__device__ __forceinline__ bool ray_hit(const RayParams &p, const Ray &r, float4 g, int sub,
+                                        RayHit &h)
+{
+    h.t = g.x;
+    const bool hit = h.t > 0.0f && h.t < INFINITY;
+    if (!hit) {
+        h.px = h.py = h.pz = 0.0f;
+        return false;
+    }
+    float ox, oy, oz;
+    if (ray8_applies<TK>(p))
+        displacement_ray8<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, sub & 7, ox, oy, oz);
+    else
+        displacement<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, ox, oy, oz);
+    h.px = r.ox + ox;
+    h.py = r.oy + oy;
+    h.pz = r.oz + oz;
+    return true;
+}
+
+// Sample k of a hit ray: placement along d, contraction, cube map.
+__device__ __forceinline__ void sample_at(const RayParams &p, const RayHit &h, float dx, float dy,
+                                          float dz, int k, float &x0, float &x1, float &x2)
+{
+    const float off = h.t + ((float)k - 0.5f * (float)(p.K - 1)) * p.delta;
+    contract_to_cube(h.px + off * dx, h.py + off * dy, h.pz + off * dz, x0, x1, x2);
+}
+
 // Steps before the grid for sample k of a ray: hit test, Eq. 2 calibration,
 // sample placement, contraction.  Returns false for a miss.
 template <typename TK>
 __device__ __forceinline__ bool sample_position(const RayParams &p, const Ray &r, float4 g, int k,
                                                 float &x0, float &x1, float &x2)
 {
-    const float t = g.x;
-    const bool hit = t > 0.0f && t < INFINITY;
-    if (!hit) {
+    RayHit h;
+    if (!ray_hit<TK>(p, r, g, k, h)) {
         x0 = x1 = x2 = 0.0f;
         return false;
     }
-    float ox, oy, oz;
-    if (ray8_applies<TK>(p))
-        displacement_ray8<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, k & 7, ox, oy, oz);
-    else
-        displacement<TK>(p, g.y, g.z, r.dx, r.dy, r.dz, ox, oy, oz);
-    const float off = t + ((float)k - 0.5f * (float)(p.K - 1)) * p.delta;
-    contract_to_cube(r.ox + ox + off * r.dx, r.oy + oy + off * r.dy, r.oz + oz + off * r.dz, x0,
-                     x1, x2);
+    sample_at(p, h, r.dx, r.dy, r.dz, k, x0, x1, x2);
     return true;
 }
 

@@ -56,7 +56,7 @@ class MixrtError(RuntimeError):
 
 class CreateInfo(C.Structure):
     _fields_ = [("device", C.c_int32), ("hip_stream", C.c_void_p), ("flags", C.c_uint32),
-                ("tile_stripe", C.c_int32)]
+                ("tile_stripe", C.c_int32), ("early_stop_chunk", C.c_int32)]
 
 
 class GBuffer(C.Structure):
@@ -135,7 +135,8 @@ def lib(variant=None):
             "mixrt_render_launch_shape": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                     C.POINTER(DispTex), C.POINTER(HashGrid),
                                                     C.POINTER(Mlp), C.POINTER(Sampling),
-                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
+                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int32),
+                                                    C.POINTER(C.c_int32)]),
             "mixrt_debug_phase_cycles": (C.c_int, [P, P, C.c_int]),
             "mixrt_debug_ray_setup": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                 C.POINTER(DispTex), C.POINTER(Sampling), P, P]),
@@ -396,11 +397,14 @@ class Renderer:
     """One mixrt context bound to a device and a HIP stream."""
 
     def __init__(self, device: int = 0, stream=None, sync_check: bool = False, blocks=None,
-                 tile_stripe: int = 0, variant=None):
+                 tile_stripe: int = 0, early_stop_chunk: int = 0, variant=None):
         """blocks: None (the library's choice), "full" or "two": the render
         kernel's persistent blocks per CU; tile_stripe: 0 (the library's
         choice), > 0 stripes of that many tiles, < 0 row-major (the order in
-        which waves take tiles).  Both change speed only, never a result.
+        which waves take tiles); early_stop_chunk: 0 (the library's choice),
+        < 0 every sample of a ray at once (the tile path), > 0 front to back
+        in rounds of that many samples with stopped rays dropped.  They
+        change speed only, never a result.
         variant: None (libmixrt.so) or a profiling build (see lib())."""
         import torch
         self.device = device
@@ -409,7 +413,7 @@ class Renderer:
         self.stream = stream
         ci = CreateInfo(device, C.c_void_p(int(stream.cuda_stream)),
                         (MIXRT_FLAG_SYNC_CHECK if sync_check else 0) | _BLOCKS[blocks],
-                        int(tile_stripe))
+                        int(tile_stripe), int(early_stop_chunk))
         self._L = lib(variant)
         h = C.c_void_p()
         rc = self._L.mixrt_create(C.byref(h), C.byref(ci))
@@ -451,19 +455,20 @@ class Renderer:
     def phase_cycles(self, reset: bool = False):
         """The phase-timer build's counters (see mixrt_debug_phase_cycles):
         {"setup", "hash", "mlp", "composite": shader clocks summed over
-        waves, "tiles", "waves"}."""
+        waves, "tiles", "waves", "samples": samples evaluated}."""
         out = (C.c_uint64 * 8)()
         self._check(self._L.mixrt_debug_phase_cycles(self._h, out, int(reset)))
-        names = ("setup", "hash", "mlp", "composite", "tiles", "waves")
+        names = ("setup", "hash", "mlp", "composite", "tiles", "waves", "samples")
         return {n: int(out[i]) for i, n in enumerate(names)}
 
-    def launch_shape(self, ds: DeviceScene):
-        """(blocks, tile stripe) that render(ds) launches."""
-        b, st = C.c_int32(), C.c_int32()
+    def launch_shape(self, ds: DeviceScene, chunk: bool = False):
+        """(blocks, tile stripe) that render(ds) launches, and with chunk=True
+        also its samples per ray per round (0: the tile path)."""
+        b, st, ch = C.c_int32(), C.c_int32(), C.c_int32()
         self._check(self._L.mixrt_render_launch_shape(
             self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp), C.byref(ds.grid),
-            C.byref(ds.mlp), C.byref(ds.smp), C.byref(b), C.byref(st)))
-        return b.value, st.value
+            C.byref(ds.mlp), C.byref(ds.smp), C.byref(b), C.byref(st), C.byref(ch)))
+        return (b.value, st.value, ch.value) if chunk else (b.value, st.value)
 
     # -- geometry
     def raycast(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):

@@ -1,9 +1,13 @@
 """GPU checks of what changes the render kernel's speed but never its result:
-the tile order (stripes of tiles per XCD), the profiling builds that time
-the kernel's phases, and the gather-replay microbenchmark that measures the
-floor of its gather stream.
+the tile order (stripes of tiles per XCD), the early-termination path (rays
+evaluated front to back in rounds, stopped rays dropped), the profiling
+builds that time the kernel's phases, and the gather-replay microbenchmark
+that measures the floor of its gather stream.
 
   - every tile order renders the same frame bit for bit, and every pixel;
+  - the early-termination path renders the tile path's frame bit for bit
+    (the same samples composited in the same order), at every round size,
+    and evaluates fewer samples on opaque content;
   - the phase-timer build renders the same frame as the library, and its
     counters cover every tile of every launch;
   - the replay loads exactly the table entries of the oracle's corner
@@ -124,14 +128,6 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
             res = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N,
                                    st, [grid], reps=1)
             assert res["best"]["ms"] > 0
-    sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
-    rc = mb.lib().mixrt_mb_gather_replay(
-        x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table.data_ptr(),
-        cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F, N.ctypes.data,
-        stripe, 0, blocks, sink.data_ptr(), None)
-    assert rc == 0
-    torch.cuda.synchronize()
-    got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
     xs = x.cpu().numpy().reshape(-1, cfg.K, 3)[hit.cpu().numpy() != 0].reshape(-1, 3)
     _, idx, _, _ = oracle.hash_encode(xs, sc.table, cfg.N_min, cfg.N_max)
     words = sc.table.view(np.uint32).reshape(cfg.L, cfg.T, -1)      # an entry's 32-bit words
@@ -139,5 +135,99 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
     for l in range(cfg.L):
         w = words[l][idx[:, l, :].reshape(-1)]
         acc ^= np.bitwise_xor.reduce(w.reshape(-1))
-    assert got == acc
+    # the tile path's order and every rounds order the render can take
+    for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
+        sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
+        rc = mb.lib().mixrt_mb_gather_replay(
+            x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K,
+            ds.table.data_ptr(), cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F,
+            N.ctypes.data, stripe, chunk, 0, blocks, sink.data_ptr(), None)
+        assert rc == 0
+        torch.cuda.synchronize()
+        got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+        assert got == acc, chunk
     r.close()
+
+
+@pytest.mark.parametrize("cfg", [synth.VIEW720P, synth.VIEW720P_DENSE,
+                                 synth.VIEW720P_DENSE.replace(name="d05", delta=0.05),
+                                 synth.VIEW720P.replace(name="k2", K=2),
+                                 synth.VIEW720P.replace(name="k3", K=3),
+                                 synth.BATCH8X1080P, synth.PAPER720P],
+                         ids=lambda c: c.name)
+def test_default_round_size_follows_the_rule(cfg):
+    """The library's default samples per round (0 = the tile path): 4 when a
+    ray's samples share the voxels of half the levels and a level fits one
+    XCD's L2, 2 or 1 as they share fewer, the tile path for K < 4 or K not a
+    power of two and for coherent samples on levels larger than the L2."""
+    want = {"view720p": 4, "view720p_dense": 1, "d05": 2, "k2": 0, "k3": 0,
+            "batch8x1080p": 0, "paper720p": 0}[cfg.name]
+    sc = synth.make_scene(cfg.replace(H=16, W=64, views=1))
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    r = mixrt.Renderer(0)
+    assert r.launch_shape(ds, chunk=True)[2] == want
+    r.close()
+
+
+QUEUE_CFGS = [
+    synth.TINY64_DENSE.replace(name="q_tiny_dense", t_term=1e-2),
+    synth.TINY64_DENSE.replace(name="q_ragged_k3", H=23, W=37, views=2, K=3, gbuf="iid",
+                               t_term=1e-2),
+    synth.TINY64_DENSE.replace(name="q_ragged_k7", H=19, W=21, views=3, K=7, gbuf="iid",
+                               t_term=1e-3),
+    synth.TINY64_DENSE.replace(name="q_k64", H=9, W=11, K=64, gbuf="iid", t_term=0.0),
+    synth.TINY64_DENSE.replace(name="q_k1", H=33, W=31, views=2, K=1, gbuf="iid"),
+    synth.TINY64_DENSE.replace(name="q_nomlp", widths=(16,), seed=16, t_term=1e-2),
+    synth.TINY64_VEC3, synth.TINY64_U8,
+    synth.OPAQUE720P, synth.TRANSLUCENT720P, synth.VIEW720P_DENSE, synth.PAPER720P,
+]
+
+
+@pytest.mark.parametrize("cfg", QUEUE_CFGS, ids=lambda c: c.name)
+def test_early_termination_path_renders_the_same_frame(cfg):
+    """Every round size renders the tile path's frame bit for bit, misses
+    included (5% of each kind on the small workloads)."""
+    say("early termination", cfg.name)
+    sc = synth.make_scene(cfg)
+    if cfg.rays < 20000:
+        flat = sc.g0.reshape(-1, 4)
+        rng = np.random.default_rng(cfg.seed)
+        miss = rng.choice(flat.shape[0], flat.shape[0] // 20, replace=False)
+        flat[miss, 0] = rng.choice([0.0, -1.0, np.nan, np.inf], miss.size)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    ref, _ = _render(ds, early_stop_chunk=-1)
+    assert np.all(np.isfinite(ref))
+    for chunk in (1, 2, 4, 8, 64):
+        got, _ = _render(ds, early_stop_chunk=chunk)
+        assert np.array_equal(got, ref), chunk
+    got, _ = _render(ds, early_stop_chunk=2, tile_stripe=-1, blocks="two")
+    assert np.array_equal(got, ref)
+
+
+@pytest.mark.parametrize("cfg", [synth.OPAQUE720P, synth.TRANSLUCENT720P],
+                         ids=lambda c: c.name)
+def test_early_termination_against_the_oracle(cfg):
+    """The frame within 2e-3 + t_term of the oracle (which never stops a
+    ray) on sampled pixels, and fewer samples evaluated than the tile path
+    (counted by the phase-timer build)."""
+    say("early termination vs oracle", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    got, _ = _render(ds, early_stop_chunk=1)
+    rng = np.random.default_rng(9)
+    pix = np.unique(np.concatenate([rng.choice(cfg.rays, 3000, replace=False),
+                                    np.arange(cfg.W)]))
+    ref = oracle.OracleScene(sc).render_pixels(pix, threads=oracle.max_threads())
+    err = np.abs(got[pix] - ref).max()
+    say(f"  max |gpu - oracle| = {err:.3e}")
+    assert err <= 2e-3 + cfg.t_term
+    counts = {}
+    for chunk in (-1, 1, 2, 4):
+        r = mixrt.Renderer(0, sync_check=True, variant="timer", early_stop_chunk=chunk)
+        r.phase_cycles(reset=True)
+        r.render(ds)
+        counts[chunk] = r.phase_cycles(reset=True)["samples"]
+        r.close()
+    say("  samples evaluated by round size:", counts)
+    assert counts[-1] == cfg.rays * cfg.K            # every pixel hits
+    assert counts[1] < counts[2] <= counts[4] < counts[-1]

@@ -305,7 +305,26 @@ def test_frame_is_deterministic(R):
     assert torch.equal(a, b)
 
 
-def test_large_batch_one_view_sampled(R):
+@pytest.mark.parametrize("cfg", [synth.VIEW720P_DENSE, synth.PAPER720P], ids=lambda c: c.name)
+def test_full_frame_every_pixel(R, cfg):
+    """Every pixel of a 1280x720 frame, in the launch the benchmark times,
+    against the oracle (OpenMP over pixels; about half a minute for K = 8)."""
+    say("full frame", cfg.name, cfg.rays)
+    sc, ds = scene_of(cfg)
+    out = R.render(ds)
+    R.sync()
+    got = out.cpu().numpy()
+    ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays), threads=oracle.max_threads())
+    err = np.abs(got - ref)
+    say(f"  max |gpu - oracle| = {err.max():.3e}, mean {err.mean():.3e}, "
+        f"pixels above 1e-4: {(err.max(axis=1) > 1e-4).sum()}")
+    assert err.max() <= FRAME_TOL
+    assert np.all(np.isfinite(got))
+
+
+def test_large_batch_whole_view(R):
+    """The 8-view 1920x1080 batch in one launch: every pixel of one whole
+    view, plus samples of the other seven and the view boundaries."""
     cfg = synth.BATCH8X1080P
     say("frame", cfg.name)
     sc = synth.make_scene(cfg)
@@ -316,12 +335,15 @@ def test_large_batch_one_view_sampled(R):
     rng = np.random.default_rng(5)
     view = 5
     hw = cfg.H * cfg.W
-    pix = view * hw + rng.choice(hw, 1500, replace=False)
-    pix = np.concatenate([pix, [0, cfg.rays - 1, hw - 1, hw]])   # view boundaries
+    others = rng.choice(cfg.rays - hw, 2000, replace=False)
+    others[others >= view * hw] += hw
+    pix = np.concatenate([np.arange(view * hw, (view + 1) * hw), others,
+                          [0, cfg.rays - 1, hw - 1, hw]])   # view boundaries
     ref = oracle.OracleScene(sc).render_pixels(pix, threads=oracle.max_threads())
     err = np.abs(got[pix] - ref).max()
-    say(f"  max |gpu - oracle| = {err:.3e}")
+    say(f"  max |gpu - oracle| = {err:.3e} over {pix.size} px")
     assert err <= FRAME_TOL
+    assert np.all(np.isfinite(got))
     del ds
 
 
