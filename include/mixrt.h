@@ -173,7 +173,9 @@ typedef struct {
                             to output i mod 4, width[0] a multiple of 4,
                             view_sh_dim 0, data unused */
     int32_t width[MIXRT_MAX_LAYERS + 1]; /* width[0] = L*F + view_sh_dim,
-                            hidden widths equal (16, 32 or 64), last = 4 */
+                            hidden widths equal (8, 16, 32 or 64; 8 runs on
+                            the 16-wide MFMA tile with zero padding, which
+                            computes the 8-wide network exactly), last = 4 */
     int32_t view_sh_dim; /* 0 or 16 */
     const uint16_t *data;/* device fp16 weights, layer m row-major
                             [width[m]][width[m+1]], layers concatenated;

@@ -176,7 +176,9 @@ int check_grid(const mixrt_hash_grid *g, Msg m)
     return MIXRT_OK;
 }
 
-// hidden width and hidden-layer count of a valid MLP
+// hidden width of the kernel (an 8-wide hidden layer runs on the 16-wide
+// tile, zero-padded as its weights are loaded) and hidden-layer count of a
+// valid MLP
 int check_mlp(const mixrt_mlp *p, int expect_in, Msg m, int *hid, int *nhid)
 {
     if (!p) return vfail(m, MIXRT_EINVAL, "mlp is NULL");
@@ -207,15 +209,16 @@ int check_mlp(const mixrt_mlp *p, int expect_in, Msg m, int *hid, int *nhid)
     for (int i = 1; i < p->n_layers; ++i)
         if (p->width[i] != h)
             return vfail(m, MIXRT_EUNSUPPORTED, "mlp hidden widths differ (%d vs %d)", p->width[i], h);
-    if (p->width[0] % 16 || (h != 16 && h != 32 && h != 64))
-        return vfail(m, MIXRT_EUNSUPPORTED, "mlp widths in=%d hidden=%d (in %%16, hidden 16/32/64)",
-                     p->width[0], h);
-    if (!mixrt::mlp_variant_supported(p->width[0], h, p->n_layers - 1))
+    if (p->width[0] % 16 || (h != 8 && h != 16 && h != 32 && h != 64))
+        return vfail(m, MIXRT_EUNSUPPORTED,
+                     "mlp widths in=%d hidden=%d (in %%16, hidden 8/16/32/64)", p->width[0], h);
+    const int hk = h < 16 ? 16 : h;
+    if (!mixrt::mlp_variant_supported(p->width[0], hk, p->n_layers - 1))
         return vfail(m, MIXRT_EUNSUPPORTED, "mlp %d->%dx%d->4 not built", p->width[0], h,
                      p->n_layers - 1);
     if (!p->data) return vfail(m, MIXRT_EINVAL, "mlp.data is NULL");
     if (!aligned16(p->data)) return vfail(m, MIXRT_EINVAL, "mlp.data not 16-byte aligned");
-    *hid = h;
+    *hid = hk;
     *nhid = p->n_layers - 1;
     return MIXRT_OK;
 }
@@ -232,6 +235,24 @@ int check_sampling(const mixrt_sampling *s, Msg m)
     return MIXRT_OK;
 }
 
+// The render kernel's texture kind: the kind specialised for the map's
+// dtype and SH degree when a kernel is built for it with this grid and MLP,
+// else (Eq. 2 as printed) the kind that takes the degree at run time.
+int render_tex(const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+               int hid, int nhid)
+{
+    const bool tf16 = grid->dtype == MIXRT_F16;
+    const int t = mixrt::tex_id(disp->dtype, disp->mode, disp->sh_degree);
+    if (t >= 0 && mixrt::render_variant_supported(t, grid->F, tf16, mlp->width[0], hid, nhid))
+        return t;
+    if (disp->mode == MIXRT_DISP_SH_VEC3) {
+        const int g = mixrt::tex_id_any_degree(disp->dtype);
+        if (mixrt::render_variant_supported(g, grid->F, tf16, mlp->width[0], hid, nhid))
+            return g;
+    }
+    return t;
+}
+
 int validate_all(const mixrt_gbuffer *gbuf, const mixrt_camera *cams, const mixrt_disp_tex *disp,
                  const mixrt_hash_grid *grid, const mixrt_mlp *mlp, const mixrt_sampling *smp,
                  Msg m, int *hid, int *nhid)
@@ -243,7 +264,7 @@ int validate_all(const mixrt_gbuffer *gbuf, const mixrt_camera *cams, const mixr
     if ((rc = check_sampling(smp, m))) return rc;
     if (!mlp) return vfail(m, MIXRT_EINVAL, "mlp is NULL");
     if ((rc = check_mlp(mlp, grid->L * grid->F + mlp->view_sh_dim, m, hid, nhid))) return rc;
-    const int tex = mixrt::tex_id(disp->dtype, disp->mode, disp->sh_degree);
+    const int tex = render_tex(disp, grid, mlp, *hid, *nhid);
     if (!mixrt::render_variant_supported(tex, grid->F, grid->dtype == MIXRT_F16, mlp->width[0],
                                          *hid, *nhid))
         return vfail(m, MIXRT_EUNSUPPORTED,
@@ -285,6 +306,7 @@ void fill_ray_params(mixrt::RayParams &rp, const mixrt_gbuffer *g, const mixrt_c
     rp.tex_R = none ? 1 : d->R;
     rp.tex_V = d->mode == MIXRT_DISP_ALONG_RAY ? d->V : 0;
     rp.tex_C = none ? 1 : stored_channels(d);
+    rp.tex_degree = d->mode == MIXRT_DISP_SH_VEC3 ? d->sh_degree : 0;
     for (int i = 0; i < 2; ++i) {
         rp.q_scale[i] = d->q_scale[i];
         rp.q_offset[i] = d->q_offset[i];
@@ -649,12 +671,13 @@ void fill_render_launch(mixrt::RenderLaunch &L, const mixrt_ctx *ctx, const mixr
     L.weights = (const _Float16 *)mlp->data;
     L.out = (float4 *)out_rgba;
     L.view_sh = mlp->view_sh_dim;
-    L.tex = mixrt::tex_id(disp->dtype, disp->mode, disp->sh_degree);
+    L.tex = render_tex(disp, grid, mlp, hid, nhid);
     L.tf16 = grid->dtype == MIXRT_F16;
     L.F = grid->F;
     L.in = mlp->width[0];
     L.hid = hid;
     L.nhid = nhid;
+    L.hid_w = nhid > 0 ? mlp->width[1] : 0;
     L.cus = ctx->cus;
     L.l2_bytes = ctx->l2_bytes;
     L.blocks_mode = (ctx->flags & MIXRT_FLAG_BLOCKS_FULL) ? 1 : (ctx->flags & MIXRT_FLAG_BLOCKS_TWO) ? 2 : 0;
@@ -781,9 +804,10 @@ int mixrt_debug_mlp(mixrt_ctx *ctx, const mixrt_mlp *mlp, const uint16_t *in_f16
         return fail(ctx, MIXRT_EINVAL, "in_f16/out4 not 16-byte aligned");
     if ((rc = bind_device(ctx))) return rc;
     return finish_launch(ctx,
-                         mixrt::launch_mlp(mlp->width[0], hid, nhid, (const _Float16 *)mlp->data,
-                                           (const _Float16 *)in_f16, n, (float4 *)out4,
-                                           ctx->cus, ctx->stream),
+                         mixrt::launch_mlp(mlp->width[0], hid, nhid,
+                                           nhid > 0 ? mlp->width[1] : 0,
+                                           (const _Float16 *)mlp->data, (const _Float16 *)in_f16,
+                                           n, (float4 *)out4, ctx->cus, ctx->stream),
                          "mlp");
 }
 

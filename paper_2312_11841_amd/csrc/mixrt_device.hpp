@@ -43,6 +43,7 @@ struct RayParams {
     const void *tex;        // displacement coefficients [R][R][C]
     const void *tex_scale;  // Eq. 2 scale map [R][R] (SH_VEC3)
     int32_t tex_R, tex_V, tex_C;
+    int32_t tex_degree;             // SH degree of Eq. 2's vector form
     float q_scale[2], q_offset[2];  // 8-bit dequantisation: coefficients, scale
     int32_t K;
     float delta;
@@ -145,6 +146,7 @@ __device__ __forceinline__ void sh_basis(float x, float y, float z, float *Y)
 // --------------------------------------------------------------------------
 enum DispMode { kDispAlongRay = 0, kDispShVec3 = 1, kDispNone = 2 };
 
+// DEG < 0: Eq. 2's vector form with the SH degree (0..3) taken at run time.
 template <typename XT, int MODE, int DEG = 0>
 struct TexKind {
     typedef XT T;
@@ -218,6 +220,39 @@ __device__ __forceinline__ float bilinear_elem(const XT *tex, const Bilinear &B,
     return m;
 }
 
+// Eq. 2 as printed for SH degree DEG: S_a = sum_v Y_v(d) m[a nb + v] over
+// nb = (DEG + 1)^2 harmonics per axis, and the offset m_s(p_t) S.
+template <typename XT, int DEG>
+__device__ __forceinline__ void vec3_offset(const RayParams &p, const Bilinear &B, float u,
+                                            float v, const float *Y, bool vec, float &ox,
+                                            float &oy, float &oz)
+{
+    constexpr int EPV = 16 / (int)sizeof(XT);
+    constexpr int NB = (DEG + 1) * (DEG + 1), NCH = 3 * NB;
+    constexpr int NCHUNK = (NCH + EPV - 1) / EPV;
+    const XT *tex = (const XT *)p.tex;
+    const float qs = p.q_scale[0], qo = p.q_offset[0];
+    float m[NCHUNK * EPV];
+    if (vec) {
+#pragma unroll
+        for (int q = 0; q < NCHUNK; ++q) bilinear_chunk<XT>(tex, B, q * EPV, qs, qo, m + q * EPV);
+    } else {
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) m[c] = bilinear_elem<XT>(tex, B, c, qs, qo);
+    }
+    const Bilinear Bs = bilinear_taps(p.tex_R, 1, u, v);
+    const float ms =
+        bilinear_elem<XT>((const XT *)p.tex_scale, Bs, 0, p.q_scale[1], p.q_offset[1]);
+    float S[3] = {0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int a = 0; a < 3; ++a)
+#pragma unroll
+        for (int vv = 0; vv < NB; ++vv) S[a] += Y[vv] * m[a * NB + vv];
+    ox = ms * S[0];
+    oy = ms * S[1];
+    oz = ms * S[2];
+}
+
 // Offset p_cali - p for the ray direction d at texture coordinate (u, v).
 template <typename TK>
 __device__ __forceinline__ void displacement(const RayParams &p, float u, float v, float dx,
@@ -255,29 +290,15 @@ __device__ __forceinline__ void displacement(const RayParams &p, float u, float 
         ox = s * dx;
         oy = s * dy;
         oz = s * dz;
+    } else if (TK::degree >= 0) {
+        vec3_offset<XT, (TK::degree >= 0 ? TK::degree : 0)>(p, B, u, v, Y, vec, ox, oy, oz);
     } else {
-        // Eq. 2 as printed: S_a = sum_v Y_v(d) m[a nb + v]; p_cali = p + m_s S
-        constexpr int NB = TK::nb, NCH = 3 * NB;
-        constexpr int NCHUNK = (NCH + EPV - 1) / EPV;
-        float m[NCHUNK * EPV];
-        if (vec) {
-#pragma unroll
-            for (int q = 0; q < NCHUNK; ++q) bilinear_chunk<XT>(tex, B, q * EPV, qs, qo, m + q * EPV);
-        } else {
-#pragma unroll
-            for (int c = 0; c < NCH; ++c) m[c] = bilinear_elem<XT>(tex, B, c, qs, qo);
+        switch (p.tex_degree) {
+        case 0: vec3_offset<XT, 0>(p, B, u, v, Y, vec, ox, oy, oz); break;
+        case 1: vec3_offset<XT, 1>(p, B, u, v, Y, vec, ox, oy, oz); break;
+        case 2: vec3_offset<XT, 2>(p, B, u, v, Y, vec, ox, oy, oz); break;
+        default: vec3_offset<XT, 3>(p, B, u, v, Y, vec, ox, oy, oz); break;
         }
-        const Bilinear Bs = bilinear_taps(p.tex_R, 1, u, v);
-        const float ms =
-            bilinear_elem<XT>((const XT *)p.tex_scale, Bs, 0, p.q_scale[1], p.q_offset[1]);
-        float S[3] = {0.0f, 0.0f, 0.0f};
-#pragma unroll
-        for (int a = 0; a < 3; ++a)
-#pragma unroll
-            for (int vv = 0; vv < NB; ++vv) S[a] += Y[vv] * m[a * NB + vv];
-        ox = ms * S[0];
-        oy = ms * S[1];
-        oz = ms * S[2];
     }
 }
 
@@ -701,27 +722,31 @@ struct LayerA {
     h8 a32[MT][NC > 0 ? NC : 1];
     h4 a16[MT];
 
-    // W: fp16 [KIN][MOUT] row-major in global memory.
-    __device__ __forceinline__ void load(const _Float16 *W, int lane)
+    // W: fp16 [kin][mout] row-major in global memory, a layer of logical
+    // widths kin <= KIN, mout <= MOUT; the tile's other rows and columns are
+    // zero, so a narrower layer (Tab. 3's 8 hidden neurons on the 16-wide
+    // tile) is computed exactly: its padded neurons stay 0 through ReLU and
+    // add nothing downstream.
+    __device__ __forceinline__ void load(const _Float16 *W, int lane, int kin, int mout)
     {
         const int c = lane & 15, g = lane >> 4;
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) {
             const int o = mt * 16 + c;
-            const bool ok = o < MOUT;
+            const bool ok = o < mout;
 #pragma unroll
             for (int ch = 0; ch < NC; ++ch) {
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
                     const int k = FROM_REGS ? perm32(ch, g, j) : ch * 32 + 8 * g + j;
-                    a32[mt][ch][j] = ok ? W[k * MOUT + o] : (_Float16)0.0f;
+                    a32[mt][ch][j] = ok && k < kin ? W[k * mout + o] : (_Float16)0.0f;
                 }
             }
             if (R16) {
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
                     const int k = NC * 32 + 4 * g + j;
-                    a16[mt][j] = ok ? W[k * MOUT + o] : (_Float16)0.0f;
+                    a16[mt][j] = ok && k < kin ? W[k * mout + o] : (_Float16)0.0f;
                 }
             }
         }
@@ -818,16 +843,18 @@ struct MlpWeights {
     LayerA<HID, HID, true> mid[NHID > 1 ? NHID - 1 : 1];
     LayerA<HID, 4, true> head;
 
-    __device__ __forceinline__ void load(const _Float16 *W, int lane)
+    // hl: the hidden width of the weights in W (at most HID; the layers are
+    // [IN][hl], [hl][hl] x (NHID-1), [hl][4]).
+    __device__ __forceinline__ void load(const _Float16 *W, int lane, int hl)
     {
-        first.load(W, lane);
-        const _Float16 *p = W + IN * HID;
+        first.load(W, lane, IN, hl);
+        const _Float16 *p = W + IN * hl;
 #pragma unroll
         for (int m = 0; m < NHID - 1; ++m) {
-            mid[m].load(p, lane);
-            p += HID * HID;
+            mid[m].load(p, lane, hl, hl);
+            p += hl * hl;
         }
-        head.load(p, lane);
+        head.load(p, lane, hl, 4);
     }
 };
 

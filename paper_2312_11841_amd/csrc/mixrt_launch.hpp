@@ -20,6 +20,9 @@ enum TexId {
     kTexF16Vec3D2,
     kTexU8Vec3D2,
     kTexNone,
+    kTexF32Vec3,   // Eq. 2 as printed, SH degree 0..3 at run time
+    kTexF16Vec3,
+    kTexU8Vec3,
 };
 
 template <int ID>
@@ -31,6 +34,9 @@ template <> struct TexOf<kTexF32Vec3D1> { typedef TexKind<float, kDispShVec3, 1>
 template <> struct TexOf<kTexF16Vec3D2> { typedef TexKind<_Float16, kDispShVec3, 2> type; };
 template <> struct TexOf<kTexU8Vec3D2> { typedef TexKind<uint8_t, kDispShVec3, 2> type; };
 template <> struct TexOf<kTexNone> { typedef TexKind<float, kDispNone> type; };
+template <> struct TexOf<kTexF32Vec3> { typedef TexKind<float, kDispShVec3, -1> type; };
+template <> struct TexOf<kTexF16Vec3> { typedef TexKind<_Float16, kDispShVec3, -1> type; };
+template <> struct TexOf<kTexU8Vec3> { typedef TexKind<uint8_t, kDispShVec3, -1> type; };
 
 // dtype: 0 f32, 1 f16, 2 u8 (mixrt_dtype); mode: mixrt_disp_mode.  -1 when
 // no kernel is built for the combination.
@@ -42,8 +48,16 @@ inline int tex_id(int dtype, int mode, int degree)
         if (dtype == 0 && degree == 1) return kTexF32Vec3D1;
         if (dtype == 1 && degree == 2) return kTexF16Vec3D2;
         if (dtype == 2 && degree == 2) return kTexU8Vec3D2;
+        if (degree < 0 || degree > 3) return -1;
+        return dtype == 0 ? kTexF32Vec3 : dtype == 1 ? kTexF16Vec3 : kTexU8Vec3;
     }
     return -1;
+}
+
+// Eq. 2's vector form at any degree (0..3, taken at run time) for a dtype.
+inline int tex_id_any_degree(int dtype)
+{
+    return dtype == 0 ? kTexF32Vec3 : dtype == 1 ? kTexF16Vec3 : kTexU8Vec3;
 }
 
 struct RenderLaunch {
@@ -55,6 +69,7 @@ struct RenderLaunch {
     int tex;          // TexId
     bool tf16;
     int F, in, hid, nhid;
+    int hid_w;        // hidden width of the weights (<= hid, the kernel's)
     int cus;
     int64_t l2_bytes;   // L2 of one XCD
     int blocks_mode;    // 0: by the gathers' line sharing, 1: all that fit, 2: two per CU
@@ -76,8 +91,8 @@ hipError_t launch_ray_setup(const RayParams &rp, int tex, float *out_x, int32_t 
                             hipStream_t stream);
 hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const float *x, int64_t n,
                               int32_t *oc, uint32_t *oi, float *ow, float *of, hipStream_t stream);
-hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const _Float16 *x,
-                      int64_t n, float4 *out4, int cus, hipStream_t stream);
+hipError_t launch_mlp(int in, int hid, int nhid, int hid_w, const _Float16 *weights,
+                      const _Float16 *x, int64_t n, float4 *out4, int cus, hipStream_t stream);
 hipError_t launch_composite(const float4 *srgb, int64_t rays, int K, float delta, float t_term,
                             const float *bg, float4 *out, hipStream_t stream);
 

@@ -76,13 +76,13 @@ __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, floa
 
 // Stand-in for the weights when the MLP is removed.
 struct NoMlp {
-    __device__ __forceinline__ void load(const _Float16 *, int) {}
+    __device__ __forceinline__ void load(const _Float16 *, int, int) {}
 };
 
 template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
                                                         const _Float16 *__restrict__ weights,
-                                                        int view_sh, int stripe,
+                                                        int view_sh, int hid_w, int stripe,
                                                         float4 *__restrict__ out)
 {
 #ifdef MIXRT_SPLIT_NO_DISP
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     // NHID = 0: the MLP removed; the level features are summed per component
     constexpr bool SUM = NHID == 0;
     typename std::conditional<SUM, NoMlp, MlpWeights<IN, HID, NHID>>::type Wt;
-    Wt.load(weights, lane);
+    Wt.load(weights, lane, hid_w);
 
     const int K = rp.K;
     const int R = kWave / K;                 // rays per tile
@@ -260,8 +260,8 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
 template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, GridParams gp,
                                                               const _Float16 *__restrict__ weights,
-                                                              int view_sh, int stripe, int C,
-                                                              float4 *__restrict__ out)
+                                                              int view_sh, int hid_w, int stripe,
+                                                              int C, float4 *__restrict__ out)
 {
 #ifdef MIXRT_SPLIT_NO_DISP
     typedef TexKind<float, kDispNone> TK;
@@ -287,7 +287,7 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
 
     constexpr bool SUM = NHID == 0;
     typename std::conditional<SUM, NoMlp, MlpWeights<IN, HID, NHID>>::type Wt;
-    Wt.load(weights, lane);
+    Wt.load(weights, lane, hid_w);
 
     const int K = rp.K;
     const int R = kWave / K;                 // rays per tile
@@ -484,7 +484,13 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
     X(kTexNone, 4, true, 0, 0, 0)               \
     X(kTexNone, 2, false, 0, 0, 0)              \
     X(kTexF32Ray, 2, false, 0, 0, 0)            \
-    X(kTexU8Vec3D2, 4, true, 0, 0, 0)
+    X(kTexU8Vec3D2, 4, true, 0, 0, 0)           \
+    X(kTexF32Vec3, 2, false, 16, 32, 1)         \
+    X(kTexF16Vec3, 2, false, 16, 32, 1)         \
+    X(kTexU8Vec3, 2, false, 16, 32, 1)          \
+    X(kTexF32Vec3, 4, true, 32, 64, 2)          \
+    X(kTexF16Vec3, 4, true, 32, 64, 2)          \
+    X(kTexU8Vec3, 4, true, 32, 64, 2)
 
 bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid)
 {
@@ -622,11 +628,11 @@ hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
         if (chunk > 0)                                                                         \
             hipLaunchKernelGGL((render_queue_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks), \
                                dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh,      \
-                               stripe, chunk, L.out);                                          \
+                               L.hid_w, stripe, chunk, L.out);                                 \
         else                                                                                   \
             hipLaunchKernelGGL((render_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks),      \
                                dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh,      \
-                               stripe, L.out);                                                 \
+                               L.hid_w, stripe, L.out);                                        \
         return hipGetLastError();                                                              \
     }
     MIXRT_RENDER_VARIANTS(X)

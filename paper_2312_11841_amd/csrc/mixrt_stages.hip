@@ -126,8 +126,8 @@ constexpr int kStores = 4;   // one per 16-row sub-tile, by lanes 0..15
 
 template <int IN, int HID, int NHID, int DEPTH>
 __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict__ weights,
-                                                     const _Float16 *__restrict__ in, int64_t n,
-                                                     float4 *__restrict__ out4)
+                                                     int hid_w, const _Float16 *__restrict__ in,
+                                                     int64_t n, float4 *__restrict__ out4)
 {
     static_assert(IN % 8 == 0, "rows are moved in 16-byte chunks");
     static_assert(DEPTH >= 1 && DEPTH <= 2, "tiles in flight");
@@ -139,7 +139,7 @@ __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict_
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     MlpWeights<IN, HID, NHID> Wt;
-    Wt.load(weights, lane);
+    Wt.load(weights, lane, hid_w);
     const int64_t n_tiles = (n + kWave - 1) / kWave;
     const int64_t total = (int64_t)gridDim.x * kWavesPerBlock;
     const int64_t first = (int64_t)blockIdx.x * kWavesPerBlock + wv;
@@ -232,7 +232,7 @@ hipError_t launch_ray_setup(const RayParams &rp, int tex, float *out_x, int32_t 
         break;
     switch (tex) {
         T(kTexF32Ray) T(kTexF16Ray) T(kTexU8Ray) T(kTexF32Vec3D1) T(kTexF16Vec3D2) T(kTexU8Vec3D2)
-        T(kTexNone)
+        T(kTexNone) T(kTexF32Vec3) T(kTexF16Vec3) T(kTexU8Vec3)
     default: return hipErrorInvalidValue;
     }
 #undef T
@@ -262,8 +262,8 @@ hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const floa
 // ms for 7.37M rows of 48).
 constexpr int kMlpDepth = 1;
 
-hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const _Float16 *x,
-                      int64_t n, float4 *out4, int cus, hipStream_t stream)
+hipError_t launch_mlp(int in, int hid, int nhid, int hid_w, const _Float16 *weights,
+                      const _Float16 *x, int64_t n, float4 *out4, int cus, hipStream_t stream)
 {
     if (n == 0) return hipSuccess;
     if (nhid == 0) {
@@ -278,8 +278,8 @@ hipError_t launch_mlp(int in, int hid, int nhid, const _Float16 *weights, const 
         static std::atomic<int> per_cu{0};                                                   \
         const int64_t resident = (int64_t)blocks_per_cu((const void *)fn, per_cu) * cus;     \
         const int64_t blocks = want < resident ? want : resident;                            \
-        hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, weights, x, n, \
-                           out4);                                                            \
+        hipLaunchKernelGGL(fn, dim3((unsigned)blocks), dim3(kBlock), 0, stream, weights, hid_w, \
+                           x, n, out4);                                                      \
         return hipGetLastError();                                                            \
     }
     MIXRT_MLP_VARIANTS(X)

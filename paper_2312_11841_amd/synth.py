@@ -191,9 +191,9 @@ PAPER720P_NOVDD = PAPER720P.replace(name="paper720p_novdd", disp="none")
 def table3_config(L: int, log2_T: int, mlp: bool) -> SceneConfig:
     """Tab. 3's profiling points: one query per pixel, no displacement map, F=4
     entries over the deployed 256..4096 resolutions, with the MLP (two hidden
-    layers; width 16, the narrowest MFMA tile, for the table's 8) or without
-    it (level features summed per component)."""
-    widths = (L * 4, 16, 16, 4) if mlp else (L * 4,)
+    layers of 8 neurons, as the table gives it) or without it (level
+    features summed per component)."""
+    widths = (L * 4, 8, 8, 4) if mlp else (L * 4,)
     return PAPER720P.replace(name=f"tab3_L{L}_T{log2_T}" + ("_mlp" if mlp else ""), disp="none",
                              L=L, log2_T=log2_T, view_sh_dim=0, widths=widths, seed=7)
 

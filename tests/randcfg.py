@@ -15,6 +15,11 @@ TEX = {
     "u8_vec3_d2": dict(tex_dtype="u8", disp="vec3", sh_degree=2),
     "f32_vec3_d1": dict(tex_dtype="f32", disp="vec3", sh_degree=1),
     "none": dict(tex_dtype="f32", disp="none"),
+    # Eq. 2 as printed at a random SH degree 0..3 (the kernels that take the
+    # degree at run time)
+    "f32_vec3": dict(tex_dtype="f32", disp="vec3"),
+    "f16_vec3": dict(tex_dtype="f16", disp="vec3"),
+    "u8_vec3": dict(tex_dtype="u8", disp="vec3"),
 }
 
 # (displacement, F, fp16 table, MLP in, hidden, hidden layers); 0, 0, 0 = the
@@ -29,9 +34,13 @@ BUILT = [
     ("none", 4, True, 32, 64, 2), ("none", 4, True, 32, 16, 2),
     ("none", 4, True, 0, 0, 0), ("none", 2, False, 0, 0, 0),
     ("f32_ray", 2, False, 0, 0, 0), ("u8_vec3_d2", 4, True, 0, 0, 0),
+    ("f32_vec3", 2, False, 16, 32, 1), ("f16_vec3", 2, False, 16, 32, 1),
+    ("u8_vec3", 2, False, 16, 32, 1), ("f32_vec3", 4, True, 32, 64, 2),
+    ("f16_vec3", 4, True, 32, 64, 2), ("u8_vec3", 4, True, 32, 64, 2),
+    ("none", 4, True, 32, 8, 2),   # hidden width 8 on the 16-wide tile
 ]
 
-SEEDS = list(range(1000, 1048))
+SEEDS = list(range(1000, 1050))
 
 
 def _random_rotation(rng: np.random.Generator) -> np.ndarray:
@@ -59,13 +68,16 @@ def random_config(seed: int) -> synth.SceneConfig:
     n_min = int(rng.integers(2, 41))
     n_max = int(min(2048, n_min * rng.uniform(1.0, 64.0)))
     H, W = int(rng.integers(1, 38)), int(rng.integers(1, 42))
+    tex_kw = dict(TEX[tex])
+    if tex_kw["disp"] == "vec3" and "sh_degree" not in tex_kw:
+        tex_kw["sh_degree"] = int(rng.integers(0, 4))
     return synth.TINY64.replace(
         name=f"rand{seed}", views=int(rng.integers(1, 4)), H=H, W=W,
         K=int(rng.choice([1, 2, 3, 4, 5, 7, 8, 13, 16, 32, 64])),
         delta=float(rng.uniform(0.002, 0.3)),
         gbuf=str(rng.choice(["iid", "room"])),
         tex_R=int(rng.integers(1, 49)), tex_V=int(rng.integers(1, 17)),
-        tex_range=float(rng.uniform(0.02, 0.3)), **TEX[tex],
+        tex_range=float(rng.uniform(0.02, 0.3)), **tex_kw,
         L=L, log2_T=int(rng.integers(6, 18)), F=F, N_min=n_min, N_max=n_max,
         table_dtype="f16" if f16 else "f32", table_range=float(rng.uniform(0.01, 0.5)),
         widths=widths, view_sh_dim=view_sh, w_std=float(rng.uniform(0.03, 0.12)),

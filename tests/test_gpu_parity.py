@@ -154,7 +154,8 @@ def _mlp_bound(x, weights):
     return 2.0 * err + 1e-6
 
 
-MLP_SHAPES = [(16, 32, 1), (32, 32, 1), (48, 64, 2), (32, 64, 2), (16, 64, 2), (32, 16, 2)]
+MLP_SHAPES = [(16, 32, 1), (32, 32, 1), (48, 64, 2), (32, 64, 2), (16, 64, 2), (32, 16, 2),
+              (32, 8, 2)]   # hidden width 8 (Tab. 3), on the 16-wide tile
 
 
 @pytest.mark.parametrize("shape", MLP_SHAPES, ids=lambda s: f"{s[0]}-{s[1]}x{s[2]}")
@@ -241,6 +242,13 @@ FRAME_CFGS = [synth.TINY64, synth.TINY64_DENSE, synth.VIEW720P, synth.VIEW720P_D
               synth.DEPLOYED720P, synth.PAPER720P, synth.PAPER720P_NOVDD, synth.TINY64_VEC3,
               synth.TINY64_U8, synth.TINY64_NODISP, *synth.TABLE3,
               synth.TINY64_DENSE.replace(name="tiny64_nomlp", widths=(16,), seed=16)]
+# Eq. 2 as printed at every SH degree and storage type (Sec. 4.3.2 leaves
+# D_SH open), on the tiny MLP and on the deployed grid and MLP
+FRAME_CFGS += [synth.TINY64_VEC3.replace(name=f"tiny64_vec3_{dt}_d{d}", tex_dtype=dt,
+                                         sh_degree=d, seed=30 + 4 * i + d)
+               for i, dt in enumerate(("f32", "f16", "u8")) for d in (0, 3)]
+FRAME_CFGS += [synth.PAPER720P.replace(name=f"paper720p_d{d}", sh_degree=d) for d in (0, 3)]
+FRAME_CFGS += [synth.PAPER720P.replace(name="paper720p_f16_d1", tex_dtype="f16", sh_degree=1)]
 # the level and table-size sweeps' remaining points
 FRAME_CFGS += list({c.name: c for c in synth.LEVEL_SWEEP + synth.SIZE_SWEEP
                     if c.name not in {f.name for f in FRAME_CFGS}}.values())
