@@ -29,6 +29,7 @@ import pytest
 
 import oracle
 from paper_2312_11841_amd import mixrt, synth
+import meshbars
 
 torch = pytest.importorskip("torch")
 pytestmark = pytest.mark.gpu
@@ -107,19 +108,15 @@ def _check_gbuffer(mesh, cams, W, H, g0, g1, pix, label, max_amb=0.01):
         d = np.array([oracle.camera_ray(cams[v], W, H, ii, jj)[1]
                       for v, ii, jj in zip(view, i, j)])
         cos = np.abs(np.einsum("ij,ij->i", d, ref_n[hit]))
-        inv_cos = 1.0 / np.maximum(cos, 1e-3)
-        # conditioning of the fp32 solve: the vertices' distance from the
-        # camera, the longest edge and the triangle's shape L_max^2 / (2 area)
-        P = mesh.positions.astype(np.float64)[mesh.faces[ref_tri[hit]]]    # [n, 3, 3]
+        # conditioning of the fp32 solve (tests/meshbars.py): the vertices'
+        # distance from the camera, the longest edge and the triangle's shape
         origin = np.asarray(cams, np.float64).reshape(-1, 16)[view][:, [3, 7, 11]]
-        dist = np.linalg.norm(P - origin[:, None, :], axis=2).max(1)
-        edges = np.stack([P[:, 1] - P[:, 0], P[:, 2] - P[:, 1], P[:, 0] - P[:, 2]], 1)
-        l_max = np.linalg.norm(edges, axis=2).max(1)
-        area = 0.5 * np.linalg.norm(np.cross(edges[:, 0], -edges[:, 2]), axis=1)
-        shape = l_max ** 2 / (2.0 * area)
+        dist, l_max, shape = meshbars.conditioning(mesh.positions, mesh.faces, ref_tri[hit],
+                                                   origin)
         t_ref = ref_g0[hit, 0]
         dt = np.abs(got0[hit, 0] - t_ref)
-        assert np.all(dt <= (1e-5 * t_ref + 1e-6 * dist * shape) * inv_cos), (dt / t_ref).max()
+        tb = meshbars.t_bar(t_ref, dist, shape, cos)
+        assert np.all(dt <= tb), ((dt / tb).max(), (dt / t_ref).max())
         terr = dt / t_ref
         uerr = np.abs(got0[hit, 1:3] - ref_g0[hit, 1:3]).max(1)
         if mesh.uv is None:
@@ -127,8 +124,10 @@ def _check_gbuffer(mesh, cams, W, H, g0, g1, pix, label, max_amb=0.01):
         else:
             corners = mesh.uv.astype(np.float64)[mesh.faces[ref_tri[hit]]]      # [n, 3, 2]
             spread = (corners.max(1) - corners.min(1)).max(1)
-            bar = spread * (1e-4 + 1e-6 * dist * shape / l_max) * inv_cos + 1e-6
-            assert np.all(uerr <= bar), uerr.max()
+            ub = meshbars.uv_bar(spread, dist, shape, l_max, cos)
+            assert np.all(uerr <= ub), ((uerr / ub).max(), uerr.max())
+        say(f"  largest share of the bars used: t {(dt / tb).max():.3f}"
+            + ("" if mesh.uv is None else f", uv {(uerr / ub).max():.3f}"))
         assert np.all(got0[hit, 3] == 0)
         nerr = np.abs(got1[hit, :3] - ref_n[hit]).max()
         assert nerr <= 1e-4, nerr
@@ -152,7 +151,7 @@ def _check_gbuffer(mesh, cams, W, H, g0, g1, pix, label, max_amb=0.01):
         shape = (np.linalg.norm(e, axis=1).max() ** 2
                  / np.linalg.norm(np.cross(e[0], -e[2])))
         assert min(b1, b2, 1 - b1 - b2) > -4e-4 * g
-        assert abs(got0[q, 0] - t) <= (1e-5 * t + 1e-6 * dist * shape) * g
+        assert abs(got0[q, 0] - t) <= (meshbars.T_REL * t + meshbars.T_COND * dist * shape) * g
         if ref_tri[q] >= 0:
             assert t <= ref_g0[q, 0] * (1 + 2e-4 * g)
 
