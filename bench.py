@@ -92,9 +92,25 @@ def standalone_mlp(cfg, ds, renderer, samples):
         torch.cuda.synchronize()
     sec = time_launches(renderer.stream, lambda: renderer.mlp(ds.mlp, xi), 50) * 1e-3
     flops = samples * 2 * sum(p * q for p, q in zip(cfg.widths[:-1], cfg.widths[1:]))
-    return {"samples": samples, "ms": round(sec * 1e3, 4), "TFLOPs": round(flops / sec / 1e12, 1),
-            "util_of_peak": round(flops / sec / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
-            "hbm_bytes": samples * (cfg.widths[0] * 2 + 16)}
+    in_bytes = cfg.widths[0] * 2
+    out = {"samples": samples, "ms": round(sec * 1e3, 4), "TFLOPs": round(flops / sec / 1e12, 1),
+           "util_of_peak": round(flops / sec / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+           "hbm_bytes": samples * (in_bytes + 16),
+           "GBps": round(samples * (in_bytes + 16) / sec / 1e9, 1)}
+    if in_bytes in (32, 64, 96):
+        # the stage's own memory pattern alone (rows in, 16 B per row out),
+        # measured now: the most the stage can stream on this GPU
+        from paper_2312_11841_amd import microbench as mb
+        st = mb.rowstream(samples, in_bytes, blocks_list=(1, 2, 3, 4, 6, 8))
+        ceiling_s = samples * (in_bytes + 16) / (st["GBps"] * 1e9)
+        out["stream_ceiling"] = {
+            "pattern": f"{in_bytes} B read + 16 B written per row, 64-row tiles, coalesced, "
+                       "non-temporal (mixrt_mb_rowstream)",
+            "GBps": round(st["GBps"], 1), "blocks": st["blocks"],
+            "ms": round(ceiling_s * 1e3, 4),
+            "util_of_peak": round(flops / ceiling_s / 1e12 / MFMA_F16_PEAK_TFLOPS, 4),
+            "stage_frac_of_ceiling": round(ceiling_s / sec, 4)}
+    return out
 
 
 def gather_replay_floor(cfg, ds, renderer):

@@ -34,6 +34,15 @@ int mixrt_mb_copy(const void *src, void *dst, uint64_t bytes, int blocks, void *
  * sink: device uint32 [blocks*256] (written, keeps the loads live). */
 int mixrt_mb_read(const void *src, uint64_t bytes, int blocks, uint32_t *sink, void *stream);
 
+/* Mixed read/write stream in the MLP stage's pattern: rows (a multiple of
+ * 64) rows of in_bytes (32, 64 or 96) read from src in tiles of 64 rows
+ * (coalesced 16-byte loads), and 16 bytes per row written to dst (the XOR of
+ * the row's chunks that the lane loaded); blocks x 256 threads, a wave per
+ * tile, non-temporal loads and stores.  src: device [rows][in_bytes],
+ * dst: device [rows][16], both 16-byte aligned. */
+int mixrt_mb_rowstream(const void *src, void *dst, int64_t rows, int in_bytes, int blocks,
+                       void *stream);
+
 /* iters x 8 independent fp16 16x16x32 MFMAs per wave; blocks x 256 threads;
  * out: device float [blocks*256]. */
 int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);

@@ -104,6 +104,33 @@ __global__ __launch_bounds__(kBlock) void read_kernel(const uint4 *__restrict__ 
     sink[(uint64_t)blockIdx.x * kBlock + threadIdx.x] = acc;
 }
 
+// Mixed read/write stream in the MLP stage's pattern: each wave takes tiles
+// of 64 rows of `in_chunks` 16-byte chunks (read coalesced, lane l taking
+// chunks l, l + 64, ...) and writes one 16-byte chunk per row (64 per tile),
+// so reads and writes keep the stage's ratio (96 B in, 16 B out per row for
+// 48 fp16 inputs).  Loads and stores are non-temporal like the stage's.
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+template <int IN_CHUNKS>
+__global__ __launch_bounds__(kBlock) void rowstream_kernel(const u32x4 *__restrict__ src,
+                                                           u32x4 *__restrict__ dst,
+                                                           int64_t n_tiles)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t total = (int64_t)gridDim.x * (kBlock / 64);
+    for (int64_t t = (int64_t)blockIdx.x * (kBlock / 64) + threadIdx.x / 64; t < n_tiles;
+         t += total) {
+        const u32x4 *s = src + t * 64 * IN_CHUNKS;
+        u32x4 v[IN_CHUNKS];
+#pragma unroll
+        for (int c = 0; c < IN_CHUNKS; ++c) v[c] = __builtin_nontemporal_load(s + c * 64 + lane);
+        u32x4 a = v[0];
+#pragma unroll
+        for (int c = 1; c < IN_CHUNKS; ++c) a ^= v[c];
+        __builtin_nontemporal_store(a, dst + t * 64 + lane);
+    }
+}
+
 typedef _Float16 h8 __attribute__((ext_vector_type(8)));
 typedef float f4 __attribute__((ext_vector_type(4)));
 
@@ -360,6 +387,26 @@ int mixrt_mb_read(const void *src, uint64_t bytes, int blocks, uint32_t *sink, v
     if (!src || !sink || (bytes & 15) || blocks < 1) return hipErrorInvalidValue;
     hipLaunchKernelGGL(read_kernel, dim3(blocks), dim3(kBlock), 0, (hipStream_t)stream,
                        (const uint4 *)src, bytes / 16, sink);
+    return hipGetLastError();
+}
+
+int mixrt_mb_rowstream(const void *src, void *dst, int64_t rows, int in_bytes, int blocks,
+                       void *stream)
+{
+    if (!src || !dst || blocks < 1 || rows < 0 || rows % 64) return hipErrorInvalidValue;
+    if (((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return hipErrorInvalidValue;
+    const int64_t tiles = rows / 64;
+    hipStream_t s = (hipStream_t)stream;
+#define RS(C)                                                                                   \
+    hipLaunchKernelGGL((rowstream_kernel<C>), dim3(blocks), dim3(kBlock), 0, s,                  \
+                       (const u32x4 *)src, (u32x4 *)dst, tiles)
+    switch (in_bytes) {
+    case 32: RS(2); break;
+    case 64: RS(4); break;
+    case 96: RS(6); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef RS
     return hipGetLastError();
 }
 

@@ -25,6 +25,8 @@ def lib():
         L.mixrt_mb_copy.argtypes = [P, P, C.c_uint64, C.c_int, P]
         L.mixrt_mb_read.argtypes = [P, C.c_uint64, C.c_int, P, P]
         L.mixrt_mb_mfma.argtypes = [C.c_int, C.c_int, P, P]
+        L.mixrt_mb_rowstream.argtypes = [P, P, C.c_int64, C.c_int, C.c_int, P]
+        L.mixrt_mb_rowstream.restype = C.c_int
         I32 = C.c_int32
         L.mixrt_mb_gather_replay.argtypes = [P, P, I32, I32, I32, I32, P, I32, I32, I32, P, I32,
                                              I32, I32, I32, P, P]
@@ -168,3 +170,27 @@ def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_str
         rows.append(res)
     best = min(rows, key=lambda r: r["ms"])
     return {"by_blocks": rows, "best": best}
+
+
+def rowstream(rows: int, in_bytes: int = 96, blocks_list=None, reps: int = 20):
+    """The MLP stage's memory pattern alone (mixrt_mb_rowstream): rows of
+    in_bytes read, 16 bytes per row written.  Returns the fastest of the
+    grid sizes tried, as bytes moved per second."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    rows -= rows % 64
+    src = torch.empty(rows * in_bytes // 4, dtype=torch.int32, device="cuda")
+    src.random_()
+    dst = torch.empty(rows * 4, dtype=torch.int32, device="cuda")
+    best = None
+    for k in (blocks_list or (1, 2, 3, 4, 6, 8)):
+        blocks = int(k * cus)
+
+        def launch(s):
+            _check(lib().mixrt_mb_rowstream(src.data_ptr(), dst.data_ptr(), rows, in_bytes,
+                                            blocks, s.cuda_stream))
+        t = _timed(launch, reps)
+        r = {"blocks": blocks, "seconds": t, "GBps": rows * (in_bytes + 16) / t / 1e9}
+        if best is None or r["GBps"] > best["GBps"]:
+            best = r
+    return {"rows": rows, "in_bytes": in_bytes, **best}
