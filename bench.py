@@ -487,8 +487,8 @@ def main():
         geometry()   # the G-buffer the legs below read
     if not args.no_rooflines:
         print("bench: rooflines, replay and stage builds", file=sys.stderr, flush=True)
-        extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
         extra["rooflines_measured"] = measured_rooflines(cfg)
+        extra["mlp_standalone"] = standalone_mlp(cfg, ds, r, cfg.samples)
         replay = gather_replay_floor(cfg, ds, r)
         stages = stage_metrics(cfg, ds, out, max(args.steps, 20), args.early_stop_chunk)
 
