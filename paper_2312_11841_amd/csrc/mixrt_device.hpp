@@ -8,6 +8,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace mixrt {
 
 typedef _Float16 h2 __attribute__((ext_vector_type(2)));
@@ -193,30 +195,47 @@ __device__ __forceinline__ Bilinear bilinear_taps(int R, int C, float u, float v
     return B;
 }
 
+// The 4 tap weights with an 8-bit map's dequantisation folded in: the
+// weights sum to one, so sum_k w_k (qo + qs e_k) = qo + sum_k (w_k qs) e_k,
+// and a filtered channel costs one conversion and one fma per tap instead of
+// two fmas.  fp32 and fp16 maps are read as stored (base 0, weights as is).
+template <typename XT>
+struct TapWeights {
+    float w[4];
+    float base;
+    __device__ __forceinline__ TapWeights(const Bilinear &B, float qs, float qo)
+    {
+        constexpr bool Q = std::is_same<XT, uint8_t>::value;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) w[k] = Q ? B.w[k] * qs : B.w[k];
+        base = Q ? qo : 0.0f;
+    }
+};
+
 // Filtered channels [c0, c0 + EPV) of one 16-byte chunk of every texel.
 template <typename XT>
-__device__ __forceinline__ void bilinear_chunk(const XT *tex, const Bilinear &B, int c0,
-                                               float qs, float qo, float *m)
+__device__ __forceinline__ void bilinear_chunk(const XT *tex, const Bilinear &B,
+                                               const TapWeights<XT> &tw, int c0, float *m)
 {
     constexpr int EPV = 16 / (int)sizeof(XT);
 #pragma unroll
-    for (int e = 0; e < EPV; ++e) m[e] = 0.0f;
+    for (int e = 0; e < EPV; ++e) m[e] = tw.base;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         XT e[EPV];
         *(uint4 *)e = *(const uint4 *)(tex + B.t[k] + c0);
 #pragma unroll
-        for (int i = 0; i < EPV; ++i) m[i] += B.w[k] * tex_elem(e[i], qs, qo);
+        for (int i = 0; i < EPV; ++i) m[i] += tw.w[k] * (float)e[i];
     }
 }
 
 template <typename XT>
-__device__ __forceinline__ float bilinear_elem(const XT *tex, const Bilinear &B, int c, float qs,
-                                               float qo)
+__device__ __forceinline__ float bilinear_elem(const XT *tex, const Bilinear &B,
+                                               const TapWeights<XT> &tw, int c)
 {
-    float m = 0.0f;
+    float m = tw.base;
 #pragma unroll
-    for (int k = 0; k < 4; ++k) m += B.w[k] * tex_elem(tex[B.t[k] + c], qs, qo);
+    for (int k = 0; k < 4; ++k) m += tw.w[k] * (float)tex[B.t[k] + c];
     return m;
 }
 
@@ -231,18 +250,18 @@ __device__ __forceinline__ void vec3_offset(const RayParams &p, const Bilinear &
     constexpr int NB = (DEG + 1) * (DEG + 1), NCH = 3 * NB;
     constexpr int NCHUNK = (NCH + EPV - 1) / EPV;
     const XT *tex = (const XT *)p.tex;
-    const float qs = p.q_scale[0], qo = p.q_offset[0];
+    const TapWeights<XT> tw(B, p.q_scale[0], p.q_offset[0]);
     float m[NCHUNK * EPV];
     if (vec) {
 #pragma unroll
-        for (int q = 0; q < NCHUNK; ++q) bilinear_chunk<XT>(tex, B, q * EPV, qs, qo, m + q * EPV);
+        for (int q = 0; q < NCHUNK; ++q) bilinear_chunk<XT>(tex, B, tw, q * EPV, m + q * EPV);
     } else {
 #pragma unroll
-        for (int c = 0; c < NCH; ++c) m[c] = bilinear_elem<XT>(tex, B, c, qs, qo);
+        for (int c = 0; c < NCH; ++c) m[c] = bilinear_elem<XT>(tex, B, tw, c);
     }
     const Bilinear Bs = bilinear_taps(p.tex_R, 1, u, v);
-    const float ms =
-        bilinear_elem<XT>((const XT *)p.tex_scale, Bs, 0, p.q_scale[1], p.q_offset[1]);
+    const float ms = bilinear_elem<XT>((const XT *)p.tex_scale, Bs,
+                                       TapWeights<XT>(Bs, p.q_scale[1], p.q_offset[1]), 0);
     float S[3] = {0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int a = 0; a < 3; ++a)
@@ -264,19 +283,19 @@ __device__ __forceinline__ void displacement(const RayParams &p, float u, float 
     constexpr int EPV = 16 / (int)sizeof(XT);
     const XT *tex = (const XT *)p.tex;
     const Bilinear B = bilinear_taps(p.tex_R, p.tex_C, u, v);
-    const float qs = p.q_scale[0], qo = p.q_offset[0];
     const bool vec = ((p.tex_C * (int)sizeof(XT)) & 15) == 0;
     float Y[16];
     sh_basis<16>(dx, dy, dz, Y);
     if (TK::mode == kDispAlongRay) {
         // s = sum_v Y_v(d) m_v over the first V channels; p_cali = p + s d
+        const TapWeights<XT> tw(B, p.q_scale[0], p.q_offset[0]);
         float s = 0.0f;
         if (vec) {
 #pragma unroll
             for (int c0 = 0; c0 < 16; c0 += EPV) {
                 if (c0 < p.tex_V) {
                     float m[EPV];
-                    bilinear_chunk<XT>(tex, B, c0, qs, qo, m);
+                    bilinear_chunk<XT>(tex, B, tw, c0, m);
 #pragma unroll
                     for (int e = 0; e < EPV && c0 + e < 16; ++e)
                         if (c0 + e < p.tex_V) s += Y[c0 + e] * m[e];
@@ -285,7 +304,7 @@ __device__ __forceinline__ void displacement(const RayParams &p, float u, float 
         } else {
 #pragma unroll
             for (int c = 0; c < 16; ++c)
-                if (c < p.tex_V) s += Y[c] * bilinear_elem<XT>(tex, B, c, qs, qo);
+                if (c < p.tex_V) s += Y[c] * bilinear_elem<XT>(tex, B, tw, c);
         }
         ox = s * dx;
         oy = s * dy;
@@ -591,9 +610,16 @@ __device__ __forceinline__ void level_setup(const GridParams &gp, int l, bool de
     uint32_t c[3];
 #pragma unroll
     for (int a = 0; a < 3; ++a) {
-        // floor(min(p, N - 1)) = min(floor(p), N - 1) since N - 1 is integral
-        s.cf[a] = floorf(IN_UNIT ? fminf(p[a], top) : fminf(fmaxf(p[a], 0.0f), top));
-        c[a] = (uint32_t)s.cf[a];
+        if (IN_UNIT) {
+            // 0 <= p <= N: truncation is the floor, clamped to N - 1 in
+            // integers (the float clamp would first have to quiet p)
+            c[a] = min((uint32_t)p[a], N - 1u);
+            s.cf[a] = (float)c[a];
+        } else {
+            // floor(min(p, N - 1)) = min(floor(p), N - 1), N - 1 integral
+            s.cf[a] = floorf(fminf(fmaxf(p[a], 0.0f), top));
+            c[a] = (uint32_t)s.cf[a];
+        }
         s.fr[a] = p[a] - s.cf[a];
     }
     if (dense) {
