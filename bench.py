@@ -122,14 +122,16 @@ def gather_replay_floor(cfg, ds, renderer):
     from paper_2312_11841_amd import microbench as mb
     from paper_2312_11841_amd import mixrt
     x, hit = renderer.ray_setup(ds)
-    blocks, stripe, chunk = renderer.launch_shape(ds, chunk=True)
+    plan = renderer.launch_plan(ds)
+    blocks, stripe, chunk = plan["blocks"], plan["tile_stripe"], plan["chunk"]
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     N = mixrt.level_resolutions(ds.grid)
     grids = sorted({blocks} | {k * cus for k in (1, 2, 3, 4, 6, 8)})
     r = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N, stripe,
-                         grids, chunk=chunk)
+                         grids, chunk=chunk, block_from=plan["block_from"])
     del x, hit
-    return {"render_blocks": blocks, "tile_stripe": stripe, "early_stop_chunk": chunk, **r}
+    return {"render_blocks": blocks, "tile_stripe": stripe, "early_stop_chunk": chunk,
+            "block_from": plan["block_from"], **r}
 
 
 def stage_metrics(cfg, ds, out, steps, chunk=0):
@@ -492,7 +494,7 @@ def main():
         replay = gather_replay_floor(cfg, ds, r)
         stages = stage_metrics(cfg, ds, out, max(args.steps, 20), args.early_stop_chunk)
 
-    launch = r.launch_shape(ds, chunk=True)
+    plan = r.launch_plan(ds)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -642,7 +644,8 @@ def main():
             "rays": cfg.rays,
             "samples": cfg.samples,
             "parallelism": "single GPU",
-            "launch": dict(zip(("blocks", "tile_stripe", "early_stop_chunk"), launch)),
+            "launch": {"blocks": plan["blocks"], "tile_stripe": plan["tile_stripe"],
+                       "early_stop_chunk": plan["chunk"], "block_from": plan["block_from"]},
         },
         "roofline": roofline,
         **stage_fields,

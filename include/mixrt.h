@@ -106,6 +106,13 @@ typedef struct {
                             larger than one XCD's L2; otherwise rounds of 4, 2
                             or 1 as a ray's samples share the voxels of at
                             least half, a quarter or fewer of the levels */
+    int32_t block_levels; /* how many of the finest hash levels gather each
+                            x-neighbour pair of corners as one aligned 16-byte
+                            block holding both entries (tables of 2 fp16
+                            features only; speed only, never a result): > 0
+                            that many (hashed levels only), < 0 none, 0 the
+                            library's choice (the three finest, among the
+                            hashed levels finer than a ray's sample spacing) */
 } mixrt_create_info;
 
 /* The coarse-mesh hit per pixel (Fig. 2 step 1): rasterisation output. */
@@ -229,15 +236,16 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
                  const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
 
 /* The persistent grid (blocks of 256 threads), the tile-order stripe width
- * (tiles; the image's tile columns for row-major order) and the samples per
- * ray per round (0: all K at once) that mixrt_render would launch for these
- * descriptors on this context; nothing is enqueued.  blocks, tile_stripe,
- * chunk: host int32. */
+ * (tiles; the image's tile columns for row-major order), the samples per ray
+ * per round (0: all K at once) and the first level gathered in 16-byte
+ * blocks (L: none) that mixrt_render would launch for these descriptors on
+ * this context; nothing is enqueued.  blocks, tile_stripe, chunk,
+ * block_from: host int32 (block_from may be NULL). */
 int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
                               const mixrt_camera *cams, const mixrt_disp_tex *disp,
                               const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
                               const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe,
-                              int32_t *chunk);
+                              int32_t *chunk, int32_t *block_from);
 
 /* ---- stage entry points (the same device code as mixrt_render) ------------ */
 

@@ -63,13 +63,19 @@ int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
  * most K) replays the early-termination path with rounds of chunk samples
  * as it runs when every ray hits and none stops (runs of K/chunk tiles per
  * wave, lane s*chunk + j on sample c*chunk + j of the run's ray s in round
- * c).  N: host int32 [L], the level resolutions (non-decreasing).  sink:
- * device uint32 [blocks*256] (written). */
+ * c).  block_from: hashed levels from this one on (4-byte entries only) are
+ * gathered as the render kernel gathers them there, one aligned 16-byte
+ * block per x-neighbour corner pair plus the x + 1 entries of voxels that
+ * straddle two blocks, one level per batch (as returned by
+ * mixrt_render_launch_shape; L: none).  N: host int32 [L], the level
+ * resolutions (non-decreasing).  sink: device uint32 [blocks*256]
+ * (written); with mode 0 the XOR over all of it is the XOR of the 8 corner
+ * entries of every level of every hit sample. */
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
-                           int32_t chunk, int32_t mode, int32_t blocks, uint32_t *sink,
-                           void *stream);
+                           int32_t chunk, int32_t block_from, int32_t mode, int32_t blocks,
+                           uint32_t *sink, void *stream);
 
 /* Properties of HIP device `device` the measurements are quoted against:
  * peak shader clock (kHz), memory clock (kHz), compute units, L2 bytes, and

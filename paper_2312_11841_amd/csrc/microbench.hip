@@ -165,8 +165,9 @@ __global__ __launch_bounds__(kBlock) void mfma_kernel(int iters, float *__restri
 // mapping and tile order (stripe) as the render kernel; a lane takes the
 // same sample of the same tile, reads that sample's position from the frame's
 // ray-setup output, and issues the same loads in the same batches (dense
-// levels as x-neighbour pairs, two levels per batch).  The loaded words are
-// XOR-folded into one word per lane (no fp16 conversion, no interpolation,
+// levels as x-neighbour pairs, hashed levels of 4-byte entries as 16-byte
+// blocks per x-neighbour pair, two levels per batch).  The corner entries'
+// words are XOR-folded into one word per lane (no fp16 conversion, no interpolation,
 // no MLP, no compositing), so the kernel's time is the floor that this exact
 // access stream, plus the address arithmetic that produces it, sets.  MODE 1
 // drops the loads and folds the offsets instead (the address arithmetic
@@ -209,7 +210,7 @@ template <> struct RawEntry<16> {
     }
 };
 
-template <uint32_t EB, int G, bool DENSE, int MODE>
+template <uint32_t EB, int G, bool DENSE, int MODE, bool BLOCKS = false>
 __device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, int l0, float x0,
                                                  float x1, float x2)
 {
@@ -217,10 +218,30 @@ __device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, in
 #pragma unroll
     for (int g = 0; g < G; ++g)
         mixrt::level_setup<EB, true>(gp, l0 + g, DENSE, x0, x1, x2, s[g]);
+    // hashed levels with 4-byte entries from block_from on: the render's
+    // block loads (one aligned 16-byte block per x-neighbour pair, the x + 1
+    // entries loaded apart where the voxel straddles two blocks), and the
+    // two words picked
+    constexpr bool kBlocks = BLOCKS && !DENSE && EB == 4;
     uint32_t v[G][8];
+    uint4 blk[G][4];
+    uint32_t far[G][4];
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         const char *t = (const char *)gp.table + (size_t)(l0 + g) * ((size_t)gp.T_mask + 1) * EB;
+        if (kBlocks && MODE == 0) {
+            const bool straddle = (s[g].off[0] ^ s[g].off[1]) >= 16u;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                blk[g][q] = *(const uint4 *)(t + (s[g].off[2 * q] & ~15u));
+                far[g][q] = 0u;
+            }
+            if (straddle) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) far[g][q] = RawEntry<EB>::one(t, s[g].off[2 * q + 1]);
+            }
+            continue;
+        }
 #pragma unroll
         for (int b = 0; b < 8; ++b) {
             if (DENSE && (b & 1)) continue;   // a dense pair covers corners b and b + 1
@@ -232,10 +253,20 @@ __device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, in
     }
     uint32_t acc = 0;
 #pragma unroll
-    for (int g = 0; g < G; ++g)
+    for (int g = 0; g < G; ++g) {
+        if (kBlocks && MODE == 0) {
+            const bool straddle = (s[g].off[0] ^ s[g].off[1]) >= 16u;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                acc ^= mixrt::block_word(blk[g][q], s[g].off[2 * q]);
+                acc ^= straddle ? far[g][q] : mixrt::block_word(blk[g][q], s[g].off[2 * q + 1]);
+            }
+            continue;
+        }
 #pragma unroll
         for (int b = 0; b < 8; ++b)
             if (!(DENSE && (b & 1))) acc ^= v[g][b];
+    }
     return acc;
 }
 
@@ -286,8 +317,10 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
         int l = 0;
         for (; l + kGroup <= n_dense; l += kGroup) acc ^= replay_group<EB, kGroup, true, MODE>(gp, l, x0, x1, x2);
         for (; l < n_dense; ++l) acc ^= replay_group<EB, 1, true, MODE>(gp, l, x0, x1, x2);
-        for (; l + kGroup <= L; l += kGroup) acc ^= replay_group<EB, kGroup, false, MODE>(gp, l, x0, x1, x2);
-        for (; l < L; ++l) acc ^= replay_group<EB, 1, false, MODE>(gp, l, x0, x1, x2);
+        const int lb = EB == 4 && gp.block_from < L ? max(gp.block_from, l) : L;
+        for (; l + kGroup <= lb; l += kGroup) acc ^= replay_group<EB, kGroup, false, MODE>(gp, l, x0, x1, x2);
+        for (; l < lb; ++l) acc ^= replay_group<EB, 1, false, MODE>(gp, l, x0, x1, x2);
+        for (; l < L; ++l) acc ^= replay_group<EB, 1, false, MODE, true>(gp, l, x0, x1, x2);
     }
     sink[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
 }
@@ -299,8 +332,8 @@ extern "C" {
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
-                           int32_t chunk, int32_t mode, int32_t blocks, uint32_t *sink,
-                           void *stream)
+                           int32_t chunk, int32_t block_from, int32_t mode, int32_t blocks,
+                           uint32_t *sink, void *stream)
 {
     if (!x || !hit || !table || !N || !sink) return hipErrorInvalidValue;
     if (chunk < 0 || chunk > K || (chunk > 0 && (64 % chunk != 0 || (chunk & (chunk - 1)))))
@@ -318,6 +351,7 @@ int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, in
     gp.log2_T = (uint32_t)log2_T;
     gp.T_mask = (uint32_t)((1u << log2_T) - 1u);
     gp.L = L;
+    gp.block_from = block_from < 0 ? 0 : block_from > L ? L : block_from;
     const uint64_t T = 1ull << log2_T;
     for (int l = 0; l < L; ++l) {
         if (N[l] < 1 || N[l] > (1 << 20) || (l > 0 && N[l] < N[l - 1])) return hipErrorInvalidValue;

@@ -25,6 +25,7 @@ struct mixrt_ctx {
     uint32_t flags = 0;
     int32_t tile_stripe = 0;
     int32_t early_stop_chunk = 0;
+    int32_t block_levels = 0;
     int cus = 0;
     int64_t l2_bytes = 0;
     std::string err;
@@ -324,6 +325,7 @@ void fill_grid_params(mixrt::GridParams &gp, const mixrt_hash_grid *g)
     gp.log2_T = (uint32_t)g->log2_T;
     gp.T_mask = (uint32_t)((1ull << g->log2_T) - 1);
     gp.L = g->L;
+    gp.block_from = g->L;   // no block gathers unless the render launch picks some
     int32_t N[MIXRT_MAX_LEVELS];
     level_table(g->L, g->N_min, g->N_max, N);
     const uint64_t T = 1ull << g->log2_T;
@@ -633,6 +635,7 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     ctx->flags = ci->flags;
     ctx->tile_stripe = ci->tile_stripe;
     ctx->early_stop_chunk = ci->early_stop_chunk;
+    ctx->block_levels = ci->block_levels;
     ctx->cus = prop.multiProcessorCount;
     ctx->l2_bytes = prop.l2CacheSize;
     *out = ctx;
@@ -683,6 +686,7 @@ void fill_render_launch(mixrt::RenderLaunch &L, const mixrt_ctx *ctx, const mixr
     L.blocks_mode = (ctx->flags & MIXRT_FLAG_BLOCKS_FULL) ? 1 : (ctx->flags & MIXRT_FLAG_BLOCKS_TWO) ? 2 : 0;
     L.tile_stripe = ctx->tile_stripe;
     L.chunk = ctx->early_stop_chunk;
+    L.block_levels = ctx->block_levels;
 }
 
 }  // namespace
@@ -709,7 +713,7 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
                               const mixrt_camera *cams, const mixrt_disp_tex *disp,
                               const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
                               const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe,
-                              int32_t *chunk)
+                              int32_t *chunk, int32_t *block_from)
 {
     if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
     clear_err(ctx);
@@ -722,13 +726,14 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
     if ((rc = bind_device(ctx))) return rc;
     mixrt::RenderLaunch L;
     fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, nullptr);
-    int b = 0, st = 0, ch = 0;
-    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch);
+    int b = 0, st = 0, ch = 0, bf = 0;
+    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch, &bf);
     if (e != hipSuccess)
         return fail(ctx, MIXRT_EDEVICE, "render launch shape: %s", hipGetErrorString(e));
     *blocks = b;
     *tile_stripe = st;
     *chunk = ch;
+    if (block_from) *block_from = bf;
     return MIXRT_OK;
 }
 

@@ -63,6 +63,8 @@ struct GridParams {
     uint32_t N[kMaxLevels];
     float Nf[kMaxLevels];   // N as float, and N - 1 (exact: N <= 2^20), so
     float Ntop[kMaxLevels]; // that no lane converts them
+    int32_t block_from;     // levels from here on load x-neighbour corner pairs
+                            // as 16-byte blocks (4-byte entries; L: none)
 };
 
 // --------------------------------------------------------------------------
@@ -468,11 +470,15 @@ struct TableEntry;
 template <>
 struct TableEntry<2, true> {
     static constexpr uint32_t kBytes = 4;
-    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
+    static __device__ __forceinline__ void from_word(uint32_t w, float *v)
     {
-        const h2 h = __builtin_bit_cast(h2, *(const uint32_t *)(t + off));
+        const h2 h = __builtin_bit_cast(h2, w);
         v[0] = (float)h.x;
         v[1] = (float)h.y;
+    }
+    static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
+    {
+        from_word(*(const uint32_t *)(t + off), v);
     }
 };
 
@@ -650,17 +656,64 @@ __device__ __forceinline__ float corner_weight(const LevelSetup &s, int b)
     return w0 * w1 * w2;
 }
 
+// Word i of an aligned 16-byte block, i = bits 2-3 of the entry's byte
+// offset, picked with bit masks (as selects, the compiler turns the pick
+// into an indexed read of a private copy of the block)
+__device__ __forceinline__ uint32_t block_word(const uint4 &q, uint32_t off)
+{
+    const uint32_t m8 = (uint32_t)((int32_t)(off << 28) >> 31);   // bit 3 set: all ones
+    const uint32_t m4 = (uint32_t)((int32_t)(off << 29) >> 31);   // bit 2 set: all ones
+    const uint32_t lo = (q.z & m8) | (q.x & ~m8);
+    const uint32_t hi = (q.w & m8) | (q.y & ~m8);
+    return (hi & m4) | (lo & ~m4);
+}
+
+// Whether a hashed level's x-neighbour corners (2q, 2q + 1) can share one
+// aligned 16-byte block: 4-byte entries only.  The hash multiplies x by one,
+// so the entries of x and x + 1 differ in the index bits that x and x + 1
+// differ in: bits 0-1 (the same block) unless x = 3 (mod 4).
+template <int F, bool F16>
+constexpr bool kBlockPairs = TableEntry<F, F16>::kBytes == 4;
+
 // The 8 corner entries of a level: 4 pair loads on a dense level, 8 single
-// loads on a hashed one.
-template <int F, bool F16, bool DENSE>
+// loads on a hashed one.  BLOCKS (hashed levels of 4-byte entries): one
+// 16-byte block load per x-neighbour pair, which holds both entries in 3
+// voxels of 4, plus a load of each x + 1 entry in the lanes whose voxel
+// straddles two blocks: 4 full gathers and 4 partial ones instead of 8 full
+// ones.  The vector L1 charges a scattered gather by the lanes and distinct
+// lines it touches whatever its width, so this pays on levels whose lanes
+// touch distinct lines (the finest); where lanes share lines a 16-byte
+// gather costs more than a 4-byte one and the word picks cost ALU work.
+template <int F, bool F16, bool DENSE, bool BLOCKS = false>
 __device__ __forceinline__ void level_fetch(const void *table_l, const LevelSetup &s,
                                             float (*v)[F])
 {
     const char *t = (const char *)table_l;
-    if (DENSE) {
+    if constexpr (DENSE) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
             TablePair<F, F16>::load(t, s.off[2 * q], v[2 * q], v[2 * q + 1]);
+    } else if constexpr (BLOCKS && kBlockPairs<F, F16>) {
+        // the pairs' offsets differ by the same x part (the y and z parts
+        // cancel), so one test serves all four
+        const bool straddle = (s.off[0] ^ s.off[1]) >= 16u;
+        uint4 blk[4];
+        uint32_t far[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            blk[q] = *(const uint4 *)(t + (s.off[2 * q] & ~15u));
+        if (straddle) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                far[q] = *(const uint32_t *)(t + s.off[2 * q + 1]);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint32_t w0 = block_word(blk[q], s.off[2 * q]);
+            const uint32_t w1 = straddle ? far[q] : block_word(blk[q], s.off[2 * q + 1]);
+            TableEntry<F, F16>::from_word(w0, v[2 * q]);
+            TableEntry<F, F16>::from_word(w1, v[2 * q + 1]);
+        }
     } else {
 #pragma unroll
         for (int b = 0; b < 8; ++b)
@@ -693,7 +746,7 @@ __device__ __forceinline__ const void *level_base(const GridParams &g, int l, in
 // G consecutive levels starting at l0, all of one kind (dense or hashed):
 // every corner load of the group is issued before any interpolation, so a
 // wave keeps 4G (dense) or 8G (hashed) gathers in flight.
-template <int F, bool F16, int G, bool DENSE>
+template <int F, bool F16, int G, bool DENSE, bool BLOCKS = false>
 __device__ __forceinline__ void hash_group(const GridParams &gp, int l0, float x0, float x1,
                                            float x2, float (*feat)[F])
 {
@@ -704,7 +757,7 @@ __device__ __forceinline__ void hash_group(const GridParams &gp, int l0, float x
         level_setup<TableEntry<F, F16>::kBytes, true>(gp, l0 + g, DENSE, x0, x1, x2, s[g]);
 #pragma unroll
     for (int g = 0; g < G; ++g)
-        level_fetch<F, F16, DENSE>(level_base(gp, l0 + g, F, F16), s[g], v[g]);
+        level_fetch<F, F16, DENSE, BLOCKS>(level_base(gp, l0 + g, F, F16), s[g], v[g]);
 #pragma unroll
     for (int g = 0; g < G; ++g)
         level_accumulate<F>(s[g], v[g], feat[g]);

@@ -75,6 +75,8 @@ struct RenderLaunch {
     int blocks_mode;    // 0: by the gathers' line sharing, 1: all that fit, 2: two per CU
     int tile_stripe;    // > 0: stripe width of the tile order in tiles; <= 0: the default
     int chunk;          // > 0: early-termination path with this many samples per round
+    int block_levels;   // finest levels with 16-byte block gathers: > 0 that many,
+                        // < 0 none, 0 the default rule
 };
 
 bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid);
@@ -85,8 +87,10 @@ hipError_t launch_render(const RenderLaunch &L, hipStream_t stream);
 // mixrt_render.hip), after waiting for the device; hipErrorNotSupported in
 // other builds.
 hipError_t phase_cycles_read(uint64_t *out, bool reset);
-// The grid size and tile-order stripe launch_render would use (no launch).
-hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk);
+// The grid size, tile-order stripe, samples per round and first level of
+// 16-byte block gathers launch_render would use (no launch).
+hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk,
+                               int *block_from);
 hipError_t launch_ray_setup(const RayParams &rp, int tex, float *out_x, int32_t *out_hit,
                             hipStream_t stream);
 hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const float *x, int64_t n,

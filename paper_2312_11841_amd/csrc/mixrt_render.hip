@@ -49,12 +49,12 @@ __device__ unsigned long long phase_cycles[8];
 
 // G levels of one query: into its fp16 row of MLP inputs, or (the MLP
 // removed) added in fp32 to the per-component sums acc[(l F + i) mod 4].
-template <int F, bool TF16, int G, bool DENSE, bool SUM>
+template <int F, bool TF16, int G, bool DENSE, bool SUM, bool BLOCKS = false>
 __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, float x0, float x1,
                                               float x2, _Float16 *row, float *acc)
 {
     float f[G][F];
-    hash_group<F, TF16, G, DENSE>(gp, l0, x0, x1, x2, f);
+    hash_group<F, TF16, G, DENSE, BLOCKS>(gp, l0, x0, x1, x2, f);
 #pragma unroll
     for (int g = 0; g < G; ++g) {
         if (SUM) {
@@ -71,6 +71,31 @@ __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, floa
             for (int i = 0; i < F; i += 2)
                 *(h2 *)(row + (l0 + g) * F + i) = h2{(_Float16)f[g][i], (_Float16)f[g][i + 1]};
         }
+    }
+}
+
+// Every level of one query in order: dense levels, hashed levels with
+// single-entry gathers, then hashed levels from gp.block_from on with
+// 16-byte block gathers (4-byte entries), one level per batch there (two
+// levels' blocks in flight would cost a wave of occupancy).
+template <int F, bool TF16, bool SUM>
+__device__ __forceinline__ void encode_query(const GridParams &gp, float x0, float x1, float x2,
+                                             _Float16 *row, float *acc)
+{
+    const int L = gp.L, n_dense = gp.n_dense;
+    int l = 0;
+    for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
+        encode_levels<F, TF16, kLevelGroup, true, SUM>(gp, l, x0, x1, x2, row, acc);
+    for (; l < n_dense; ++l)
+        encode_levels<F, TF16, 1, true, SUM>(gp, l, x0, x1, x2, row, acc);
+    const int lb = kBlockPairs<F, TF16> && gp.block_from < L ? max(gp.block_from, l) : L;
+    for (; l + kLevelGroup <= lb; l += kLevelGroup)
+        encode_levels<F, TF16, kLevelGroup, false, SUM>(gp, l, x0, x1, x2, row, acc);
+    for (; l < lb; ++l)
+        encode_levels<F, TF16, 1, false, SUM>(gp, l, x0, x1, x2, row, acc);
+    if constexpr (kBlockPairs<F, TF16>) {
+        for (; l < L; ++l)
+            encode_levels<F, TF16, 1, false, SUM, true>(gp, l, x0, x1, x2, row, acc);
     }
 }
 
@@ -116,7 +141,6 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     const int r_loc = lane / K;
     const int k = lane - r_loc * K;
     const int L = gp.L;
-    const int n_dense = gp.n_dense;
 #ifdef MIXRT_PHASE_TIMER
     uint64_t ph[4] = {0, 0, 0, 0}, n_tiles_done = 0, n_samples = 0;
     uint64_t t_last = __builtin_readcyclecounter();
@@ -155,15 +179,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
 #else
         if (hit) {
 #endif
-            int l = 0;
-            for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
-                encode_levels<F, TF16, kLevelGroup, true, SUM>(gp, l, x0, x1, x2, row, acc);
-            for (; l < n_dense; ++l)
-                encode_levels<F, TF16, 1, true, SUM>(gp, l, x0, x1, x2, row, acc);
-            for (; l + kLevelGroup <= L; l += kLevelGroup)
-                encode_levels<F, TF16, kLevelGroup, false, SUM>(gp, l, x0, x1, x2, row, acc);
-            for (; l < L; ++l)
-                encode_levels<F, TF16, 1, false, SUM>(gp, l, x0, x1, x2, row, acc);
+            encode_query<F, TF16, SUM>(gp, x0, x1, x2, row, acc);
         } else if (!SUM) {
             for (int e = 0; e < L * F; e += 2)
                 *(h2 *)(row + e) = h2{(_Float16)0.0f, (_Float16)0.0f};
@@ -297,7 +313,6 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
     const int total = gridDim.x * kWavesPerBlock;
     const int NS = kWave / C;               // ray slots
     const int L = gp.L;
-    const int n_dense = gp.n_dense;
 
     // slot state of the owner lanes s < NS
     int s_ray = -1, s_kn = 0, s_view = 0;
@@ -391,15 +406,7 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
 #else
         if (live) {
 #endif
-            int l = 0;
-            for (; l + kLevelGroup <= n_dense; l += kLevelGroup)
-                encode_levels<F, TF16, kLevelGroup, true, SUM>(gp, l, x0, x1, x2, row, acc);
-            for (; l < n_dense; ++l)
-                encode_levels<F, TF16, 1, true, SUM>(gp, l, x0, x1, x2, row, acc);
-            for (; l + kLevelGroup <= L; l += kLevelGroup)
-                encode_levels<F, TF16, kLevelGroup, false, SUM>(gp, l, x0, x1, x2, row, acc);
-            for (; l < L; ++l)
-                encode_levels<F, TF16, 1, false, SUM>(gp, l, x0, x1, x2, row, acc);
+            encode_query<F, TF16, SUM>(gp, x0, x1, x2, row, acc);
         } else if (!SUM) {
             for (int e = 0; e < L * F; e += 2)
                 *(h2 *)(row + e) = h2{(_Float16)0.0f, (_Float16)0.0f};
@@ -589,6 +596,29 @@ static int render_chunk(const RenderLaunch &L)
     return c;
 }
 
+// First level whose x-neighbour corner pairs are gathered as 16-byte
+// blocks (gp.L: none; tables of 4-byte entries only).  By default the three
+// finest levels, among the hashed levels finer than a ray's sample spacing
+// (coarser levels hand a ray's neighbouring samples the same lines, where a
+// 4-byte gather is cheaper).  Measured against single-entry gathers on every
+// level: the finest 2 or 4 levels were 2-15% faster at 720p (K 1 to 16,
+// spacings 0.01 to 0.25, early termination or not) and on the 8-view 1080p
+// batch, 1-5% slower only at K = 32 on a 4096-pixel-wide view; all hashed
+// levels (or every level finer than the spacing) were slower on most.
+static int render_block_from(const RenderLaunch &L)
+{
+    const int nl = L.gp.L;
+    if (!(L.tf16 && L.F == 2) || L.block_levels < 0) return nl;
+    int lo = L.gp.n_dense;
+    if (L.block_levels > 0) return nl - L.block_levels > lo ? nl - L.block_levels : lo;
+    constexpr int kFinest = 3;
+    if (L.rp.K > 1) {
+        const int shared = levels_shared_by_samples(L);
+        if (shared > lo) lo = shared;
+    }
+    return nl - kFinest > lo ? nl - kFinest : (lo < nl ? lo : nl);
+}
+
 // Grid size and tile order of a frame, given the blocks of its kernel that
 // fit on one CU.
 static void render_shape(const RenderLaunch &L, int resident, int64_t &blocks, int &stripe)
@@ -617,8 +647,10 @@ static int render_resident(bool queue)
 #define MIXRT_RENDER_MATCH(a, b, c, d, e, f) \
     (L.tex == a && L.F == b && L.tf16 == c && L.nhid == f && (f == 0 || (L.in == d && L.hid == e)))
 
-hipError_t launch_render(const RenderLaunch &L, hipStream_t stream)
+hipError_t launch_render(const RenderLaunch &L0, hipStream_t stream)
 {
+    RenderLaunch L = L0;
+    L.gp.block_from = render_block_from(L);
 #define X(a, b, c, d, e, f)                                                                    \
     if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
         int64_t blocks;                                                                        \
@@ -657,8 +689,10 @@ hipError_t phase_cycles_read(uint64_t *out, bool reset)
 #endif
 }
 
-hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk)
+hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk,
+                               int *block_from)
 {
+    *block_from = render_block_from(L);
 #define X(a, b, c, d, e, f)                                                                    \
     if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
         int64_t nb;                                                                            \

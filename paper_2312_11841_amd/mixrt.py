@@ -56,7 +56,8 @@ class MixrtError(RuntimeError):
 
 class CreateInfo(C.Structure):
     _fields_ = [("device", C.c_int32), ("hip_stream", C.c_void_p), ("flags", C.c_uint32),
-                ("tile_stripe", C.c_int32), ("early_stop_chunk", C.c_int32)]
+                ("tile_stripe", C.c_int32), ("early_stop_chunk", C.c_int32),
+                ("block_levels", C.c_int32)]
 
 
 class GBuffer(C.Structure):
@@ -136,7 +137,7 @@ def lib(variant=None):
                                                     C.POINTER(DispTex), C.POINTER(HashGrid),
                                                     C.POINTER(Mlp), C.POINTER(Sampling),
                                                     C.POINTER(C.c_int32), C.POINTER(C.c_int32),
-                                                    C.POINTER(C.c_int32)]),
+                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
             "mixrt_debug_phase_cycles": (C.c_int, [P, P, C.c_int]),
             "mixrt_debug_ray_setup": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                 C.POINTER(DispTex), C.POINTER(Sampling), P, P]),
@@ -397,13 +398,16 @@ class Renderer:
     """One mixrt context bound to a device and a HIP stream."""
 
     def __init__(self, device: int = 0, stream=None, sync_check: bool = False, blocks=None,
-                 tile_stripe: int = 0, early_stop_chunk: int = 0, variant=None):
+                 tile_stripe: int = 0, early_stop_chunk: int = 0, block_levels: int = 0,
+                 variant=None):
         """blocks: None (the library's choice), "full" or "two": the render
         kernel's persistent blocks per CU; tile_stripe: 0 (the library's
         choice), > 0 stripes of that many tiles, < 0 row-major (the order in
         which waves take tiles); early_stop_chunk: 0 (the library's choice),
         < 0 every sample of a ray at once (the tile path), > 0 front to back
-        in rounds of that many samples with stopped rays dropped.  They
+        in rounds of that many samples with stopped rays dropped;
+        block_levels: 0 (the library's choice), > 0 that many finest levels
+        gather x-neighbour corner pairs as 16-byte blocks, < 0 none.  They
         change speed only, never a result.
         variant: None (libmixrt.so) or a profiling build (see lib())."""
         import torch
@@ -413,7 +417,7 @@ class Renderer:
         self.stream = stream
         ci = CreateInfo(device, C.c_void_p(int(stream.cuda_stream)),
                         (MIXRT_FLAG_SYNC_CHECK if sync_check else 0) | _BLOCKS[blocks],
-                        int(tile_stripe), int(early_stop_chunk))
+                        int(tile_stripe), int(early_stop_chunk), int(block_levels))
         self._L = lib(variant)
         h = C.c_void_p()
         rc = self._L.mixrt_create(C.byref(h), C.byref(ci))
@@ -464,11 +468,22 @@ class Renderer:
     def launch_shape(self, ds: DeviceScene, chunk: bool = False):
         """(blocks, tile stripe) that render(ds) launches, and with chunk=True
         also its samples per ray per round (0: the tile path)."""
-        b, st, ch = C.c_int32(), C.c_int32(), C.c_int32()
+        p = self.launch_plan(ds)
+        out = (p["blocks"], p["tile_stripe"], p["chunk"])
+        return out if chunk else out[:2]
+
+    def launch_plan(self, ds: DeviceScene) -> dict:
+        """Everything mixrt_render_launch_shape reports for render(ds):
+        blocks, tile_stripe, chunk (samples per ray per round, 0: the tile
+        path) and block_from (first level gathered in 16-byte blocks, L:
+        none)."""
+        b, st, ch, bf = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32()
         self._check(self._L.mixrt_render_launch_shape(
             self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp), C.byref(ds.grid),
-            C.byref(ds.mlp), C.byref(ds.smp), C.byref(b), C.byref(st), C.byref(ch)))
-        return (b.value, st.value, ch.value) if chunk else (b.value, st.value)
+            C.byref(ds.mlp), C.byref(ds.smp), C.byref(b), C.byref(st), C.byref(ch),
+            C.byref(bf)))
+        return {"blocks": b.value, "tile_stripe": st.value, "chunk": ch.value,
+                "block_from": bf.value}
 
     # -- geometry
     def raycast(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):

@@ -1,6 +1,7 @@
 """GPU checks of what changes the render kernel's speed but never its result:
 the tile order (stripes of tiles per XCD), the early-termination path (rays
-evaluated front to back in rounds, stopped rays dropped), the profiling
+evaluated front to back in rounds, stopped rays dropped), the 16-byte block
+gathers of x-neighbour corner pairs on the finest levels, the profiling
 builds that time the kernel's phases, and the gather-replay microbenchmark
 that measures the floor of its gather stream.
 
@@ -8,6 +9,8 @@ that measures the floor of its gather stream.
   - the early-termination path renders the tile path's frame bit for bit
     (the same samples composited in the same order), at every round size,
     and evaluates fewer samples on opaque content;
+  - block gathers on any set of finest levels render the same frame bit for
+    bit as single-entry gathers;
   - the phase-timer build renders the same frame as the library, and its
     counters cover every tile of every launch;
   - the replay loads exactly the table entries of the oracle's corner
@@ -135,18 +138,73 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
     for l in range(cfg.L):
         w = words[l][idx[:, l, :].reshape(-1)]
         acc ^= np.bitwise_xor.reduce(w.reshape(-1))
-    # the tile path's order and every rounds order the render can take
-    for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
-        sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
-        rc = mb.lib().mixrt_mb_gather_replay(
-            x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K,
-            ds.table.data_ptr(), cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F,
-            N.ctypes.data, stripe, chunk, 0, blocks, sink.data_ptr(), None)
-        assert rc == 0
-        torch.cuda.synchronize()
-        got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
-        assert got == acc, chunk
+    # the tile path's order and every rounds order the render can take, with
+    # the render's 16-byte block gathers on none, the library's choice, all
+    # hashed levels (4-byte entries only; other entry sizes ignore it)
+    plan = r.launch_plan(ds)
+    n_dense = int(sum((N.astype(np.int64) + 1) ** 3 <= cfg.T))
+    for block_from in sorted({cfg.L, plan["block_from"], n_dense, 0}):
+        for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
+            sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
+            rc = mb.lib().mixrt_mb_gather_replay(
+                x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K,
+                ds.table.data_ptr(), cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F,
+                N.ctypes.data, stripe, chunk, block_from, 0, blocks, sink.data_ptr(), None)
+            assert rc == 0
+            torch.cuda.synchronize()
+            got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+            assert got == acc, (block_from, chunk)
     r.close()
+
+
+BLOCK_CFGS = [
+    synth.VIEW720P.replace(name="blk_720p_rows", rows=64),
+    synth.VIEW720P_DENSE.replace(name="blk_dense_rows", rows=64),
+    synth.OPAQUE720P.replace(name="blk_opaque_rows", rows=64),
+    synth.VIEW720P.replace(name="blk_k1", K=1, rows=96),
+    synth.VIEW720P.replace(name="blk_ragged", H=23, W=37, views=2, K=3, gbuf="iid",
+                           delta=0.5, log2_T=12, N_max=2048),
+]
+
+
+@pytest.mark.parametrize("cfg", BLOCK_CFGS, ids=lambda c: c.name)
+def test_block_gathers_give_the_same_frame(cfg):
+    """16-byte block gathers of x-neighbour corner pairs read the same two
+    entries as single gathers: every choice of levels renders the same bits,
+    on the tile path and in rounds."""
+    say("block gathers", cfg.name)
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    ref = None
+    seen = set()
+    for chunk in (-1, 0):
+        for levels in (-1, 0, 1, 3, cfg.L):
+            r = mixrt.Renderer(0, sync_check=True, early_stop_chunk=chunk, block_levels=levels)
+            seen.add(r.launch_plan(ds)["block_from"])
+            out = torch.full((ds.rays, 4), float("nan"), dtype=torch.float32, device="cuda:0")
+            r.render(ds, out)
+            r.sync()
+            r.close()
+            got = out.cpu().numpy()
+            assert np.isfinite(got).all()
+            if ref is None:
+                ref = got
+            assert np.array_equal(got, ref), (chunk, levels)
+    say(f"  first block levels launched: {sorted(seen)}")
+    assert len(seen) >= 3
+
+
+def test_block_gathers_spot_check_against_the_oracle():
+    cfg = BLOCK_CFGS[1]
+    sc = synth.make_scene(cfg)
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    r = mixrt.Renderer(0, sync_check=True, block_levels=cfg.L)
+    assert r.launch_plan(ds)["block_from"] < cfg.L
+    got = r.render(ds).cpu().numpy()
+    r.close()
+    pix = np.random.default_rng(5).choice(cfg.rays, 2000, replace=False)
+    ref = oracle.OracleScene(sc).render_pixels(pix, threads=oracle.max_threads())
+    assert np.abs(got[pix] - ref).max() <= 2e-3
 
 
 @pytest.mark.parametrize("cfg", [synth.VIEW720P, synth.VIEW720P_DENSE,
