@@ -128,10 +128,11 @@ def gather_replay_floor(cfg, ds, renderer):
     N = mixrt.level_resolutions(ds.grid)
     grids = sorted({blocks} | {k * cus for k in (1, 2, 3, 4, 6, 8)})
     r = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N, stripe,
-                         grids, chunk=chunk, block_from=plan["block_from"])
+                         grids, chunk=chunk, block_from=plan["block_from"],
+                         hash_batch=plan["hash_batch"])
     del x, hit
     return {"render_blocks": blocks, "tile_stripe": stripe, "early_stop_chunk": chunk,
-            "block_from": plan["block_from"], **r}
+            "block_from": plan["block_from"], "hash_batch": plan["hash_batch"], **r}
 
 
 def stage_metrics(cfg, ds, out, steps, chunk=0):
@@ -645,7 +646,8 @@ def main():
             "samples": cfg.samples,
             "parallelism": "single GPU",
             "launch": {"blocks": plan["blocks"], "tile_stripe": plan["tile_stripe"],
-                       "early_stop_chunk": plan["chunk"], "block_from": plan["block_from"]},
+                       "early_stop_chunk": plan["chunk"], "block_from": plan["block_from"],
+                       "hash_batch": plan["hash_batch"]},
         },
         "roofline": roofline,
         **stage_fields,

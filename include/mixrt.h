@@ -235,17 +235,23 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
                  const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
                  const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
 
-/* The persistent grid (blocks of 256 threads), the tile-order stripe width
- * (tiles; the image's tile columns for row-major order), the samples per ray
- * per round (0: all K at once) and the first level gathered in 16-byte
- * blocks (L: none) that mixrt_render would launch for these descriptors on
- * this context; nothing is enqueued.  blocks, tile_stripe, chunk,
- * block_from: host int32 (block_from may be NULL). */
+/* How mixrt_render launches a frame (none of it changes a result). */
+typedef struct {
+    int32_t blocks;      /* persistent grid, blocks of 256 threads */
+    int32_t tile_stripe; /* tile-order stripe width in tiles (the image's tile
+                            columns for row-major order) */
+    int32_t chunk;       /* samples per ray per round (0: all K at once) */
+    int32_t block_from;  /* first hash level whose x-neighbour corner pairs
+                            are gathered as 16-byte blocks (L: none) */
+    int32_t hash_batch;  /* hashed levels per batch of gathers (2 or 4) */
+} mixrt_launch_plan;
+
+/* The launch mixrt_render would make for these descriptors on this
+ * context; nothing is enqueued.  plan: host, written on success. */
 int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
                               const mixrt_camera *cams, const mixrt_disp_tex *disp,
                               const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
-                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe,
-                              int32_t *chunk, int32_t *block_from);
+                              const mixrt_sampling *smp, mixrt_launch_plan *plan);
 
 /* ---- stage entry points (the same device code as mixrt_render) ------------ */
 

@@ -67,15 +67,17 @@ int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
  * gathered as the render kernel gathers them there, one aligned 16-byte
  * block per x-neighbour corner pair plus the x + 1 entries of voxels that
  * straddle two blocks, one level per batch (as returned by
- * mixrt_render_launch_shape; L: none).  N: host int32 [L], the level
+ * mixrt_render_launch_shape; L: none); hash_batch: hashed levels per batch
+ * of the other gathers, 2 or 4 (4 only for entries of 8 or more bytes, as
+ * the render kernel batches them).  N: host int32 [L], the level
  * resolutions (non-decreasing).  sink: device uint32 [blocks*256]
  * (written); with mode 0 the XOR over all of it is the XOR of the 8 corner
  * entries of every level of every hit sample. */
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
-                           int32_t chunk, int32_t block_from, int32_t mode, int32_t blocks,
-                           uint32_t *sink, void *stream);
+                           int32_t chunk, int32_t block_from, int32_t hash_batch,
+                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream);
 
 /* Properties of HIP device `device` the measurements are quoted against:
  * peak shader clock (kHz), memory clock (kHz), compute units, L2 bytes, and

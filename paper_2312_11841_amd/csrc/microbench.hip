@@ -318,6 +318,8 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
         for (; l + kGroup <= n_dense; l += kGroup) acc ^= replay_group<EB, kGroup, true, MODE>(gp, l, x0, x1, x2);
         for (; l < n_dense; ++l) acc ^= replay_group<EB, 1, true, MODE>(gp, l, x0, x1, x2);
         const int lb = EB == 4 && gp.block_from < L ? max(gp.block_from, l) : L;
+        if (EB >= 8 && gp.hash_batch >= 4)
+            for (; l + 4 <= lb; l += 4) acc ^= replay_group<EB, 4, false, MODE>(gp, l, x0, x1, x2);
         for (; l + kGroup <= lb; l += kGroup) acc ^= replay_group<EB, kGroup, false, MODE>(gp, l, x0, x1, x2);
         for (; l < lb; ++l) acc ^= replay_group<EB, 1, false, MODE>(gp, l, x0, x1, x2);
         for (; l < L; ++l) acc ^= replay_group<EB, 1, false, MODE, true>(gp, l, x0, x1, x2);
@@ -332,8 +334,8 @@ extern "C" {
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
-                           int32_t chunk, int32_t block_from, int32_t mode, int32_t blocks,
-                           uint32_t *sink, void *stream)
+                           int32_t chunk, int32_t block_from, int32_t hash_batch,
+                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream)
 {
     if (!x || !hit || !table || !N || !sink) return hipErrorInvalidValue;
     if (chunk < 0 || chunk > K || (chunk > 0 && (64 % chunk != 0 || (chunk & (chunk - 1)))))
@@ -344,6 +346,7 @@ int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, in
         return hipErrorInvalidValue;
     if (entry_bytes != 4 && entry_bytes != 8 && entry_bytes != 16) return hipErrorInvalidValue;
     if ((mode != 0 && mode != 1) || blocks < 1) return hipErrorInvalidValue;
+    if (hash_batch != 2 && hash_batch != 4) return hipErrorInvalidValue;
     if (((uintptr_t)table & 15) != 0) return hipErrorInvalidValue;
     mixrt::GridParams gp;
     memset(&gp, 0, sizeof gp);
@@ -352,6 +355,7 @@ int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, in
     gp.T_mask = (uint32_t)((1u << log2_T) - 1u);
     gp.L = L;
     gp.block_from = block_from < 0 ? 0 : block_from > L ? L : block_from;
+    gp.hash_batch = hash_batch;
     const uint64_t T = 1ull << log2_T;
     for (int l = 0; l < L; ++l) {
         if (N[l] < 1 || N[l] > (1 << 20) || (l > 0 && N[l] < N[l - 1])) return hipErrorInvalidValue;

@@ -326,6 +326,7 @@ void fill_grid_params(mixrt::GridParams &gp, const mixrt_hash_grid *g)
     gp.T_mask = (uint32_t)((1ull << g->log2_T) - 1);
     gp.L = g->L;
     gp.block_from = g->L;   // no block gathers unless the render launch picks some
+    gp.hash_batch = 2;
     int32_t N[MIXRT_MAX_LEVELS];
     level_table(g->L, g->N_min, g->N_max, N);
     const uint64_t T = 1ull << g->log2_T;
@@ -712,8 +713,7 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
 int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
                               const mixrt_camera *cams, const mixrt_disp_tex *disp,
                               const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
-                              const mixrt_sampling *smp, int32_t *blocks, int32_t *tile_stripe,
-                              int32_t *chunk, int32_t *block_from)
+                              const mixrt_sampling *smp, mixrt_launch_plan *plan)
 {
     if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
     clear_err(ctx);
@@ -721,19 +721,19 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
     int hid = 0, nhid = 0;
     int rc = validate_all(gbuf, cams, disp, grid, mlp, smp, Msg{msg, sizeof msg}, &hid, &nhid);
     if (rc) return fail(ctx, rc, "%s", msg);
-    if (!blocks || !tile_stripe || !chunk)
-        return fail(ctx, MIXRT_EINVAL, "blocks, tile_stripe or chunk is NULL");
+    if (!plan) return fail(ctx, MIXRT_EINVAL, "plan is NULL");
     if ((rc = bind_device(ctx))) return rc;
     mixrt::RenderLaunch L;
     fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, nullptr);
-    int b = 0, st = 0, ch = 0, bf = 0;
-    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch, &bf);
+    int b = 0, st = 0, ch = 0, bf = 0, hb = 0;
+    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch, &bf, &hb);
     if (e != hipSuccess)
         return fail(ctx, MIXRT_EDEVICE, "render launch shape: %s", hipGetErrorString(e));
-    *blocks = b;
-    *tile_stripe = st;
-    *chunk = ch;
-    if (block_from) *block_from = bf;
+    plan->blocks = b;
+    plan->tile_stripe = st;
+    plan->chunk = ch;
+    plan->block_from = bf;
+    plan->hash_batch = hb;
     return MIXRT_OK;
 }
 

@@ -65,6 +65,8 @@ struct GridParams {
     float Ntop[kMaxLevels]; // that no lane converts them
     int32_t block_from;     // levels from here on load x-neighbour corner pairs
                             // as 16-byte blocks (4-byte entries; L: none)
+    int32_t hash_batch;     // hashed levels per batch of gathers: 2, or 4
+                            // (entries of 8 or more bytes)
 };
 
 // --------------------------------------------------------------------------

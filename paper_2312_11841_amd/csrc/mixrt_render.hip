@@ -75,9 +75,10 @@ __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, floa
 }
 
 // Every level of one query in order: dense levels, hashed levels with
-// single-entry gathers, then hashed levels from gp.block_from on with
-// 16-byte block gathers (4-byte entries), one level per batch there (two
-// levels' blocks in flight would cost a wave of occupancy).
+// single-entry gathers (gp.hash_batch levels per batch, 4 only for entries
+// of 8 or more bytes), then hashed levels from gp.block_from on with 16-byte
+// block gathers (4-byte entries), one level per batch there (two levels'
+// blocks in flight would cost a wave of occupancy).
 template <int F, bool TF16, bool SUM>
 __device__ __forceinline__ void encode_query(const GridParams &gp, float x0, float x1, float x2,
                                              _Float16 *row, float *acc)
@@ -89,6 +90,11 @@ __device__ __forceinline__ void encode_query(const GridParams &gp, float x0, flo
     for (; l < n_dense; ++l)
         encode_levels<F, TF16, 1, true, SUM>(gp, l, x0, x1, x2, row, acc);
     const int lb = kBlockPairs<F, TF16> && gp.block_from < L ? max(gp.block_from, l) : L;
+    if constexpr (TableEntry<F, TF16>::kBytes >= 8) {
+        if (gp.hash_batch >= 4)
+            for (; l + 4 <= lb; l += 4)
+                encode_levels<F, TF16, 4, false, SUM>(gp, l, x0, x1, x2, row, acc);
+    }
     for (; l + kLevelGroup <= lb; l += kLevelGroup)
         encode_levels<F, TF16, kLevelGroup, false, SUM>(gp, l, x0, x1, x2, row, acc);
     for (; l < lb; ++l)
@@ -619,6 +625,22 @@ static int render_block_from(const RenderLaunch &L)
     return nl - kFinest > lo ? nl - kFinest : (lo < nl ? lo : nl);
 }
 
+// Hashed levels per batch of gathers: 4 for entries of 8 or more bytes
+// (F = 4 fp16 and up) when one batch then covers every hashed level of a
+// query (at most 4), so a wave waits for its table once per tile instead of
+// twice; else 2.  Measured at 720p with one query per pixel: the deployed
+// grid (4 levels of 16 MiB) 5.5-8.6% faster with the Eq. 2 map, without it
+// and without the MLP.  With 8 hashed levels, batches of 4 were 6% faster
+// on 1 MiB levels without the MLP but 14% slower with the 2 x 8 MLP, 10%
+// slower on 2^5-entry levels and 1.5% faster on 16 and 32 MiB levels, so 8
+// levels keep batches of 2.  The batch changes only when loads are issued,
+// never a result.
+static int render_hash_batch(const RenderLaunch &L)
+{
+    const int eb = L.F * (L.tf16 ? 2 : 4);
+    return eb >= 8 && L.gp.L - L.gp.n_dense <= 4 ? 4 : 2;
+}
+
 // Grid size and tile order of a frame, given the blocks of its kernel that
 // fit on one CU.
 static void render_shape(const RenderLaunch &L, int resident, int64_t &blocks, int &stripe)
@@ -651,6 +673,7 @@ hipError_t launch_render(const RenderLaunch &L0, hipStream_t stream)
 {
     RenderLaunch L = L0;
     L.gp.block_from = render_block_from(L);
+    L.gp.hash_batch = render_hash_batch(L);
 #define X(a, b, c, d, e, f)                                                                    \
     if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
         int64_t blocks;                                                                        \
@@ -690,9 +713,10 @@ hipError_t phase_cycles_read(uint64_t *out, bool reset)
 }
 
 hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk,
-                               int *block_from)
+                               int *block_from, int *hash_batch)
 {
     *block_from = render_block_from(L);
+    *hash_batch = render_hash_batch(L);
 #define X(a, b, c, d, e, f)                                                                    \
     if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
         int64_t nb;                                                                            \

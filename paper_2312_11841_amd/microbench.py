@@ -29,7 +29,7 @@ def lib():
         L.mixrt_mb_rowstream.restype = C.c_int
         I32 = C.c_int32
         L.mixrt_mb_gather_replay.argtypes = [P, P, I32, I32, I32, I32, P, I32, I32, I32, P, I32,
-                                             I32, I32, I32, I32, P, P]
+                                             I32, I32, I32, I32, I32, P, P]
         L.mixrt_mb_gather_replay.restype = C.c_int
         IP = C.POINTER(C.c_int)
         L.mixrt_mb_device_info.argtypes = [C.c_int, IP, IP, IP, IP, C.c_char_p, C.c_int]
@@ -138,7 +138,8 @@ def device_info(device: int = 0) -> dict:
 
 
 def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_stripe: int,
-                  blocks_list, reps: int = 20, chunk: int = 0, block_from=None):
+                  blocks_list, reps: int = 20, chunk: int = 0, block_from=None,
+                  hash_batch: int = 2):
     """The frame's hash-grid loads replayed in the render kernel's order
     (mixrt_mb_gather_replay): for each grid size in blocks_list, the mean time
     of the loads (mode 0) and of their address arithmetic alone (mode 1).
@@ -146,7 +147,8 @@ def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_str
     frame's ray setup; table: the device hash table [L][T][F]; N: level
     resolutions; chunk: the render's samples per ray per round (0: the tile
     path); block_from: the render's first level of 16-byte block gathers
-    (None: none).  Returns per-grid-size times and the fastest."""
+    (None: none); hash_batch: its hashed levels per batch of gathers.
+    Returns per-grid-size times and the fastest."""
     import numpy as np
     import torch
     L_, T, F = (int(n) for n in table.shape)
@@ -165,7 +167,7 @@ def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_str
                 _check(lib().mixrt_mb_gather_replay(
                     x.data_ptr(), hit.data_ptr(), views, W, H, K, table.data_ptr(), L_,
                     T.bit_length() - 1, eb, Nh.ctypes.data, int(tile_stripe), int(chunk), bf,
-                    mode, int(blocks), sink.data_ptr(), s.cuda_stream))
+                    int(hash_batch), mode, int(blocks), sink.data_ptr(), s.cuda_stream))
             for _ in range(3):
                 launch(torch.cuda.current_stream())
             res[name] = _timed(launch, reps) * 1e3

@@ -60,6 +60,11 @@ class CreateInfo(C.Structure):
                 ("block_levels", C.c_int32)]
 
 
+class LaunchPlan(C.Structure):
+    _fields_ = [("blocks", C.c_int32), ("tile_stripe", C.c_int32), ("chunk", C.c_int32),
+                ("block_from", C.c_int32), ("hash_batch", C.c_int32)]
+
+
 class GBuffer(C.Structure):
     _fields_ = [("views", C.c_int32), ("W", C.c_int32), ("H", C.c_int32),
                 ("g0", C.c_void_p), ("g1", C.c_void_p)]
@@ -136,8 +141,7 @@ def lib(variant=None):
             "mixrt_render_launch_shape": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                     C.POINTER(DispTex), C.POINTER(HashGrid),
                                                     C.POINTER(Mlp), C.POINTER(Sampling),
-                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int32),
-                                                    C.POINTER(C.c_int32), C.POINTER(C.c_int32)]),
+                                                    C.POINTER(LaunchPlan)]),
             "mixrt_debug_phase_cycles": (C.c_int, [P, P, C.c_int]),
             "mixrt_debug_ray_setup": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                 C.POINTER(DispTex), C.POINTER(Sampling), P, P]),
@@ -473,17 +477,15 @@ class Renderer:
         return out if chunk else out[:2]
 
     def launch_plan(self, ds: DeviceScene) -> dict:
-        """Everything mixrt_render_launch_shape reports for render(ds):
-        blocks, tile_stripe, chunk (samples per ray per round, 0: the tile
-        path) and block_from (first level gathered in 16-byte blocks, L:
-        none)."""
-        b, st, ch, bf = C.c_int32(), C.c_int32(), C.c_int32(), C.c_int32()
+        """The mixrt_launch_plan of render(ds): blocks, tile_stripe, chunk
+        (samples per ray per round, 0: the tile path), block_from (first
+        level gathered in 16-byte blocks, L: none), hash_batch (hashed
+        levels per batch of gathers)."""
+        plan = LaunchPlan()
         self._check(self._L.mixrt_render_launch_shape(
             self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp), C.byref(ds.grid),
-            C.byref(ds.mlp), C.byref(ds.smp), C.byref(b), C.byref(st), C.byref(ch),
-            C.byref(bf)))
-        return {"blocks": b.value, "tile_stripe": st.value, "chunk": ch.value,
-                "block_from": bf.value}
+            C.byref(ds.mlp), C.byref(ds.smp), C.byref(plan)))
+        return {name: int(getattr(plan, name)) for name, _ in LaunchPlan._fields_}
 
     # -- geometry
     def raycast(self, mesh: DeviceMesh, cams, W: int, H: int, g1: bool = True, out=None):

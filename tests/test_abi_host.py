@@ -65,7 +65,8 @@ def test_every_header_is_checked():
 
 
 def test_struct_layout_matches_header():
-    structs = {"mixrt_create_info": mixrt.CreateInfo, "mixrt_gbuffer": mixrt.GBuffer,
+    structs = {"mixrt_create_info": mixrt.CreateInfo, "mixrt_launch_plan": mixrt.LaunchPlan,
+               "mixrt_gbuffer": mixrt.GBuffer,
                "mixrt_camera": mixrt.Camera, "mixrt_disp_tex": mixrt.DispTex,
                "mixrt_hash_grid": mixrt.HashGrid, "mixrt_mlp": mixrt.Mlp,
                "mixrt_sampling": mixrt.Sampling, "mixrt_mesh_desc": mixrt.MeshDesc,

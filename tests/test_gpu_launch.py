@@ -144,16 +144,18 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
     plan = r.launch_plan(ds)
     n_dense = int(sum((N.astype(np.int64) + 1) ** 3 <= cfg.T))
     for block_from in sorted({cfg.L, plan["block_from"], n_dense, 0}):
-        for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
-            sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
-            rc = mb.lib().mixrt_mb_gather_replay(
-                x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K,
-                ds.table.data_ptr(), cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F,
-                N.ctypes.data, stripe, chunk, block_from, 0, blocks, sink.data_ptr(), None)
-            assert rc == 0
-            torch.cuda.synchronize()
-            got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
-            assert got == acc, (block_from, chunk)
+        for batch in (2, 4):
+            for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
+                sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
+                rc = mb.lib().mixrt_mb_gather_replay(
+                    x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K,
+                    ds.table.data_ptr(), cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F,
+                    N.ctypes.data, stripe, chunk, block_from, batch, 0, blocks,
+                    sink.data_ptr(), None)
+                assert rc == 0
+                torch.cuda.synchronize()
+                got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+                assert got == acc, (block_from, batch, chunk)
     r.close()
 
 
