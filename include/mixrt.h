@@ -111,7 +111,8 @@ typedef struct {
                             block holding both entries (tables of 2 fp16
                             features only; speed only, never a result): > 0
                             that many (hashed levels only), < 0 none, 0 the
-                            library's choice (the three finest, among the
+                            library's choice (the three finest, four when a
+                            level's table exceeds one XCD's L2, among the
                             hashed levels finer than a ray's sample spacing) */
 } mixrt_create_info;
 

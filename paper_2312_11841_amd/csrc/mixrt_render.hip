@@ -604,20 +604,23 @@ static int render_chunk(const RenderLaunch &L)
 
 // First level whose x-neighbour corner pairs are gathered as 16-byte
 // blocks (gp.L: none; tables of 4-byte entries only).  By default the three
-// finest levels, among the hashed levels finer than a ray's sample spacing
-// (coarser levels hand a ray's neighbouring samples the same lines, where a
-// 4-byte gather is cheaper).  Measured against single-entry gathers on every
-// level: the finest 2 or 4 levels were 2-15% faster at 720p (K 1 to 16,
-// spacings 0.01 to 0.25, early termination or not) and on the 8-view 1080p
-// batch, 1-5% slower only at K = 32 on a 4096-pixel-wide view; all hashed
-// levels (or every level finer than the spacing) were slower on most.
+// finest levels (four when a level's table exceeds one XCD's L2, whose
+// misses scatter more), among the hashed levels finer than a ray's sample
+// spacing (coarser levels hand a ray's neighbouring samples the same lines,
+// where a 4-byte gather is cheaper).  Measured against single-entry gathers
+// on every level: the finest 2 to 4 levels were 2-15% faster at 720p (K 1 to
+// 16, spacings 0.01 to 0.25, early termination or not) and 5-8% on the
+// 8-view 1080p batch (8 MiB levels; 4 levels 1.5% faster there than 3),
+// 1-5% slower only at K = 32 on a 4096-pixel-wide view; all hashed levels
+// (or every level finer than the spacing) were slower on most.
 static int render_block_from(const RenderLaunch &L)
 {
     const int nl = L.gp.L;
     if (!(L.tf16 && L.F == 2) || L.block_levels < 0) return nl;
     int lo = L.gp.n_dense;
     if (L.block_levels > 0) return nl - L.block_levels > lo ? nl - L.block_levels : lo;
-    constexpr int kFinest = 3;
+    const int64_t level_bytes = ((int64_t)L.gp.T_mask + 1) * 4;
+    const int kFinest = level_bytes > L.l2_bytes ? 4 : 3;
     if (L.rp.K > 1) {
         const int shared = levels_shared_by_samples(L);
         if (shared > lo) lo = shared;
