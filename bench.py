@@ -396,6 +396,24 @@ def cpu_model() -> str:
     return "unknown"
 
 
+def gather_cost():
+    """Cycles per gather instruction per CU as a function of the distinct
+    128-byte lines its 64 lanes touch (1 to 64), whether the lanes sharing a
+    line are adjacent, the load width (4, 8, 16 bytes) and where the lines
+    live (a 16 KiB table stays in the vector L1, a 2 MiB one in the L2).
+    One JSON line per point."""
+    from paper_2312_11841_amd import microbench as mb
+    for kib in (16, 2048):
+        for width in (4, 8, 16):
+            for lines in (1, 2, 4, 8, 16, 32, 64):
+                for adjacent in ((True,) if lines in (1, 64) else (True, False)):
+                    cyc = mb.gather_lines(kib * 1024, width, lines, adjacent)
+                    print(json.dumps({"table_KiB": kib, "width": width, "lines": lines,
+                                      "adjacent": adjacent,
+                                      "cycles_per_instruction_per_cu": round(cyc, 2)}),
+                          flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1, help="GPUs (one: the only count measured)")
@@ -417,6 +435,9 @@ def main():
     ap.add_argument("--early-stop-chunk", type=int, default=0, metavar="C",
                     help="render in front-to-back rounds of C samples per ray, dropping rays "
                          "once opaque (0: the library's default, the tile path)")
+    ap.add_argument("--gather-cost", action="store_true",
+                    help="only measure how the vector L1 charges a gather instruction "
+                         "(cycles per instruction by distinct lines, lanes per line, width)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device copy of BYTES bytes per step (the "
                          "reference kernel that scales the FETCH_SIZE / WRITE_SIZE counters)")
@@ -440,6 +461,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "steps": args.steps}), flush=True)
+        return
+    if args.gather_cost:
+        gather_cost()
         return
     if args.paper_tables:
         paper_tables(args.steps, args.warmup)

@@ -25,6 +25,16 @@ extern "C" {
 int mixrt_mb_gather(const void *table, uint64_t table_bytes, int width, int loads_per_iter,
                     int iters, int pattern, int blocks, uint32_t *sink, void *stream);
 
+/* Gathers of controlled line sharing: blocks x 256 threads, each wave doing
+ * iters iterations of 8 independent width-byte (4, 8 or 16) loads, each load
+ * instruction touching exactly `lines` distinct 128-byte lines of `table`
+ * (lines divides 64; 64/lines lanes per line, consecutive lanes when
+ * adjacent != 0, else lane l on line l mod lines).  table_bytes: a
+ * power-of-two multiple of 128 (a small table stays in the vector L1, a
+ * larger one in L2).  sink: device uint32 [blocks*256] (written). */
+int mixrt_mb_gather_lines(const void *table, uint64_t table_bytes, int width, int lines,
+                          int adjacent, int iters, int blocks, uint32_t *sink, void *stream);
+
 /* Streaming copy of `bytes` (a multiple of 16) from src to dst with a
  * grid-stride loop over blocks x 256 threads. */
 int mixrt_mb_copy(const void *src, void *dst, uint64_t bytes, int blocks, void *stream);

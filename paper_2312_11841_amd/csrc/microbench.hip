@@ -74,6 +74,41 @@ __global__ __launch_bounds__(kBlock) void gather_kernel(const char *__restrict__
     sink[gid] = acc;
 }
 
+// Gathers whose 64 lanes touch exactly D distinct 128-byte lines per
+// instruction (D divides 64), 64/D lanes per line: lanes j*64/D .. (j+1)*64/D
+// - 1 on line j when `adjacent`, else lane l on line l mod D; within a line
+// the lanes take consecutive W-byte words.  Each iteration issues 8
+// independent loads on fresh pseudo-random line sets of a table of n_lines
+// lines (a power of two).  The time per instruction tells how the vector L1
+// charges a gather: by lanes, by distinct lines, or by lanes per line.
+template <int W>
+__global__ __launch_bounds__(kBlock) void lines_kernel(const char *__restrict__ table,
+                                                       uint32_t line_mask, int iters, int D,
+                                                       int adjacent, uint32_t *__restrict__ sink)
+{
+    typedef typename Vec<W>::T T;
+    const int lane = threadIdx.x & 63;
+    const uint32_t gw = blockIdx.x * (kBlock / 64) + threadIdx.x / 64;
+    const int per = 64 / D;
+    const uint32_t j = (uint32_t)(adjacent ? lane / per : lane % D);
+    const uint32_t q = (uint32_t)(adjacent ? lane % per : lane / D);
+    const uint32_t within = (q * (uint32_t)W) & (128u - (uint32_t)W);
+    uint32_t base = gw * 2654435761u + 12345u, acc = 0;
+    for (int it = 0; it < iters; ++it) {
+        T v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            const uint32_t b = (base + (uint32_t)u * 0x9E3779B9u) >> 7;
+            const uint32_t line = (b * 64u + j * 97u) & line_mask;
+            v[u] = *(const T *)(table + (size_t)line * 128u + within);
+        }
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc ^= Vec<W>::fold(v[u]);
+        base = base * 1664525u + 1013904223u;
+    }
+    sink[blockIdx.x * kBlock + threadIdx.x] = acc;
+}
+
 __global__ __launch_bounds__(kBlock) void copy_kernel(const uint4 *__restrict__ src,
                                                       uint4 *__restrict__ dst, uint64_t n)
 {
@@ -409,6 +444,28 @@ int mixrt_mb_gather(const void *table, uint64_t table_bytes, int width, int load
         else G(16, 1);
     }
 #undef G
+    return hipGetLastError();
+}
+
+int mixrt_mb_gather_lines(const void *table, uint64_t table_bytes, int width, int lines,
+                          int adjacent, int iters, int blocks, uint32_t *sink, void *stream)
+{
+    if (!table || !sink || blocks < 1 || iters < 1) return hipErrorInvalidValue;
+    if (width != 4 && width != 8 && width != 16) return hipErrorInvalidValue;
+    if (lines < 1 || lines > 64 || 64 % lines != 0) return hipErrorInvalidValue;
+    const uint64_t n = table_bytes / 128u;
+    if (n == 0 || (n & (n - 1)) || n > (1ull << 31) || n * 128u != table_bytes)
+        return hipErrorInvalidValue;
+    const uint32_t mask = (uint32_t)(n - 1);
+    hipStream_t s = (hipStream_t)stream;
+    const char *t = (const char *)table;
+#define LK(W)                                                                                   \
+    hipLaunchKernelGGL((lines_kernel<W>), dim3(blocks), dim3(kBlock), 0, s, t, mask, iters, lines, \
+                       adjacent, sink)
+    if (width == 4) LK(4);
+    else if (width == 8) LK(8);
+    else LK(16);
+#undef LK
     return hipGetLastError();
 }
 

@@ -23,6 +23,9 @@ def lib():
         L.mixrt_mb_gather.argtypes = [P, C.c_uint64, C.c_int, C.c_int, C.c_int, C.c_int, C.c_int,
                                       P, P]
         L.mixrt_mb_copy.argtypes = [P, P, C.c_uint64, C.c_int, P]
+        L.mixrt_mb_gather_lines.argtypes = [P, C.c_uint64, C.c_int, C.c_int, C.c_int, C.c_int,
+                                            C.c_int, P, P]
+        L.mixrt_mb_gather_lines.restype = C.c_int
         L.mixrt_mb_read.argtypes = [P, C.c_uint64, C.c_int, P, P]
         L.mixrt_mb_mfma.argtypes = [C.c_int, C.c_int, P, P]
         L.mixrt_mb_rowstream.argtypes = [P, P, C.c_int64, C.c_int, C.c_int, P]
@@ -81,6 +84,26 @@ def gather(table_bytes: int, width: int = 4, pattern: int = 0, iters: int = 64,
             "useful_GBps": lane_loads * width / t / 1e9,
             "wave_instr_per_s": wave_instr / t,
             "ns_per_wave_instr_per_cu": t * 1e9 * cus / wave_instr}
+
+
+def gather_lines(table_bytes: int, width: int, lines: int, adjacent: bool,
+                 blocks_per_cu: int = 4, iters: int = 256):
+    """Cycles per gather instruction per CU (at the 2.4 GHz peak clock) when
+    each instruction's 64 lanes touch `lines` distinct 128-byte lines
+    (mixrt_mb_gather_lines)."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    blocks = blocks_per_cu * cus
+    t = torch.randint(0, 2**31 - 1, (table_bytes // 4,), dtype=torch.int32, device="cuda")
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+
+    def launch(s):
+        _check(lib().mixrt_mb_gather_lines(t.data_ptr(), table_bytes, width, lines,
+                                           int(bool(adjacent)), iters, blocks, sink.data_ptr(),
+                                           s.cuda_stream))
+    sec = _timed(launch, 10)
+    instr_per_cu = blocks * 4 * iters * 8 / cus
+    return sec * 2.4e9 / instr_per_cu
 
 
 def copy(bytes_: int = 1 << 30, blocks: int | None = None):

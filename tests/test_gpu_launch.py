@@ -313,3 +313,22 @@ def test_early_termination_against_the_oracle(cfg):
     say("  samples evaluated by round size:", counts)
     assert counts[-1] == cfg.rays * cfg.K            # every pixel hits
     assert counts[1] < counts[2] <= counts[4] < counts[-1]
+
+
+def test_gather_lines_microbenchmark():
+    """The L1 cost probe behind the block gathers: runs at every width and
+    sharing pattern, refuses a line count that does not divide 64, and a
+    gather touching 64 lines costs more than one touching 4."""
+    from paper_2312_11841_amd import microbench as mb
+    t = torch.zeros(16 * 1024 // 4, dtype=torch.int32, device="cuda:0")
+    sink = torch.empty(256 * 256, dtype=torch.int32, device="cuda:0")
+    assert mb.lib().mixrt_mb_gather_lines(t.data_ptr(), 16 * 1024, 4, 3, 1, 1, 256,
+                                          sink.data_ptr(), None) != 0
+    assert mb.lib().mixrt_mb_gather_lines(t.data_ptr(), 16 * 1024 + 128, 4, 4, 1, 1, 256,
+                                          sink.data_ptr(), None) != 0
+    few = mb.gather_lines(16 * 1024, 4, 4, True, iters=32)
+    many = mb.gather_lines(16 * 1024, 4, 64, True, iters=32)
+    for width in (8, 16):
+        assert mb.gather_lines(2048 * 1024, width, 16, False, iters=16) > 0
+    say(f"  cycles per gather: 4 lines {few:.1f}, 64 lines {many:.1f}")
+    assert many > 2 * few
