@@ -109,7 +109,10 @@ __device__ __forceinline__ void wait_vm_upto(int n)
 
 // Persistent: weights are loaded once per wave, then 64-row tiles.  A tile's
 // rows are one contiguous block of 64 * CH 16-byte chunks, copied to LDS in
-// CH coalesced loads, DEPTH tiles ahead of the one being computed.
+// CH coalesced loads, DEPTH tiles ahead of the one being computed; its 64
+// outputs are gathered in LDS and written with one coalesced 1 KiB store
+// (lane l: row l), the same access pattern as the stream the stage is
+// measured against.
 //
 // The loads and stores of the tile loop are issued as assembly, so that the
 // compiler, which sees no memory operation of its own there, places no wait
@@ -118,11 +121,11 @@ __device__ __forceinline__ void wait_vm_upto(int n)
 // pending stores; either would serialise the pipelining.  The waits are
 // counted instead.  Every tile issues exactly CH loads (the chunks of rows
 // past n are read from the last row, and their outputs never stored) and
-// every tile but the last overall, which is then also the last of its wave,
-// is full and issues exactly kStores stores.  After the loads of tile k come
-// the stores of the min(k, DEPTH) tiles before it and the loads of the tiles
-// after it that are already in flight, and that is the count to wait for.
-constexpr int kStores = 4;   // one per 16-row sub-tile, by lanes 0..15
+// exactly kStores stores (the lanes of rows past n masked off; a tile always
+// has a row below n).  After the loads of tile k come the stores of the
+// min(k, DEPTH) tiles before it and the loads of the tiles after it that are
+// already in flight, and that is the count to wait for.
+constexpr int kStores = 1;
 
 template <int IN, int HID, int NHID, int DEPTH>
 __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict__ weights,
@@ -136,6 +139,7 @@ __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict_
     static_assert(DEPTH * (CH + kStores) <= 63, "vmcnt range");
     // NB tile buffers per wave, rows of IN halves back to back
     __shared__ __attribute__((aligned(16))) _Float16 s_rows[kWavesPerBlock][NB][kWave * IN];
+    __shared__ f4 s_res[kWavesPerBlock][kWave];
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
     MlpWeights<IN, HID, NHID> Wt;
@@ -168,12 +172,13 @@ __global__ __launch_bounds__(kBlock) void mlp_kernel(const _Float16 *__restrict_
 #pragma unroll
         for (int nt = 0; nt < 4; ++nt) {
             const f4 o = mlp_tile<IN, HID, NHID>(Wt, rows + nt * 16 * IN, IN, lane);
-            const int64_t s = base + nt * 16 + c;
-            if (g == 0 && s < n) {
+            if (g == 0) {
                 const float4 a = mlp_activate(o);
-                store16(out4 + s, f4{a.x, a.y, a.z, a.w});
+                s_res[wv][nt * 16 + c] = f4{a.x, a.y, a.z, a.w};
             }
         }
+        wave_lds_sync();
+        if (base + lane < n) store16(out4 + base + lane, s_res[wv][lane]);
     }
     wait_vm<0>();
 }
