@@ -202,11 +202,16 @@ typedef struct {
 /* ---- lifecycle ---------------------------------------------------------- */
 
 /* Create a context bound to ci->device and ci->hip_stream.  Fails with
- * MIXRT_EUNSUPPORTED unless the device is gfx950. *out is NULL on failure. */
+ * MIXRT_EUNSUPPORTED unless the device is gfx950. *out is NULL on failure.
+ * Allocates the context's 10 KiB of render work counters on ci->device
+ * (MIXRT_ENOMEM if that fails); the caller's current device is kept.
+ * Renders of one context must not run at the same time (they share the
+ * counters): keep them on its stream. */
 int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci);
 
 /* Release the context (not the caller's buffers or stream).  NULL is a
- * no-op.  Pending work on the stream is not waited for. */
+ * no-op.  Waits for the work pending on the context's stream, then frees
+ * its work counters. */
 int mixrt_destroy(mixrt_ctx *ctx);
 
 /* Wait for all work enqueued by the context; MIXRT_EDEVICE on a device

@@ -16,6 +16,7 @@
 #include <new>
 #include <string>
 
+#include "mixrt_common.hpp"
 #include "mixrt_launch.hpp"
 #include "mixrt_mesh.hpp"
 
@@ -26,6 +27,7 @@ struct mixrt_ctx {
     int32_t tile_stripe = 0;
     int32_t early_stop_chunk = 0;
     int32_t block_levels = 0;
+    unsigned int *work = nullptr;   // device: the render kernels' work counters
     int cus = 0;
     int64_t l2_bytes = 0;
     std::string err;
@@ -629,8 +631,27 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
         return fail(nullptr, MIXRT_EUNSUPPORTED, "device %d is %s, this library is built for gfx950",
                     ci->device, prop.gcnArchName);
+    // the render kernels' work counters: one small zeroed buffer per
+    // context, allocated on its device (the caller's current device is kept)
+    int prev = 0;
+    if ((e = hipGetDevice(&prev)) != hipSuccess || (e = hipSetDevice(ci->device)) != hipSuccess)
+        return fail(nullptr, MIXRT_EDEVICE, "hipSetDevice(%d): %s", ci->device, hipGetErrorString(e));
+    unsigned int *work = nullptr;
+    e = hipMalloc((void **)&work, mixrt::kWorkWords * sizeof(unsigned int));
+    if (e == hipSuccess) e = hipMemset(work, 0, mixrt::kWorkWords * sizeof(unsigned int));
+    if (e != hipSuccess) {
+        if (work) (void)hipFree(work);
+        (void)hipSetDevice(prev);
+        return fail(nullptr, e == hipErrorOutOfMemory ? MIXRT_ENOMEM : MIXRT_EDEVICE,
+                    "work counters: %s", hipGetErrorString(e));
+    }
+    (void)hipSetDevice(prev);
     mixrt_ctx *ctx = new (std::nothrow) mixrt_ctx;
-    if (!ctx) return fail(nullptr, MIXRT_ENOMEM, "host allocation failed");
+    if (!ctx) {
+        (void)hipFree(work);
+        return fail(nullptr, MIXRT_ENOMEM, "host allocation failed");
+    }
+    ctx->work = work;
     ctx->device = ci->device;
     ctx->stream = (hipStream_t)ci->hip_stream;
     ctx->flags = ci->flags;
@@ -645,6 +666,16 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
 
 int mixrt_destroy(mixrt_ctx *ctx)
 {
+    if (!ctx) return MIXRT_OK;
+    if (ctx->work) {
+        // freed once the context's stream has finished the work enqueued on it
+        int prev = 0;
+        if (hipGetDevice(&prev) == hipSuccess && hipSetDevice(ctx->device) == hipSuccess) {
+            (void)hipStreamSynchronize(ctx->stream);
+            (void)hipFree(ctx->work);
+            (void)hipSetDevice(prev);
+        }
+    }
     delete ctx;
     return MIXRT_OK;
 }
@@ -688,6 +719,7 @@ void fill_render_launch(mixrt::RenderLaunch &L, const mixrt_ctx *ctx, const mixr
     L.tile_stripe = ctx->tile_stripe;
     L.chunk = ctx->early_stop_chunk;
     L.block_levels = ctx->block_levels;
+    L.work = ctx->work;
 }
 
 }  // namespace

@@ -77,6 +77,7 @@ struct RenderLaunch {
     int chunk;          // > 0: early-termination path with this many samples per round
     int block_levels;   // finest levels with 16-byte block gathers: > 0 that many,
                         // < 0 none, 0 the default rule
+    unsigned int *work; // device, kWorkWords words of work counters (zero)
 };
 
 bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nhid);

@@ -114,6 +114,7 @@ template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
                                                         const _Float16 *__restrict__ weights,
                                                         int view_sh, int hid_w, int stripe,
+                                                        unsigned int *__restrict__ work,
                                                         float4 *__restrict__ out)
 {
 #ifdef MIXRT_SPLIT_NO_DISP
@@ -142,17 +143,20 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
     const int R = kWave / K;                 // rays per tile
     const int spt = R * K;                   // sample slots used per tile
     const TileShape ts = tile_shape(R, rp.views, rp.W, rp.H, stripe);
-    const int gw = xcd_logical_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wv;
-    const int total = gridDim.x * kWavesPerBlock;
     const int r_loc = lane / K;
     const int k = lane - r_loc * K;
     const int L = gp.L;
+    // tiles from the per-XCD pools (a counted tile's claim is in flight
+    // while the tile before it is rendered)
+    WorkPools pools(work, ts.n_tiles, lane);
 #ifdef MIXRT_PHASE_TIMER
     uint64_t ph[4] = {0, 0, 0, 0}, n_tiles_done = 0, n_samples = 0;
     uint64_t t_last = __builtin_readcyclecounter();
 #endif
 
-    for (int tile = gw; tile < ts.n_tiles; tile += total) {
+    for (;;) {
+        const int tile = pools.take(lane);
+        if (tile < 0) break;
         // the tile's pixel block, and ray r of it at (r % RW, r / RW)
         const TilePos tp = tile_at(ts, tile);
         const int view = tp.view;
@@ -195,6 +199,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         row[0] = (_Float16)((x0 + x1 + x2) * 0.0f);
 #endif
         MIXRT_PHASE(1);
+        pools.prefetch(lane);
         if (!SUM && view_sh) {
             float Y[16];
             sh_basis<16>(ry.dx, ry.dy, ry.dz, Y);
@@ -250,6 +255,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
         n_samples += __popcll(__ballot(hit));
 #endif
     }
+    pools.finish();
 #ifdef MIXRT_PHASE_TIMER
     if (lane == 0) {
         for (int i = 0; i < 4; ++i) atomicAdd(&phase_cycles[i], (unsigned long long)ph[i]);
@@ -283,7 +289,8 @@ template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
 __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, GridParams gp,
                                                               const _Float16 *__restrict__ weights,
                                                               int view_sh, int hid_w, int stripe,
-                                                              int C, float4 *__restrict__ out)
+                                                              int C, unsigned int *__restrict__ work,
+                                                              float4 *__restrict__ out)
 {
 #ifdef MIXRT_SPLIT_NO_DISP
     typedef TexKind<float, kDispNone> TK;
@@ -315,8 +322,6 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
     const int R = kWave / K;                 // rays per tile
     const int spt = R * K;
     const TileShape ts = tile_shape(R, rp.views, rp.W, rp.H, stripe);
-    const int gw = xcd_logical_block(blockIdx.x, gridDim.x) * kWavesPerBlock + wv;
-    const int total = gridDim.x * kWavesPerBlock;
     const int NS = kWave / C;               // ray slots
     const int L = gp.L;
 
@@ -324,11 +329,13 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
     int s_ray = -1, s_kn = 0, s_view = 0;
     Composite cp;
     // A wave holds the rays of about K/C tiles at once, so it takes its tiles
-    // in runs of B = K/C consecutive ones (run c of the tile order goes to
-    // wave c mod total): the rays in flight in a wave are neighbours, and an
-    // XCD's rays in flight stay one compact block of the image.
+    // in runs of B = K/C consecutive ones (the units of the per-XCD pools):
+    // the rays in flight in a wave are neighbours, and an XCD's rays in
+    // flight stay one compact block of the image.  The claim of a wave's
+    // next run is in flight while the current run is admitted.
     const int B = K / C > 1 ? K / C : 1;
-    int run = gw, in_run = 0;
+    WorkPools pools(work, (ts.n_tiles + B - 1) / B, lane);
+    int run = 0, in_run = B;   // the first admission takes a run
 #ifdef MIXRT_PHASE_TIMER
     uint64_t ph[4] = {0, 0, 0, 0}, n_tiles_done = 0, n_samples = 0;
     uint64_t t_last = __builtin_readcyclecounter();
@@ -339,13 +346,13 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
         for (;;) {
             const bool empty = lane < NS && s_ray < 0;
             const uint64_t em = __ballot(empty);
-            const int64_t tile64 = (int64_t)run * B + in_run;
-            if (tile64 >= ts.n_tiles || __popcll(em) < R) break;
-            const int tile = (int)tile64;
-            if (++in_run == B) {
+            if (run >= 0 && (in_run == B || (int64_t)run * B + in_run >= ts.n_tiles)) {
+                // the run is used up (the last one may be short): take the next
+                run = pools.take(lane);
                 in_run = 0;
-                run += total;
             }
+            if (run < 0 || __popcll(em) < R) break;
+            const int tile = run * B + in_run++;
 #ifdef MIXRT_PHASE_TIMER
             ++n_tiles_done;
 #endif
@@ -421,6 +428,7 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
         row[0] = (_Float16)((x0 + x1 + x2) * 0.0f);
 #endif
         MIXRT_PHASE(1);
+        pools.prefetch(lane);
         if (!SUM && view_sh) {
             float Y[16];
             sh_basis<16>(fb.x, fb.y, fb.z, Y);
@@ -467,6 +475,7 @@ __global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, Grid
         wave_lds_sync();
         MIXRT_PHASE(3);
     }
+    pools.finish();
 #ifdef MIXRT_PHASE_TIMER
     if (lane == 0) {
         for (int i = 0; i < 4; ++i) atomicAdd(&phase_cycles[i], (unsigned long long)ph[i]);
@@ -686,11 +695,11 @@ hipError_t launch_render(const RenderLaunch &L0, hipStream_t stream)
         if (chunk > 0)                                                                         \
             hipLaunchKernelGGL((render_queue_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks), \
                                dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh,      \
-                               L.hid_w, stripe, chunk, L.out);                                 \
+                               L.hid_w, stripe, chunk, L.work, L.out);                         \
         else                                                                                   \
             hipLaunchKernelGGL((render_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks),      \
                                dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh,      \
-                               L.hid_w, stripe, L.out);                                        \
+                               L.hid_w, stripe, L.work, L.out);                                \
         return hipGetLastError();                                                              \
     }
     MIXRT_RENDER_VARIANTS(X)

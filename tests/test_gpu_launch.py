@@ -6,6 +6,8 @@ builds that time the kernel's phases, and the gather-replay microbenchmark
 that measures the floor of its gather stream.
 
   - every tile order renders the same frame bit for bit, and every pixel;
+  - the work counters are back at zero after every launch, whatever the
+    kernel and grid size of the next one;
   - the early-termination path renders the tile path's frame bit for bit
     (the same samples composited in the same order), at every round size,
     and evaluates fewer samples on opaque content;
@@ -68,6 +70,33 @@ def test_tile_order_never_changes_a_pixel(cfg):
             got, _ = _render(ds, tile_stripe=stripe, blocks=b)
             assert np.array_equal(got, ref), (stripe, b)
     say(f"  stripes launched: {sorted(seen)} (tiles of {R} rays)")
+
+
+def test_work_counters_are_ready_for_every_launch():
+    """One context renders frames of different kernels and grid sizes in turn
+    (a queue-kernel frame, a ragged frame, a one-sample frame on the tile
+    kernel and a frame of 25 tiles on 7 blocks, so in one pool), twice over: the pools'
+    counters, left at zero by each launch's last blocks, give every later
+    launch the same frame as a fresh context's first launch."""
+    cfgs = [synth.VIEW720P, ORDER_CFGS[4], synth.PAPER720P,
+            synth.TINY64_DENSE.replace(name="one_pool", H=5, W=37, views=1, K=8, gbuf="iid")]
+    scenes = [mixrt.DeviceScene.from_scene(synth.make_scene(c), "cuda:0") for c in cfgs]
+    refs = [_render(ds)[0] for ds in scenes]
+    r = mixrt.Renderer(0, sync_check=True)
+    try:
+        for rep in range(2):
+            for cfg, ds, ref in zip(cfgs, scenes, refs):
+                plan = r.launch_plan(ds)
+                say("counters", rep, cfg.name, plan)
+                if cfg.name == "one_pool":
+                    assert plan["blocks"] == 7
+                out = torch.full((ds.rays, 4), float("nan"), dtype=torch.float32,
+                                 device="cuda:0")
+                r.render(ds, out)
+                r.sync()
+                assert np.array_equal(out.cpu().numpy(), ref), (rep, cfg.name)
+    finally:
+        r.close()
 
 
 def test_tile_order_spot_check_against_the_oracle():
