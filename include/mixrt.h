@@ -236,10 +236,28 @@ int mixrt_level_resolutions(const mixrt_hash_grid *grid, int32_t *out_N);
 
 /* Render views * H * W pixels into out_rgba (device float [views][H][W][4]:
  * composited rgb plus alpha = 1 - final transmittance).  A miss pixel gets
- * (bg, 0).  Enqueued on the context's stream; no device memory is allocated. */
+ * (bg, 0).  Enqueued on the context's stream; no device memory is allocated
+ * (the kernels' work counters are the context's). */
 int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
                  const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
                  const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
+
+/* For callers that cannot allocate device memory or own a per-context
+ * buffer: code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc.  Renders exactly what mixrt_render renders (same
+ * arguments, same kernels, same frame bit for bit), but the kernels' work
+ * counters are one fixed array of the library's own device memory
+ * (MIXRT_NOALLOC_SCRATCH_BYTES = 10 KiB per device, held until the process
+ * ends), set up and zeroed by the first mixrt_create on that device; the
+ * call makes no hipMalloc, hipFree or other allocating call.  The array's
+ * size does not depend on the frame, so no frame is too large for it.  Every
+ * call on a device shares that device's array: calls that overlap on one
+ * device (other streams, other contexts, other threads) race and may skip
+ * or repeat tiles.  Each launch leaves the counters at zero for the next. */
+#define MIXRT_NOALLOC_SCRATCH_BYTES 10240
+int mixrt_render_noalloc(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                         const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
+                         const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba);
 
 /* How mixrt_render launches a frame (none of it changes a result). */
 typedef struct {

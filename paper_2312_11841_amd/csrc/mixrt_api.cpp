@@ -13,6 +13,8 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <atomic>
+#include <mutex>
 #include <new>
 #include <string>
 
@@ -33,6 +35,11 @@ struct mixrt_ctx {
     std::string err;
 };
 
+// The work counters of mixrt_render_noalloc: one array per device (each
+// device holds its own copy), found with hipGetSymbolAddress at set-up.
+static __device__ __align__(256) unsigned int scratch[mixrt::kWorkWords];
+static_assert(sizeof(scratch) == MIXRT_NOALLOC_SCRATCH_BYTES, "scratch size");
+
 struct mixrt_mesh {
     int device = 0;
     void *mem = nullptr;           // one device allocation holding every array
@@ -43,6 +50,30 @@ struct mixrt_mesh {
 namespace {
 
 thread_local std::string t_err;
+
+// Device address of `scratch` on each device that a context was created on
+// (null: not set up).  In host code the array's name stands for a host-side
+// handle, never a device address: kernels get these pointers.
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+std::atomic<unsigned int *> g_scratch[kMaxScratchDevices];
+
+// Once per device, with that device current: look up the array's address
+// and zero it.  Returns a HIP error; the device keeps no address on failure.
+hipError_t scratch_setup(int device)
+{
+    if (device < 0 || device >= kMaxScratchDevices) return hipSuccess;  // no no-alloc path
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch[device].load()) return hipSuccess;
+    unsigned int *ptr = nullptr;
+    hipError_t e = hipGetSymbolAddress((void **)&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    e = hipMemset(ptr, 0, sizeof(scratch));
+    if (e == hipSuccess) e = hipDeviceSynchronize();
+    if (e != hipSuccess) return e;
+    g_scratch[device].store(ptr);
+    return hipSuccess;
+}
 
 int fail(mixrt_ctx *ctx, int code, const char *fmt, ...)
 {
@@ -639,11 +670,20 @@ int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci)
     unsigned int *work = nullptr;
     e = hipMalloc((void **)&work, mixrt::kWorkWords * sizeof(unsigned int));
     if (e == hipSuccess) e = hipMemset(work, 0, mixrt::kWorkWords * sizeof(unsigned int));
+    // (done before any stream of the caller's can launch a render on it)
+    if (e == hipSuccess) e = hipDeviceSynchronize();
     if (e != hipSuccess) {
         if (work) (void)hipFree(work);
         (void)hipSetDevice(prev);
         return fail(nullptr, e == hipErrorOutOfMemory ? MIXRT_ENOMEM : MIXRT_EDEVICE,
                     "work counters: %s", hipGetErrorString(e));
+    }
+    // and, once per device, the no-alloc render's counters
+    e = scratch_setup(ci->device);
+    if (e != hipSuccess) {
+        (void)hipFree(work);
+        (void)hipSetDevice(prev);
+        return fail(nullptr, MIXRT_EDEVICE, "no-alloc work counters: %s", hipGetErrorString(e));
     }
     (void)hipSetDevice(prev);
     mixrt_ctx *ctx = new (std::nothrow) mixrt_ctx;
@@ -724,9 +764,13 @@ void fill_render_launch(mixrt::RenderLaunch &L, const mixrt_ctx *ctx, const mixr
 
 }  // namespace
 
-int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
-                 const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
-                 const mixrt_sampling *smp, float *out_rgba)
+namespace {
+
+// mixrt_render with the kernels' work counters at `work` (null: the
+// context's own)
+int render_with(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                const mixrt_sampling *smp, float *out_rgba, bool noalloc)
 {
     if (!ctx) return fail(nullptr, MIXRT_EINVAL, "ctx is NULL");
     clear_err(ctx);
@@ -736,10 +780,34 @@ int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *
     if (rc) return fail(ctx, rc, "%s", msg);
     if (!out_rgba) return fail(ctx, MIXRT_EINVAL, "out_rgba is NULL");
     if (!aligned16(out_rgba)) return fail(ctx, MIXRT_EINVAL, "out_rgba not 16-byte aligned");
+    unsigned int *work = ctx->work;
+    if (noalloc) {
+        work = ctx->device < kMaxScratchDevices ? g_scratch[ctx->device].load() : nullptr;
+        if (!work)
+            return fail(ctx, MIXRT_EUNSUPPORTED, "no no-alloc work counters on device %d",
+                        ctx->device);
+    }
     if ((rc = bind_device(ctx))) return rc;
     mixrt::RenderLaunch L;
     fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, out_rgba);
-    return finish_launch(ctx, mixrt::launch_render(L, ctx->stream), "render");
+    L.work = work;
+    return finish_launch(ctx, mixrt::launch_render(L, ctx->stream), noalloc ? "render_noalloc" : "render");
+}
+
+}  // namespace
+
+int mixrt_render(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                 const mixrt_disp_tex *disp, const mixrt_hash_grid *grid, const mixrt_mlp *mlp,
+                 const mixrt_sampling *smp, float *out_rgba)
+{
+    return render_with(ctx, gbuf, cams, disp, grid, mlp, smp, out_rgba, false);
+}
+
+int mixrt_render_noalloc(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf, const mixrt_camera *cams,
+                         const mixrt_disp_tex *disp, const mixrt_hash_grid *grid,
+                         const mixrt_mlp *mlp, const mixrt_sampling *smp, float *out_rgba)
+{
+    return render_with(ctx, gbuf, cams, disp, grid, mlp, smp, out_rgba, true);
 }
 
 int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,

@@ -32,7 +32,8 @@ MAX_VIEWS, MAX_LEVELS, MAX_LAYERS = 16, 32, 8
 # Every symbol include/mixrt.h declares.
 EXPORTS = (
     "mixrt_create", "mixrt_destroy", "mixrt_sync", "mixrt_validate",
-    "mixrt_level_resolutions", "mixrt_render", "mixrt_render_launch_shape",
+    "mixrt_level_resolutions", "mixrt_render", "mixrt_render_noalloc",
+    "mixrt_render_launch_shape",
     "mixrt_debug_phase_cycles", "mixrt_debug_ray_setup",
     "mixrt_debug_hash_encode", "mixrt_debug_mlp", "mixrt_debug_composite",
     "mixrt_mesh_plan", "mixrt_mesh_create", "mixrt_mesh_get_info", "mixrt_mesh_destroy",
@@ -138,6 +139,9 @@ def lib(variant=None):
             "mixrt_render": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                        C.POINTER(DispTex), C.POINTER(HashGrid), C.POINTER(Mlp),
                                        C.POINTER(Sampling), P]),
+            "mixrt_render_noalloc": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
+                                               C.POINTER(DispTex), C.POINTER(HashGrid),
+                                               C.POINTER(Mlp), C.POINTER(Sampling), P]),
             "mixrt_render_launch_shape": (C.c_int, [P, C.POINTER(GBuffer), C.POINTER(Camera),
                                                     C.POINTER(DispTex), C.POINTER(HashGrid),
                                                     C.POINTER(Mlp), C.POINTER(Sampling),
@@ -458,6 +462,19 @@ class Renderer:
         self._check(self._L.mixrt_render(self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp),
                                        C.byref(ds.grid), C.byref(ds.mlp), C.byref(ds.smp),
                                        _ptr(out)))
+        return out
+
+    def render_noalloc(self, ds: DeviceScene, out):
+        """render(ds) through mixrt_render_noalloc: the same frame, with the
+        kernels' work counters in the library's fixed per-device array (calls
+        that overlap on one device race).  out: the caller's float32 [rays, 4]
+        on this device; nothing is allocated."""
+        import torch
+        _require(out, "out", (torch.float32,), 4 * ds.rays, self.device)
+        ds.check(self.device)
+        self._check(self._L.mixrt_render_noalloc(self._h, C.byref(ds.gbuf), ds.cams,
+                                               C.byref(ds.disp), C.byref(ds.grid),
+                                               C.byref(ds.mlp), C.byref(ds.smp), _ptr(out)))
         return out
 
     def phase_cycles(self, reset: bool = False):
