@@ -129,10 +129,11 @@ def gather_replay_floor(cfg, ds, renderer):
     grids = sorted({blocks} | {k * cus for k in (1, 2, 3, 4, 6, 8)})
     r = mb.gather_replay(x, hit, cfg.views, cfg.W, cfg.rows_kept, cfg.K, ds.table, N, stripe,
                          grids, chunk=chunk, block_from=plan["block_from"],
-                         hash_batch=plan["hash_batch"])
+                         hash_batch=plan["hash_batch"], claims=bool(plan["claims"]))
     del x, hit
     return {"render_blocks": blocks, "tile_stripe": stripe, "early_stop_chunk": chunk,
-            "block_from": plan["block_from"], "hash_batch": plan["hash_batch"], **r}
+            "block_from": plan["block_from"], "hash_batch": plan["hash_batch"],
+            "claims": plan["claims"], **r}
 
 
 def stage_metrics(cfg, ds, out, steps, chunk=0):
@@ -671,7 +672,7 @@ def main():
             "parallelism": "single GPU",
             "launch": {"blocks": plan["blocks"], "tile_stripe": plan["tile_stripe"],
                        "early_stop_chunk": plan["chunk"], "block_from": plan["block_from"],
-                       "hash_batch": plan["hash_batch"]},
+                       "hash_batch": plan["hash_batch"], "claims": plan["claims"]},
         },
         "roofline": roofline,
         **stage_fields,

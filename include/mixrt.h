@@ -268,6 +268,9 @@ typedef struct {
     int32_t block_from;  /* first hash level whose x-neighbour corner pairs
                             are gathered as 16-byte blocks (L: none) */
     int32_t hash_batch;  /* hashed levels per batch of gathers (2 or 4) */
+    int32_t claims;      /* 1: each wave claims the last units of its XCD's
+                            pool from the work counters; 0: every unit in the
+                            fixed order */
 } mixrt_launch_plan;
 
 /* The launch mixrt_render would make for these descriptors on this

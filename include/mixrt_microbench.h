@@ -58,9 +58,12 @@ int mixrt_mb_rowstream(const void *src, void *dst, int64_t rows, int in_bytes, i
 int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
 
 /* Gather replay of one frame's hash-grid loads, the floor of the render
- * kernel's gather stream: blocks x 256 threads, the render kernel's
- * XCD-contiguous block mapping and tile order (tile_stripe as returned by
- * mixrt_render_launch_shape), one sample per lane as in the render kernel;
+ * kernel's gather stream: blocks x 256 threads, the render kernel's work
+ * distribution (per-XCD pools: each wave's first rounds in a fixed order,
+ * the rest claimed from counters in `work`, or with work NULL every unit in
+ * the fixed order, as the render does when its plan's claims is 0) and tile
+ * order (tile_stripe as returned by mixrt_render_launch_shape), one sample
+ * per lane as in the render kernel;
  * each lane reads its sample's position from x (device float
  * [views*H*W][K][3], the frame's mixrt_debug_ray_setup output; rays with
  * hit[ray] == 0 are skipped, hit: device int32 [views*H*W]), computes the
@@ -80,14 +83,18 @@ int mixrt_mb_mfma(int iters, int blocks, float *out, void *stream);
  * mixrt_render_launch_shape; L: none); hash_batch: hashed levels per batch
  * of the other gathers, 2 or 4 (4 only for entries of 8 or more bytes, as
  * the render kernel batches them).  N: host int32 [L], the level
- * resolutions (non-decreasing).  sink: device uint32 [blocks*256]
- * (written); with mode 0 the XOR over all of it is the XOR of the 8 corner
- * entries of every level of every hit sample. */
+ * resolutions (non-decreasing).  work: NULL or device uint32
+ * [MIXRT_MB_WORK_WORDS], zero before the call and left at zero by it (one
+ * buffer per stream: calls that overlap must not share it).  sink: device
+ * uint32 [blocks*256] (written); with mode 0 the XOR over all of it is the
+ * XOR of the 8 corner entries of every level of every hit sample. */
+#define MIXRT_MB_WORK_WORDS 2560
 int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, int32_t W,
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
                            int32_t chunk, int32_t block_from, int32_t hash_batch,
-                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream);
+                           int32_t mode, int32_t blocks, uint32_t *work, uint32_t *sink,
+                           void *stream);
 
 /* Properties of HIP device `device` the measurements are quoted against:
  * peak shader clock (kHz), memory clock (kHz), compute units, L2 bytes, and

@@ -17,6 +17,8 @@
 #include "mixrt_common.hpp"
 #include "mixrt_microbench.h"
 
+static_assert(MIXRT_MB_WORK_WORDS == mixrt::kWorkWords, "replay work counters");
+
 namespace {
 
 constexpr int kBlock = 256;
@@ -196,8 +198,9 @@ __global__ __launch_bounds__(kBlock) void mfma_kernel(int iters, float *__restri
 
 // ---------------------------------------------------------------------------
 // Gather replay: the hash-grid loads of one frame, in the render kernel's
-// order and nothing else.  Same persistent grid, XCD-contiguous block
-// mapping and tile order (stripe) as the render kernel; a lane takes the
+// order and nothing else.  Same persistent grid, work distribution (the
+// per-XCD pools: a static start, then runs claimed from the counters) and
+// tile order (stripe) as the render kernel; a lane takes the
 // same sample of the same tile, reads that sample's position from the frame's
 // ray-setup output, and issues the same loads in the same batches (dense
 // levels as x-neighbour pairs, hashed levels of 4-byte entries as 16-byte
@@ -310,6 +313,7 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
                                                         const int32_t *__restrict__ hit, int views,
                                                         int W, int H, int K, int stripe, int C,
                                                         mixrt::GridParams gp,
+                                                        unsigned int *__restrict__ work,
                                                         uint32_t *__restrict__ sink)
 {
     constexpr int kGroup = 2;
@@ -317,8 +321,6 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
     const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const int R = 64 / K;
     const mixrt::TileShape ts = mixrt::tile_shape(R, views, W, H, stripe);
-    const int gw = mixrt::xcd_logical_block(blockIdx.x, gridDim.x) * 4 + wv;
-    const int total = gridDim.x * 4;
     const int L = gp.L, n_dense = gp.n_dense;
     // C = 0: one tile per step, lane r K + k on sample k of ray r (the tile
     // path).  C > 0: the early-termination path's order when no ray stops
@@ -330,9 +332,16 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
     const int sl = lane / Cl, j = lane - sl * Cl;
     const int t_in_run = C > 0 ? sl / R : 0, r_loc = C > 0 ? sl - t_in_run * R : lane / K;
     uint32_t acc = 0;
-    for (int64_t run = gw; run * B < ts.n_tiles; run += total)
+    // runs from the render kernels' per-XCD pools (work null: all in the
+    // fixed order); the claim of a wave's next run goes out once the current
+    // run's first round of loads is done
+    mixrt::WorkPools pools(work, (ts.n_tiles + B - 1) / B, lane);
+    for (;;) {
+    const int run = pools.take(lane);
+    if (run < 0) break;
     for (int c = 0; c < rounds; ++c) {
-        const int64_t tile64 = run * B + t_in_run;
+        if (c > 0) pools.prefetch(lane);
+        const int64_t tile64 = (int64_t)run * B + t_in_run;
         const int k = C > 0 ? c * C + j : lane - r_loc * K;
         if (t_in_run >= B || tile64 >= ts.n_tiles || k >= K || lane >= (C > 0 ? 64 : R * K))
             continue;
@@ -359,6 +368,9 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
         for (; l < lb; ++l) acc ^= replay_group<EB, 1, false, MODE>(gp, l, x0, x1, x2);
         for (; l < L; ++l) acc ^= replay_group<EB, 1, false, MODE, true>(gp, l, x0, x1, x2);
     }
+    pools.prefetch(lane);
+    }
+    pools.finish();
     sink[(size_t)blockIdx.x * kBlock + threadIdx.x] = acc;
 }
 
@@ -370,7 +382,8 @@ int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, in
                            int32_t H, int32_t K, const void *table, int32_t L, int32_t log2_T,
                            int32_t entry_bytes, const int32_t *N, int32_t tile_stripe,
                            int32_t chunk, int32_t block_from, int32_t hash_batch,
-                           int32_t mode, int32_t blocks, uint32_t *sink, void *stream)
+                           int32_t mode, int32_t blocks, uint32_t *work, uint32_t *sink,
+                           void *stream)
 {
     if (!x || !hit || !table || !N || !sink) return hipErrorInvalidValue;
     if (chunk < 0 || chunk > K || (chunk > 0 && (64 % chunk != 0 || (chunk & (chunk - 1)))))
@@ -406,7 +419,7 @@ int mixrt_mb_gather_replay(const float *x, const int32_t *hit, int32_t views, in
     hipStream_t s = (hipStream_t)stream;
 #define RP(EB, M)                                                                                \
     hipLaunchKernelGGL((replay_kernel<EB, M>), dim3(blocks), dim3(kBlock), 0, s, x, hit, views, \
-                       W, H, K, tile_stripe, chunk, gp, sink)
+                       W, H, K, tile_stripe, chunk, gp, work, sink)
     if (mode == 0) {
         if (entry_bytes == 4) RP(4, 0);
         else if (entry_bytes == 8) RP(8, 0);

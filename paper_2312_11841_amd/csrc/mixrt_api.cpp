@@ -825,8 +825,8 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
     if ((rc = bind_device(ctx))) return rc;
     mixrt::RenderLaunch L;
     fill_render_launch(L, ctx, gbuf, cams, disp, grid, mlp, smp, hid, nhid, nullptr);
-    int b = 0, st = 0, ch = 0, bf = 0, hb = 0;
-    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch, &bf, &hb);
+    int b = 0, st = 0, ch = 0, bf = 0, hb = 0, cl = 0;
+    const hipError_t e = mixrt::render_launch_shape(L, &b, &st, &ch, &bf, &hb, &cl);
     if (e != hipSuccess)
         return fail(ctx, MIXRT_EDEVICE, "render launch shape: %s", hipGetErrorString(e));
     plan->blocks = b;
@@ -834,6 +834,7 @@ int mixrt_render_launch_shape(mixrt_ctx *ctx, const mixrt_gbuffer *gbuf,
     plan->chunk = ch;
     plan->block_from = bf;
     plan->hash_batch = hb;
+    plan->claims = cl;
     return MIXRT_OK;
 }
 

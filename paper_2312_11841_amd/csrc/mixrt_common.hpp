@@ -38,6 +38,9 @@ __device__ __forceinline__ int xcd_logical_block(int b, int nb)
 // queue its waves' claims.  A wave claims its next unit while it runs the
 // current one's MLP, so the claim's latency is hidden.
 //
+// Without counters (a null pointer) every unit goes in the fixed order, the
+// static split's last round partial.
+//
 // The counters live in device memory the caller provides (kWorkWords
 // 32-bit words, zero before a launch): claim counter c of pool p at word
 // (p * kWorkSub + c) * kWorkStride, the count of the pool's finished blocks
@@ -54,15 +57,17 @@ inline constexpr int kWorkStaticMax = 16;   // at most this many
 
 struct WorkPools {
     unsigned int *ctr;
+    int nU;                  // units
     int P, pool, Wp, total, j, S, sub;
     int r;                   // static rounds taken
+    int Sc;                  // S with counters, -1 without (no claim is due)
     bool want;               // the next claim is still to be issued
     int end;                 // the units this wave's pool hands out
     unsigned int inv;        // ceil(2^32 / Wp), for dividing by Wp
     unsigned int pending;    // lane 0: the claim in flight
 
     __device__ __forceinline__ WorkPools(unsigned int *c, int n_units, int lane)
-        : ctr(c), r(0), want(false), pending(0u)
+        : ctr(c), nU(n_units), r(0), want(false), pending(0u)
     {
         const int nb = (int)gridDim.x;
         total = nb * kWavesPerBlock;
@@ -78,10 +83,19 @@ struct WorkPools {
         rest = rest < 0 ? 0 : rest > Wp ? Wp : rest;
         end = full * Wp + rest;
         inv = __builtin_amdgcn_readfirstlane(0xffffffffu / (unsigned int)Wp + 1u);
-        S = (full * kWorkStaticPct) / 100;
-        if (S > kWorkStaticMax) S = kWorkStaticMax;
-        if (S == 0 && full > 0) S = 1;
-        if (S == 0) pending = claim(lane);
+        if (ctr) {
+            S = (full * kWorkStaticPct) / 100;
+            if (S > kWorkStaticMax) S = kWorkStaticMax;
+            if (S == 0 && full > 0) S = 1;
+            if (S == 0) pending = claim(lane);
+            Sc = S;
+        } else {
+            // no counters: every unit in the fixed order, the last round
+            // partial, and no unit to claim after it
+            S = (n_units + total - 1) / total;
+            Sc = -1;
+            end = 0;
+        }
     }
     // issues the claim of the wave's next counted unit, if it is due.  The
     // kernels call this once their gathers of a unit have returned (memory
@@ -106,9 +120,10 @@ struct WorkPools {
     // the next unit of this wave, or -1 when its pool is spent
     __device__ __forceinline__ int take(int lane)
     {
-        if (r < S) {
+        if (__builtin_expect(r < S, 1)) {
             const int t = r * total + pool * Wp + j;
-            want = ++r == S;
+            if (t >= nU) return -1;   // the fixed order's partial last round
+            want = ++r == Sc;
             return t;
         }
         prefetch(lane);
@@ -127,6 +142,7 @@ struct WorkPools {
     // the pool's last block clears the pool's counters for the next launch
     __device__ __forceinline__ void finish() const
     {
+        if (!ctr) return;
         __syncthreads();
         if (threadIdx.x == 0) {
             unsigned int *done = &ctr[(kWorkPools * kWorkSub + pool) * kWorkStride];

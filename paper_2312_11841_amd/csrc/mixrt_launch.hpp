@@ -92,7 +92,7 @@ hipError_t phase_cycles_read(uint64_t *out, bool reset);
 // 16-byte block gathers and hashed levels per batch of gathers launch_render
 // would use (no launch).
 hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk,
-                               int *block_from, int *hash_batch);
+                               int *block_from, int *hash_batch, int *claims);
 hipError_t launch_ray_setup(const RayParams &rp, int tex, float *out_x, int32_t *out_hit,
                             hipStream_t stream);
 hipError_t launch_hash_encode(const GridParams &gp, int F, bool tf16, const float *x, int64_t n,

@@ -653,6 +653,18 @@ static int render_hash_batch(const RenderLaunch &L)
     return eb >= 8 && L.gp.L - L.gp.n_dense <= 4 ? 4 : 2;
 }
 
+// Whether the waves claim the last units of their pools from the work
+// counters (else every unit goes in the fixed order).  A claim is a
+// device-scope atomic whose round trip costs about as much as a unit of 64
+// samples over fewer than 8 levels without an MLP; there it is not hidden
+// (K = 1, Tab. 3's frames with the MLP removed: L = 1..4 are 9% slower with
+// claims), while with an MLP or 8 or more levels the balance they buy wins
+// (3-6% at K = 1, 6% on the 1280x720 K = 8 frame, 15% on the 8-view batch).
+static bool render_claims(const RenderLaunch &L)
+{
+    return L.nhid > 0 || L.gp.L >= 8;
+}
+
 // Grid size and tile order of a frame, given the blocks of its kernel that
 // fit on one CU.
 static void render_shape(const RenderLaunch &L, int resident, int64_t &blocks, int &stripe)
@@ -691,15 +703,16 @@ hipError_t launch_render(const RenderLaunch &L0, hipStream_t stream)
         int64_t blocks;                                                                        \
         int stripe;                                                                            \
         const int chunk = render_chunk(L);                                                     \
+        unsigned int *work = render_claims(L) ? L.work : nullptr;                              \
         render_shape(L, render_resident<a, b, c, d, e, f>(chunk > 0), blocks, stripe);         \
         if (chunk > 0)                                                                         \
             hipLaunchKernelGGL((render_queue_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks), \
                                dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh,      \
-                               L.hid_w, stripe, chunk, L.work, L.out);                         \
+                               L.hid_w, stripe, chunk, work, L.out);                           \
         else                                                                                   \
             hipLaunchKernelGGL((render_kernel<a, b, c, d, e, f>), dim3((unsigned)blocks),      \
                                dim3(kBlock), 0, stream, L.rp, L.gp, L.weights, L.view_sh,      \
-                               L.hid_w, stripe, L.work, L.out);                                \
+                               L.hid_w, stripe, work, L.out);                                  \
         return hipGetLastError();                                                              \
     }
     MIXRT_RENDER_VARIANTS(X)
@@ -725,10 +738,11 @@ hipError_t phase_cycles_read(uint64_t *out, bool reset)
 }
 
 hipError_t render_launch_shape(const RenderLaunch &L, int *blocks, int *stripe, int *chunk,
-                               int *block_from, int *hash_batch)
+                               int *block_from, int *hash_batch, int *claims)
 {
     *block_from = render_block_from(L);
     *hash_batch = render_hash_batch(L);
+    *claims = render_claims(L) ? 1 : 0;
 #define X(a, b, c, d, e, f)                                                                    \
     if (MIXRT_RENDER_MATCH(a, b, c, d, e, f)) {                                                \
         int64_t nb;                                                                            \

@@ -10,6 +10,7 @@ import os
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libmixrt_microbench.so")
+WORK_WORDS = 2560   # MIXRT_MB_WORK_WORDS: the replay's work counters
 _lib = None
 
 
@@ -32,7 +33,7 @@ def lib():
         L.mixrt_mb_rowstream.restype = C.c_int
         I32 = C.c_int32
         L.mixrt_mb_gather_replay.argtypes = [P, P, I32, I32, I32, I32, P, I32, I32, I32, P, I32,
-                                             I32, I32, I32, I32, I32, P, P]
+                                             I32, I32, I32, I32, I32, P, P, P]
         L.mixrt_mb_gather_replay.restype = C.c_int
         IP = C.POINTER(C.c_int)
         L.mixrt_mb_device_info.argtypes = [C.c_int, IP, IP, IP, IP, C.c_char_p, C.c_int]
@@ -162,7 +163,7 @@ def device_info(device: int = 0) -> dict:
 
 def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_stripe: int,
                   blocks_list, reps: int = 20, chunk: int = 0, block_from=None,
-                  hash_batch: int = 2):
+                  hash_batch: int = 2, claims: bool = True):
     """The frame's hash-grid loads replayed in the render kernel's order
     (mixrt_mb_gather_replay): for each grid size in blocks_list, the mean time
     of the loads (mode 0) and of their address arithmetic alone (mode 1).
@@ -170,7 +171,9 @@ def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_str
     frame's ray setup; table: the device hash table [L][T][F]; N: level
     resolutions; chunk: the render's samples per ray per round (0: the tile
     path); block_from: the render's first level of 16-byte block gathers
-    (None: none); hash_batch: its hashed levels per batch of gathers.
+    (None: none); hash_batch: its hashed levels per batch of gathers;
+    claims: whether the waves claim their last runs from work counters (the
+    plan's claims) or take every run in the fixed order.
     Returns per-grid-size times and the fastest."""
     import numpy as np
     import torch
@@ -182,6 +185,7 @@ def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_str
     assert Nh.size == L_ and T & (T - 1) == 0
     bf = L_ if block_from is None else int(block_from)
     rows = []
+    work = torch.zeros(WORK_WORDS, dtype=torch.int32, device=x.device)
     for blocks in blocks_list:
         sink = torch.empty(int(blocks) * 256, dtype=torch.int32, device=x.device)
         res = {"blocks": int(blocks)}
@@ -190,7 +194,8 @@ def gather_replay(x, hit, views: int, W: int, H: int, K: int, table, N, tile_str
                 _check(lib().mixrt_mb_gather_replay(
                     x.data_ptr(), hit.data_ptr(), views, W, H, K, table.data_ptr(), L_,
                     T.bit_length() - 1, eb, Nh.ctypes.data, int(tile_stripe), int(chunk), bf,
-                    int(hash_batch), mode, int(blocks), sink.data_ptr(), s.cuda_stream))
+                    int(hash_batch), mode, int(blocks), work.data_ptr() if claims else None,
+                    sink.data_ptr(), s.cuda_stream))
             for _ in range(3):
                 launch(torch.cuda.current_stream())
             res[name] = _timed(launch, reps) * 1e3

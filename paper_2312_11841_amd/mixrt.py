@@ -63,7 +63,7 @@ class CreateInfo(C.Structure):
 
 class LaunchPlan(C.Structure):
     _fields_ = [("blocks", C.c_int32), ("tile_stripe", C.c_int32), ("chunk", C.c_int32),
-                ("block_from", C.c_int32), ("hash_batch", C.c_int32)]
+                ("block_from", C.c_int32), ("hash_batch", C.c_int32), ("claims", C.c_int32)]
 
 
 class GBuffer(C.Structure):
@@ -497,7 +497,8 @@ class Renderer:
         """The mixrt_launch_plan of render(ds): blocks, tile_stripe, chunk
         (samples per ray per round, 0: the tile path), block_from (first
         level gathered in 16-byte blocks, L: none), hash_batch (hashed
-        levels per batch of gathers)."""
+        levels per batch of gathers), claims (1: each wave's last units are
+        claimed from the work counters, 0: all in the fixed order)."""
         plan = LaunchPlan()
         self._check(self._L.mixrt_render_launch_shape(
             self._h, C.byref(ds.gbuf), ds.cams, C.byref(ds.disp), C.byref(ds.grid),

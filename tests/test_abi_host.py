@@ -35,6 +35,41 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) <= exported
 
 
+def _kernel_private_segments(obj):
+    """{kernel: private segment bytes} of the gfx950 code in one object file
+    of this build (its offload bundle's kernel metadata)."""
+    llvm = "/opt/rocm/llvm/bin"
+    with tempfile.TemporaryDirectory() as d:
+        fat, co = os.path.join(d, "fat.bin"), os.path.join(d, "co.elf")
+        subprocess.run([f"{llvm}/llvm-objcopy", f"--dump-section=.hip_fatbin={fat}", obj],
+                       check=True, capture_output=True)
+        subprocess.run([f"{llvm}/clang-offload-bundler", "--unbundle", "--type=o",
+                        f"--input={fat}", "--targets=hipv4-amdgcn-amd-amdhsa--gfx950",
+                        f"--output={co}"], check=True, capture_output=True)
+        notes = subprocess.run([f"{llvm}/llvm-readelf", "--notes", co], check=True,
+                               capture_output=True, text=True).stdout
+    names = re.findall(r"^\s+\.name:\s+(\S+)", notes, flags=re.M)
+    sizes = [int(v) for v in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", notes)]
+    assert len(names) == len(sizes)
+    return dict(zip(names, sizes))
+
+
+@pytest.mark.parametrize("source", ["mixrt_render", "mixrt_stages", "mixrt_raycast",
+                                    "mixrt_raster", "microbench"])
+def test_kernels_use_no_scratch(source):
+    """No kernel of the library has a private (scratch) segment: no register
+    spills on the hot path, and no scratch memory the HIP runtime would have
+    to allocate at a kernel's first launch (mixrt_render_noalloc allocates
+    nothing, and neither does the runtime on its behalf)."""
+    from paper_2312_11841_amd import build
+    obj = os.path.join(build.OBJ_DIR, source + ".o")
+    if not os.path.exists(obj):
+        pytest.skip("library objects not built")
+    sizes = _kernel_private_segments(obj)
+    assert sizes, source
+    assert {k: v for k, v in sizes.items() if v} == {}
+
+
 @pytest.mark.parametrize("variant", ["timer", "split_nodisp", "split_nohash", "split_nomlp"])
 def test_profiling_builds_export_the_same_symbols(variant):
     """The profiling builds (the render kernel compiled with one -D option)

@@ -75,11 +75,13 @@ def test_tile_order_never_changes_a_pixel(cfg):
 def test_work_counters_are_ready_for_every_launch():
     """One context renders frames of different kernels and grid sizes in turn
     (a queue-kernel frame, a ragged frame, a one-sample frame on the tile
-    kernel and a frame of 25 tiles on 7 blocks, so in one pool), twice over: the pools'
+    kernel, a frame of 25 tiles on 7 blocks, so in one pool, and a frame
+    whose plan takes every unit in the fixed order), twice over: the pools'
     counters, left at zero by each launch's last blocks, give every later
     launch the same frame as a fresh context's first launch."""
     cfgs = [synth.VIEW720P, ORDER_CFGS[4], synth.PAPER720P,
-            synth.TINY64_DENSE.replace(name="one_pool", H=5, W=37, views=1, K=8, gbuf="iid")]
+            synth.TINY64_DENSE.replace(name="one_pool", H=5, W=37, views=1, K=8, gbuf="iid"),
+            _table3("tab3_L1_T17")]
     scenes = [mixrt.DeviceScene.from_scene(synth.make_scene(c), "cuda:0") for c in cfgs]
     refs = [_render(ds)[0] for ds in scenes]
     r = mixrt.Renderer(0, sync_check=True)
@@ -90,6 +92,7 @@ def test_work_counters_are_ready_for_every_launch():
                 say("counters", rep, cfg.name, plan)
                 if cfg.name == "one_pool":
                     assert plan["blocks"] == 7
+                assert plan["claims"] == (0 if cfg.name == "tab3_L1_T17" else 1)
                 out = torch.full((ds.rays, 4), float("nan"), dtype=torch.float32,
                                  device="cuda:0")
                 r.render(ds, out)
@@ -172,19 +175,23 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
     # hashed levels (4-byte entries only; other entry sizes ignore it)
     plan = r.launch_plan(ds)
     n_dense = int(sum((N.astype(np.int64) + 1) ** 3 <= cfg.T))
+    # one work buffer for every call: each call leaves its counters at zero
+    work = torch.zeros(mb.WORK_WORDS, dtype=torch.int32, device="cuda:0")
     for block_from in sorted({cfg.L, plan["block_from"], n_dense, 0}):
         for batch in (2, 4):
             for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
+              for claims in (True, False):
                 sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
                 rc = mb.lib().mixrt_mb_gather_replay(
                     x.data_ptr(), hit.data_ptr(), cfg.views, cfg.W, cfg.rows_kept, cfg.K,
                     ds.table.data_ptr(), cfg.L, cfg.log2_T, ds.table.element_size() * cfg.F,
                     N.ctypes.data, stripe, chunk, block_from, batch, 0, blocks,
-                    sink.data_ptr(), None)
+                    work.data_ptr() if claims else None, sink.data_ptr(), None)
                 assert rc == 0
                 torch.cuda.synchronize()
                 got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
-                assert got == acc, (block_from, batch, chunk)
+                assert got == acc, (block_from, batch, chunk, claims)
+    assert not work.any().item()
     r.close()
 
 
@@ -278,6 +285,27 @@ def test_default_gather_plan_follows_the_rule(cfg):
     plan = r.launch_plan(ds)
     r.close()
     assert (plan["block_from"], plan["hash_batch"]) == want, plan
+
+
+def _table3(name):
+    return synth.CONFIGS[name]
+
+
+@pytest.mark.parametrize("cfg", [synth.VIEW720P, synth.PAPER720P, synth.BATCH8X1080P,
+                                 _table3("tab3_L8_T17_mlp"), _table3("tab3_L1_T17"),
+                                 _table3("tab3_L4_T17"), _table3("tab3_L8_T5")],
+                         ids=lambda c: c.name)
+def test_default_claims_follow_the_rule(cfg):
+    """The last units are claimed from the work counters when a unit's work
+    hides a claim's latency: with an MLP, or with 8 or more levels."""
+    want = {"view720p": 1, "paper720p": 1, "batch8x1080p": 1, "tab3_L8_T17_mlp": 1,
+            "tab3_L1_T17": 0, "tab3_L4_T17": 0, "tab3_L8_T5": 1}[cfg.name]
+    sc = synth.make_scene(cfg.replace(H=16, W=64, views=1))
+    ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    r = mixrt.Renderer(0)
+    plan = r.launch_plan(ds)
+    r.close()
+    assert plan["claims"] == want, plan
 
 
 QUEUE_CFGS = [
