@@ -318,7 +318,6 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
 {
     constexpr int kGroup = 2;
     const int lane = threadIdx.x & 63;
-    const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const int R = 64 / K;
     const mixrt::TileShape ts = mixrt::tile_shape(R, views, W, H, stripe);
     const int L = gp.L, n_dense = gp.n_dense;

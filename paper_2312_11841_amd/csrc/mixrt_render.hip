@@ -525,23 +525,24 @@ bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nh
 }
 
 // Persistent blocks per CU for a frame, given the most that fit (`resident`).
-// More waves hide more latency when the gathers of a wave hit the same cache
-// lines: several samples per ray, spaced finer than the cells of at least
-// half the levels, on levels whose table fits one XCD's L2.  When the gathers
-// scatter instead (one or two samples per ray, widely spaced samples, or
-// levels larger than the L2), 2 blocks per CU keep more of each wave's lines
-// in the caches and run faster than the full occupancy.  The count changes
-// only which wave renders which tile, never a result.
+// More waves hide more latency, except where a wave's gathers touch so many
+// lines that fewer waves keep more of each one's lines in the caches: rays
+// whose K >= 4 samples lie apart on most levels (spaced coarser than the
+// cells of half the levels), and kernels without an MLP, whose waves do
+// little besides gathering.  There 2 blocks per CU run faster than the full
+// occupancy.  Large tables (8 MiB levels) and one or two samples per ray
+// also wanted 2 blocks per CU while every unit went in the fixed order; with
+// each XCD's last units claimed from counters its working set stays compact
+// and the full occupancy wins there (7-17%).  The count changes only which
+// wave renders which tile, never a result.
 static int levels_shared_by_samples(const RenderLaunch &L);
 
 static int render_blocks_per_cu(const RenderLaunch &L, int resident)
 {
     if (L.blocks_mode == 1) return resident;
     if (L.blocks_mode == 2) return resident < 2 ? resident : 2;
-    const int shared = levels_shared_by_samples(L);
-    const int64_t level_bytes = ((int64_t)L.gp.T_mask + 1) * L.F * (L.tf16 ? 2 : 4);
-    const bool coherent = L.rp.K >= 4 && 2 * shared >= L.gp.L && level_bytes <= L.l2_bytes;
-    return coherent || resident < 2 ? resident : 2;
+    const bool scattered = L.rp.K >= 4 && 2 * levels_shared_by_samples(L) < L.gp.L;
+    return (scattered || L.nhid == 0) && resident > 2 ? 2 : resident;
 }
 
 // Tile order for a frame (the stripe width of tile_at, in tiles).  Waves
