@@ -528,9 +528,9 @@ bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nh
 // More waves hide more latency, except where a wave's gathers touch so many
 // lines that fewer waves keep more of each one's lines in the caches: rays
 // whose K >= 4 samples lie apart on most levels (spaced coarser than the
-// cells of half the levels), and kernels without an MLP, whose waves do
-// little besides gathering.  There 2 blocks per CU run faster than the full
-// occupancy.  Large tables (8 MiB levels) and one or two samples per ray
+// cells of half the levels), and kernels without an MLP or with one of
+// hidden width 16 or less (Tab. 3's 2 x 8), whose waves do little besides
+// gathering.  There 2 blocks per CU run faster than the full occupancy.  Large tables (8 MiB levels) and one or two samples per ray
 // also wanted 2 blocks per CU while every unit went in the fixed order; with
 // each XCD's last units claimed from counters its working set stays compact
 // and the full occupancy wins there (7-17%).  The count changes only which
@@ -542,7 +542,8 @@ static int render_blocks_per_cu(const RenderLaunch &L, int resident)
     if (L.blocks_mode == 1) return resident;
     if (L.blocks_mode == 2) return resident < 2 ? resident : 2;
     const bool scattered = L.rp.K >= 4 && 2 * levels_shared_by_samples(L) < L.gp.L;
-    return (scattered || L.nhid == 0) && resident > 2 ? 2 : resident;
+    const bool light = L.nhid == 0 || L.hid_w <= 16;
+    return (scattered || light) && resident > 2 ? 2 : resident;
 }
 
 // Tile order for a frame (the stripe width of tile_at, in tiles).  Waves
