@@ -57,18 +57,17 @@ inline constexpr int kWorkStaticMax = 16;   // at most this many
 
 struct WorkPools {
     unsigned int *ctr;
+    int nU;                  // units
     int P, pool, Wp, total, j, S, sub;
     int r;                   // static rounds taken
     int Sc;                  // S with counters, -1 without (no claim is due)
     bool want;               // the next claim is still to be issued
     int end;                 // the units this wave's pool hands out
-    int end_static;          // the same, for the fixed order
-    int full, rp;            // full rounds; units per pool in the last one
     unsigned int inv;        // ceil(2^32 / Wp), for dividing by Wp
     unsigned int pending;    // lane 0: the claim in flight
 
     __device__ __forceinline__ WorkPools(unsigned int *c, int n_units, int lane)
-        : ctr(c), r(0), want(false), pending(0u)
+        : ctr(c), nU(n_units), r(0), want(false), pending(0u)
     {
         const int nb = (int)gridDim.x;
         total = nb * kWavesPerBlock;
@@ -79,15 +78,10 @@ struct WorkPools {
         j = (P == 8 ? (int)(blockIdx.x >> 3) : (int)blockIdx.x) * kWavesPerBlock +
             (int)__builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
         sub = j & (kWorkSub - 1);
-        full = n_units / total;
-        // the last, partial round is split evenly over the pools, rp units
-        // each (the last pools may get fewer)
-        const int rest = n_units - full * total;
-        rp = (rest + P - 1) / P;
-        int cnt = rest - pool * rp;
-        cnt = cnt < 0 ? 0 : cnt > rp ? rp : cnt;
-        end = full * Wp + cnt;
-        end_static = end;
+        const int full = n_units / total;
+        int rest = n_units - full * total - pool * Wp;
+        rest = rest < 0 ? 0 : rest > Wp ? Wp : rest;
+        end = full * Wp + rest;
         inv = __builtin_amdgcn_readfirstlane(0xffffffffu / (unsigned int)Wp + 1u);
         if (ctr) {
             S = (full * kWorkStaticPct) / 100;
@@ -96,9 +90,9 @@ struct WorkPools {
             if (S == 0) pending = claim(lane);
             Sc = S;
         } else {
-            // no counters: every unit in the fixed order, and no unit to
-            // claim after it
-            S = full + (cnt > 0);
+            // no counters: every unit in the fixed order, the last round
+            // partial, and no unit to claim after it
+            S = (n_units + total - 1) / total;
             Sc = -1;
             end = 0;
         }
@@ -127,12 +121,8 @@ struct WorkPools {
     __device__ __forceinline__ int take(int lane)
     {
         if (__builtin_expect(r < S, 1)) {
-            int t = r * total + pool * Wp + j;
-            if (r == full) {
-                // the partial last round (fixed order only)
-                if (full * Wp + j >= end_static) return -1;
-                t = full * total + pool * rp + j;
-            }
+            const int t = r * total + pool * Wp + j;
+            if (t >= nU) return -1;   // the fixed order's partial last round
             want = ++r == Sc;
             return t;
         }
@@ -141,11 +131,8 @@ struct WorkPools {
         const int d = S * Wp + c * kWorkSub + sub;
         if (d >= end) return -1;
         want = true;
-        // pool unit d is unit (d / Wp) * total + pool * Wp + d % Wp in the
-        // full rounds (the quotient from the reciprocal is exact or one too
-        // large, d < 2^31), and full * total + pool * rp + (d - full * Wp)
-        // in the last one
-        if (d >= full * Wp) return full * total + pool * rp + (d - full * Wp);
+        // pool unit d is unit (d / Wp) * total + pool * Wp + d % Wp; the
+        // quotient from the reciprocal is exact or one too large (d < 2^31)
         unsigned int q = __umulhi((unsigned int)d, inv);
         if (q * (unsigned int)Wp > (unsigned int)d) --q;
         return (int)q * (total - Wp) + pool * Wp + d;
