@@ -35,9 +35,9 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) <= exported
 
 
-def _kernel_private_segments(obj):
-    """{kernel: private segment bytes} of the gfx950 code in one object file
-    of this build (its offload bundle's kernel metadata)."""
+def _kernel_metadata(obj, field):
+    """{kernel: value of an integer metadata field} of the gfx950 code in one
+    object file of this build (its offload bundle's kernel metadata)."""
     llvm = "/opt/rocm/llvm/bin"
     with tempfile.TemporaryDirectory() as d:
         fat, co = os.path.join(d, "fat.bin"), os.path.join(d, "co.elf")
@@ -49,9 +49,13 @@ def _kernel_private_segments(obj):
         notes = subprocess.run([f"{llvm}/llvm-readelf", "--notes", co], check=True,
                                capture_output=True, text=True).stdout
     names = re.findall(r"^\s+\.name:\s+(\S+)", notes, flags=re.M)
-    sizes = [int(v) for v in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", notes)]
-    assert len(names) == len(sizes)
-    return dict(zip(names, sizes))
+    values = [int(v) for v in re.findall(rf"\.{field}:\s+(\d+)", notes)]
+    assert len(names) == len(values)
+    return dict(zip(names, values))
+
+
+def _kernel_private_segments(obj):
+    return _kernel_metadata(obj, "private_segment_fixed_size")
 
 
 @pytest.mark.parametrize("source", ["mixrt_render", "mixrt_stages", "mixrt_raycast",
@@ -68,6 +72,33 @@ def test_kernels_use_no_scratch(source):
     sizes = _kernel_private_segments(obj)
     assert sizes, source
     assert {k: v for k, v in sizes.items() if v} == {}
+
+
+# The render kernels of the 1280x720 view and the 8-view batch (fp16 grid
+# of 2 features, along-ray map, MLP 48-64-64-4) and of the paper's deployed
+# grid, with the waves per SIMD their registers allow: 512 VGPRs per lane
+# and SIMD, allocated in granules of 8.
+HOT_KERNELS = {
+    "_ZN5mixrt19render_queue_kernelILi1ELi2ELb1ELi48ELi64ELi2EEE": 3,
+    "_ZN5mixrt13render_kernelILi1ELi2ELb1ELi48ELi64ELi2EEE": 3,
+    "_ZN5mixrt13render_kernelILi5ELi4ELb1ELi32ELi64ELi2EEE": 2,
+}
+
+
+def test_hot_kernels_keep_their_occupancy():
+    """The measured workloads' kernels keep the waves per SIMD their launch
+    rules and timings assume (a few more registers in these kernels have
+    cost 20% by dropping a wave)."""
+    from paper_2312_11841_amd import build
+    obj = os.path.join(build.OBJ_DIR, "mixrt_render.o")
+    if not os.path.exists(obj):
+        pytest.skip("library objects not built")
+    vgprs = _kernel_metadata(obj, "vgpr_count")
+    for prefix, waves in HOT_KERNELS.items():
+        found = [v for k, v in vgprs.items() if k.startswith(prefix)]
+        assert len(found) == 1, prefix
+        granule = (found[0] + 7) // 8 * 8
+        assert 512 // granule >= waves, (prefix, found[0])
 
 
 @pytest.mark.parametrize("variant", ["timer", "split_nodisp", "split_nohash", "split_nomlp"])
