@@ -660,11 +660,16 @@ __device__ __forceinline__ float corner_weight(const LevelSetup &s, int b)
 
 // Word i of an aligned 16-byte block, i = bits 2-3 of the entry's byte
 // offset, picked with bit masks (as selects, the compiler turns the pick
-// into an indexed read of a private copy of the block)
+// into an indexed read of a private copy of the block).  The empty asm
+// statement hides that the masks are all zeros or all ones, so they stay
+// one bitfield extract each and the picks three bitfield inserts, instead
+// of compares into lane masks and selects that need wait states between
+// them (block-gather frames 0.3-1% faster).
 __device__ __forceinline__ uint32_t block_word(const uint4 &q, uint32_t off)
 {
-    const uint32_t m8 = (uint32_t)((int32_t)(off << 28) >> 31);   // bit 3 set: all ones
-    const uint32_t m4 = (uint32_t)((int32_t)(off << 29) >> 31);   // bit 2 set: all ones
+    uint32_t m8 = (uint32_t)__builtin_amdgcn_sbfe((int)off, 3, 1);   // bit 3 set: all ones
+    uint32_t m4 = (uint32_t)__builtin_amdgcn_sbfe((int)off, 2, 1);   // bit 2 set: all ones
+    asm volatile("" : "+v"(m8), "+v"(m4));
     const uint32_t lo = (q.z & m8) | (q.x & ~m8);
     const uint32_t hi = (q.w & m8) | (q.y & ~m8);
     return (hi & m4) | (lo & ~m4);
