@@ -268,17 +268,17 @@ def test_default_round_size_follows_the_rule(cfg):
 @pytest.mark.parametrize("cfg", [synth.VIEW720P, synth.VIEW720P_DENSE,
                                  synth.VIEW720P.replace(name="k1", K=1),
                                  synth.VIEW720P.replace(name="fine_spacing", delta=1e-4),
-                                 synth.BATCH8X1080P, synth.PAPER720P, synth.DEPLOYED720P,
-                                 synth.TABLE3[0]],
+                                 synth.BATCH8X1080P, synth.BATCH8X1080P.replace(name="batch_k4", K=4),
+                                 synth.PAPER720P, synth.DEPLOYED720P, synth.TABLE3[0]],
                          ids=lambda c: c.name)
 def test_default_gather_plan_follows_the_rule(cfg):
-    """Block gathers on the three finest levels (four when a level's table
-    exceeds one XCD's L2) among hashed levels finer than the sample spacing,
-    4-byte entries only; batches of 4 hashed levels only for entries of 8+
-    bytes when that covers every hashed level."""
+    """Block gathers on the three finest levels (when a level's table exceeds
+    one XCD's L2: four, and eight at K >= 8) among hashed levels finer than
+    the sample spacing, 4-byte entries only; batches of 4 hashed levels only
+    for entries of 8+ bytes when that covers every hashed level."""
     want = {"view720p": (13, 2), "view720p_dense": (13, 2), "k1": (13, 2),
-            "fine_spacing": (16, 2), "batch8x1080p": (12, 2), "paper720p": (4, 4),
-            "deployed720p": (4, 4), "tab3_L8_T17_mlp": (8, 2)}[cfg.name]
+            "fine_spacing": (16, 2), "batch8x1080p": (8, 2), "batch_k4": (12, 2),
+            "paper720p": (4, 4), "deployed720p": (4, 4), "tab3_L8_T17_mlp": (8, 2)}[cfg.name]
     sc = synth.make_scene(cfg.replace(H=16, W=64, views=1))
     ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
     r = mixrt.Renderer(0)
