@@ -7,7 +7,8 @@ that measures the floor of its gather stream.
 
   - every tile order renders the same frame bit for bit, and every pixel;
   - the work counters are back at zero after every launch, whatever the
-    kernel and grid size of the next one;
+    kernel and grid size of the next one, and two contexts (each with its
+    own counters) render on two streams at once;
   - the early-termination path renders the tile path's frame bit for bit
     (the same samples composited in the same order), at every round size,
     and evaluates fewer samples on opaque content;
@@ -100,6 +101,32 @@ def test_work_counters_are_ready_for_every_launch():
                 assert np.array_equal(out.cpu().numpy(), ref), (rep, cfg.name)
     finally:
         r.close()
+
+
+def test_contexts_on_two_streams_render_at_once():
+    """Two contexts, each with its own work counters, render on two streams
+    at the same time (launches alternate between the streams with no wait in
+    between): every frame equals a lone context's."""
+    cfgs = [synth.VIEW720P, synth.PAPER720P]
+    scenes = [mixrt.DeviceScene.from_scene(synth.make_scene(c), "cuda:0") for c in cfgs]
+    refs = [_render(ds)[0] for ds in scenes]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    rs = [mixrt.Renderer(0, stream=st) for st in streams]
+    outs = [[torch.full((ds.rays, 4), float("nan"), dtype=torch.float32, device="cuda:0")
+             for _ in range(3)] for ds in scenes]
+    try:
+        torch.cuda.synchronize()
+        for rep in range(3):
+            for r, ds, o in zip(rs, scenes, outs):
+                r.render(ds, o[rep])
+        torch.cuda.synchronize()
+        for cfg, ref, o in zip(cfgs, refs, outs):
+            for rep in range(3):
+                say("two streams", cfg.name, rep)
+                assert np.array_equal(o[rep].cpu().numpy(), ref), (cfg.name, rep)
+    finally:
+        for r in rs:
+            r.close()
 
 
 def test_tile_order_spot_check_against_the_oracle():
