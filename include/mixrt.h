@@ -203,8 +203,9 @@ typedef struct {
 
 /* Create a context bound to ci->device and ci->hip_stream.  Fails with
  * MIXRT_EUNSUPPORTED unless the device is gfx950. *out is NULL on failure.
- * Allocates the context's 10 KiB of render work counters on ci->device
- * (MIXRT_ENOMEM if that fails); the caller's current device is kept.
+ * Allocates and zeroes the context's 10 KiB of render work counters on
+ * ci->device and waits for the device to finish that (MIXRT_ENOMEM if the
+ * allocation fails); the caller's current device is kept.
  * Renders of one context must not run at the same time (they share the
  * counters): keep them on its stream. */
 int mixrt_create(mixrt_ctx **out, const mixrt_create_info *ci);
