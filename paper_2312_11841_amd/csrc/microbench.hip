@@ -203,8 +203,8 @@ __global__ __launch_bounds__(kBlock) void mfma_kernel(int iters, float *__restri
 // tile order (stripe) as the render kernel; a lane takes the
 // same sample of the same tile, reads that sample's position from the frame's
 // ray-setup output, and issues the same loads in the same batches (dense
-// levels as x-neighbour pairs, hashed levels of 4-byte entries as 16-byte
-// blocks per x-neighbour pair, two levels per batch).  The corner entries'
+// levels as x-neighbour pairs, hashed levels of 4- or 8-byte entries from
+// block_from on as 16-byte blocks per x-neighbour pair).  The corner entries'
 // words are XOR-folded into one word per lane (no fp16 conversion, no interpolation,
 // no MLP, no compositing), so the kernel's time is the floor that this exact
 // access stream, plus the address arithmetic that produces it, sets.  MODE 1
@@ -256,11 +256,11 @@ __device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, in
 #pragma unroll
     for (int g = 0; g < G; ++g)
         mixrt::level_setup<EB, true>(gp, l0 + g, DENSE, x0, x1, x2, s[g]);
-    // hashed levels with 4-byte entries from block_from on: the render's
-    // block loads (one aligned 16-byte block per x-neighbour pair, the x + 1
-    // entries loaded apart where the voxel straddles two blocks), and the
-    // two words picked
-    constexpr bool kBlocks = BLOCKS && !DENSE && EB == 4;
+    // hashed levels with 4- or 8-byte entries from block_from on: the
+    // render's block loads (one aligned 16-byte block per x-neighbour pair,
+    // the x + 1 entries loaded apart where the voxel straddles two blocks),
+    // and the two entries' words picked
+    constexpr bool kBlocks = BLOCKS && !DENSE && (EB == 4 || EB == 8);
     uint32_t v[G][8];
     uint4 blk[G][4];
     uint32_t far[G][4];
@@ -296,8 +296,15 @@ __device__ __forceinline__ uint32_t replay_group(const mixrt::GridParams &gp, in
             const bool straddle = (s[g].off[0] ^ s[g].off[1]) >= 16u;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                acc ^= mixrt::block_word(blk[g][q], s[g].off[2 * q]);
-                acc ^= straddle ? far[g][q] : mixrt::block_word(blk[g][q], s[g].off[2 * q + 1]);
+                if constexpr (EB == 4) {
+                    acc ^= mixrt::block_word(blk[g][q], s[g].off[2 * q]);
+                    acc ^= straddle ? far[g][q] : mixrt::block_word(blk[g][q], s[g].off[2 * q + 1]);
+                } else {
+                    // 8-byte entries: the pair's two entries are the block's halves
+                    const uint4 b = blk[g][q];
+                    acc ^= straddle ? (((s[g].off[2 * q] & 8u) ? (b.z ^ b.w) : (b.x ^ b.y)) ^ far[g][q])
+                                    : (b.x ^ b.y ^ b.z ^ b.w);
+                }
             }
             continue;
         }
@@ -360,11 +367,16 @@ __global__ __launch_bounds__(kBlock) void replay_kernel(const float *__restrict_
         int l = 0;
         for (; l + kGroup <= n_dense; l += kGroup) acc ^= replay_group<EB, kGroup, true, MODE>(gp, l, x0, x1, x2);
         for (; l < n_dense; ++l) acc ^= replay_group<EB, 1, true, MODE>(gp, l, x0, x1, x2);
-        const int lb = EB == 4 && gp.block_from < L ? max(gp.block_from, l) : L;
-        if (EB >= 8 && gp.hash_batch >= 4)
+        const int lb = (EB == 4 || EB == 8) && gp.block_from < L ? max(gp.block_from, l) : L;
+        // 8-byte entries: 4 levels per batch without blocks when hash_batch
+        // asks for it, else pairs of levels, with blocks from block_from on,
+        // as the render batches them
+        if (EB >= 8 && gp.hash_batch >= 4 && lb == L)
             for (; l + 4 <= lb; l += 4) acc ^= replay_group<EB, 4, false, MODE>(gp, l, x0, x1, x2);
         for (; l + kGroup <= lb; l += kGroup) acc ^= replay_group<EB, kGroup, false, MODE>(gp, l, x0, x1, x2);
         for (; l < lb; ++l) acc ^= replay_group<EB, 1, false, MODE>(gp, l, x0, x1, x2);
+        if (EB == 8)
+            for (; l + kGroup <= L; l += kGroup) acc ^= replay_group<EB, kGroup, false, MODE, true>(gp, l, x0, x1, x2);
         for (; l < L; ++l) acc ^= replay_group<EB, 1, false, MODE, true>(gp, l, x0, x1, x2);
     }
     pools.prefetch(lane);

@@ -498,6 +498,14 @@ struct TableEntry<2, false> {
 template <>
 struct TableEntry<4, true> {
     static constexpr uint32_t kBytes = 8;
+    static __device__ __forceinline__ void from_pair(const uint2 raw, float *v)
+    {
+        const h2 a = __builtin_bit_cast(h2, raw.x), b = __builtin_bit_cast(h2, raw.y);
+        v[0] = (float)a.x;
+        v[1] = (float)a.y;
+        v[2] = (float)b.x;
+        v[3] = (float)b.y;
+    }
     static __device__ __forceinline__ void load(const char *t, uint32_t off, float *v)
     {
         const uint2 raw = *(const uint2 *)(t + off);
@@ -682,15 +690,21 @@ __device__ __forceinline__ uint32_t block_word(const uint4 &q, uint32_t off)
 template <int F, bool F16>
 constexpr bool kBlockPairs = TableEntry<F, F16>::kBytes == 4;
 
+// The same for 8-byte entries (F = 4 fp16, the deployed grid's): the
+// entries of x and x + 1 share an aligned 16-byte block when x is even.
+template <int F, bool F16>
+constexpr bool kBlockPairs8 = F16 && TableEntry<F, F16>::kBytes == 8;
+
 // The 8 corner entries of a level: 4 pair loads on a dense level, 8 single
-// loads on a hashed one.  BLOCKS (hashed levels of 4-byte entries): one
-// 16-byte block load per x-neighbour pair, which holds both entries in 3
-// voxels of 4, plus a load of each x + 1 entry in the lanes whose voxel
-// straddles two blocks: 4 full gathers and 4 partial ones instead of 8 full
-// ones.  The vector L1 charges a scattered gather by the lanes and distinct
-// lines it touches whatever its width, so this pays on levels whose lanes
-// touch distinct lines (the finest); where lanes share lines a 16-byte
-// gather costs more than a 4-byte one and the word picks cost ALU work.
+// loads on a hashed one.  BLOCKS (hashed levels of 4- or 8-byte entries):
+// one 16-byte block load per x-neighbour pair, which holds both entries in
+// 3 voxels of 4 (4-byte entries) or 1 of 2 (8-byte entries), plus a load of
+// each x + 1 entry in the lanes whose voxel straddles two blocks: 4 full
+// gathers and 4 partial ones instead of 8 full ones.  The vector L1 charges
+// a scattered gather by the lanes and distinct lines it touches whatever
+// its width, so this pays on levels whose lanes touch distinct lines (the
+// finest); where lanes share lines a 16-byte gather costs more than a
+// narrower one and the word picks cost ALU work.
 template <int F, bool F16, bool DENSE, bool BLOCKS = false>
 __device__ __forceinline__ void level_fetch(const void *table_l, const LevelSetup &s,
                                             float (*v)[F])
@@ -720,6 +734,33 @@ __device__ __forceinline__ void level_fetch(const void *table_l, const LevelSetu
             const uint32_t w1 = straddle ? far[q] : block_word(blk[q], s.off[2 * q + 1]);
             TableEntry<F, F16>::from_word(w0, v[2 * q]);
             TableEntry<F, F16>::from_word(w1, v[2 * q + 1]);
+        }
+    } else if constexpr (BLOCKS && kBlockPairs8<F, F16>) {
+        // the entries of x and x + 1 differ in bit 0 of the index when x is
+        // even (one block, the halves picked by bit 3 of the offset) and in
+        // higher bits when x is odd (a straddle, the same for all four)
+        const bool straddle = (s.off[0] ^ s.off[1]) >= 16u;
+        uint4 blk[4];
+        uint2 far[4] = {{0u, 0u}, {0u, 0u}, {0u, 0u}, {0u, 0u}};
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            blk[q] = *(const uint4 *)(t + (s.off[2 * q] & ~15u));
+        if (straddle) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                far[q] = *(const uint2 *)(t + s.off[2 * q + 1]);
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            // bit 3 set: the x entry is the block's upper half (a mask kept
+            // opaque, as in block_word)
+            uint32_t m = (uint32_t)__builtin_amdgcn_sbfe((int)s.off[2 * q], 3, 1);
+            asm volatile("" : "+v"(m));
+            const uint2 e0 = {(blk[q].z & m) | (blk[q].x & ~m), (blk[q].w & m) | (blk[q].y & ~m)};
+            const uint2 e1o = {(blk[q].x & m) | (blk[q].z & ~m), (blk[q].y & m) | (blk[q].w & ~m)};
+            const uint2 e1 = straddle ? far[q] : e1o;
+            TableEntry<F, F16>::from_pair(e0, v[2 * q]);
+            TableEntry<F, F16>::from_pair(e1, v[2 * q + 1]);
         }
     } else {
 #pragma unroll

@@ -77,8 +77,10 @@ __device__ __forceinline__ void encode_levels(const GridParams &gp, int l0, floa
 // Every level of one query in order: dense levels, hashed levels with
 // single-entry gathers (gp.hash_batch levels per batch, 4 only for entries
 // of 8 or more bytes), then hashed levels from gp.block_from on with 16-byte
-// block gathers (4-byte entries), one level per batch there (two levels'
-// blocks in flight would cost a wave of occupancy).
+// block gathers: one level per batch for 4-byte entries (two levels' blocks
+// in flight would cost a wave of occupancy), 2 for 8-byte ones (fp16 F = 4;
+// batches of 4 raise these kernels' registers by about 40 and were 1-2%
+// slower on 8 and 16 levels).
 template <int F, bool TF16, bool SUM>
 __device__ __forceinline__ void encode_query(const GridParams &gp, float x0, float x1, float x2,
                                              _Float16 *row, float *acc)
@@ -90,6 +92,23 @@ __device__ __forceinline__ void encode_query(const GridParams &gp, float x0, flo
     for (; l < n_dense; ++l)
         encode_levels<F, TF16, 1, true, SUM>(gp, l, x0, x1, x2, row, acc);
     const int lb = kBlockPairs<F, TF16> && gp.block_from < L ? max(gp.block_from, l) : L;
+    if constexpr (kBlockPairs8<F, TF16>) {
+        // 8-byte entries from gp.block_from on: 16-byte blocks of
+        // x-neighbour pairs, 2 levels per batch
+        if (gp.block_from < L) {
+            // (l < gp.block_from is implied; spelled out, it keeps a dead
+            // stack frame out of the texture-less kernel's build)
+            for (; l < gp.block_from && l + kLevelGroup <= gp.block_from; l += kLevelGroup)
+                encode_levels<F, TF16, kLevelGroup, false, SUM>(gp, l, x0, x1, x2, row, acc);
+            for (; l < gp.block_from; ++l)
+                encode_levels<F, TF16, 1, false, SUM>(gp, l, x0, x1, x2, row, acc);
+            for (; l + kLevelGroup <= L; l += kLevelGroup)
+                encode_levels<F, TF16, kLevelGroup, false, SUM, true>(gp, l, x0, x1, x2, row, acc);
+            for (; l < L; ++l)
+                encode_levels<F, TF16, 1, false, SUM, true>(gp, l, x0, x1, x2, row, acc);
+            return;
+        }
+    }
     if constexpr (TableEntry<F, TF16>::kBytes >= 8) {
         if (gp.hash_batch >= 4)
             for (; l + 4 <= lb; l += 4)
@@ -110,8 +129,16 @@ struct NoMlp {
     __device__ __forceinline__ void load(const _Float16 *, int, int) {}
 };
 
+// Kernels without an MLP or with hidden layers of 16 or fewer neurons always
+// run at 2 blocks per CU (the light case of the blocks-per-CU rule: 2 waves
+// per SIMD), so the compiler is told it may schedule for 2 waves instead of
+// the most that fit.  Measured on Tab. 3's rows: 4 levels of 2^17 entries
+// 12% faster, 8 and 16 levels within 1% either way.
+#define MIXRT_LIGHT_WAVES(NHID, HID) \
+    __attribute__((amdgpu_waves_per_eu(1, ((NHID) == 0 || (HID) <= 16) ? 2 : 8)))
+
 template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
-__global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams gp,
+__global__ __launch_bounds__(kBlock) MIXRT_LIGHT_WAVES(NHID, HID) void render_kernel(RayParams rp, GridParams gp,
                                                         const _Float16 *__restrict__ weights,
                                                         int view_sh, int hid_w, int stripe,
                                                         unsigned int *__restrict__ work,
@@ -286,7 +313,7 @@ __global__ __launch_bounds__(kBlock) void render_kernel(RayParams rp, GridParams
 // Needs C <= K and C dividing 64.
 // ---------------------------------------------------------------------------
 template <int TEX, int F, bool TF16, int IN, int HID, int NHID>
-__global__ __launch_bounds__(kBlock) void render_queue_kernel(RayParams rp, GridParams gp,
+__global__ __launch_bounds__(kBlock) MIXRT_LIGHT_WAVES(NHID, HID) void render_queue_kernel(RayParams rp, GridParams gp,
                                                               const _Float16 *__restrict__ weights,
                                                               int view_sh, int hid_w, int stripe,
                                                               int C, unsigned int *__restrict__ work,
@@ -530,11 +557,13 @@ bool render_variant_supported(int tex, int F, bool tf16, int in, int hid, int nh
 // whose K >= 4 samples lie apart on most levels (spaced coarser than the
 // cells of half the levels), and kernels without an MLP or with one of
 // hidden width 16 or less (Tab. 3's 2 x 8), whose waves do little besides
-// gathering.  There 2 blocks per CU run faster than the full occupancy.  Large tables (8 MiB levels) and one or two samples per ray
-// also wanted 2 blocks per CU while every unit went in the fixed order; with
-// each XCD's last units claimed from counters its working set stays compact
-// and the full occupancy wins there (7-17%).  The count changes only which
-// wave renders which tile, never a result.
+// gathering (their kernels are compiled for 2 waves per SIMD).  There 2
+// blocks per CU run faster than the full occupancy.  Large tables (8 MiB
+// levels) and one or two samples per ray also wanted 2 blocks per CU while
+// every unit went in the fixed order; with each XCD's last units claimed from
+// counters its working set stays compact and the full occupancy wins there
+// (7-17%).  The count changes only which wave renders which tile, never a
+// result.
 static int levels_shared_by_samples(const RenderLaunch &L);
 
 static int render_blocks_per_cu(const RenderLaunch &L, int resident)
@@ -629,7 +658,15 @@ static int render_chunk(const RenderLaunch &L)
 static int render_block_from(const RenderLaunch &L)
 {
     const int nl = L.gp.L;
-    if (!(L.tf16 && L.F == 2) || L.block_levels < 0) return nl;
+    if (L.block_levels < 0) return nl;
+    if (L.tf16 && L.F == 4) {
+        // 8-byte entries: every hashed level, with 8 or more of them in
+        // tables of at least 2^10 entries
+        const int nd = L.gp.n_dense;
+        if (L.block_levels > 0) return nl - L.block_levels > nd ? nl - L.block_levels : nd;
+        return nl - nd >= 8 && L.gp.T_mask >= 1023u ? nd : nl;
+    }
+    if (!(L.tf16 && L.F == 2)) return nl;
     int lo = L.gp.n_dense;
     if (L.block_levels > 0) return nl - L.block_levels > lo ? nl - L.block_levels : lo;
     const int64_t level_bytes = ((int64_t)L.gp.T_mask + 1) * 4;

@@ -170,7 +170,11 @@ def test_default_library_has_no_phase_timer():
 
 @pytest.mark.parametrize("cfg", [synth.TINY64_DENSE.replace(name="replay_tiny", H=40, W=56),
                                  synth.VIEW720P.replace(name="replay_720p_rows", rows=48),
-                                 synth.DEPLOYED720P.replace(name="replay_f4", rows=64)],
+                                 synth.DEPLOYED720P.replace(name="replay_f4", rows=64),
+                                 synth.TABLE3[0].replace(name="replay_f4_L8", rows=48),
+                                 synth.TABLE3[0].replace(name="replay_f4_ragged", H=23, W=37,
+                                                         views=2, K=3, gbuf="iid", delta=0.5,
+                                                         log2_T=12)],
                          ids=lambda c: c.name)
 def test_gather_replay_loads_exactly_the_corner_entries(cfg):
     from paper_2312_11841_amd import microbench as mb
@@ -199,14 +203,15 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
         acc ^= np.bitwise_xor.reduce(w.reshape(-1))
     # the tile path's order and every rounds order the render can take, with
     # the render's 16-byte block gathers on none, the library's choice, all
-    # hashed levels (4-byte entries only; other entry sizes ignore it)
+    # hashed levels (4- and 8-byte entries; 16-byte ones ignore it)
     plan = r.launch_plan(ds)
     n_dense = int(sum((N.astype(np.int64) + 1) ** 3 <= cfg.T))
     # one work buffer for every call: each call leaves its counters at zero
     work = torch.zeros(mb.WORK_WORDS, dtype=torch.int32, device="cuda:0")
-    for block_from in sorted({cfg.L, plan["block_from"], n_dense, 0}):
+    for block_from in sorted({cfg.L, plan["block_from"], n_dense, 0, max(cfg.L - 3, 0)}):
         for batch in (2, 4):
-            for chunk in sorted({0, 1, cfg.K // 2, cfg.K}):
+            # rounds of a power of two samples, as the render takes them
+            for chunk in sorted({c for c in (0, 1, cfg.K // 2, cfg.K) if c & (c - 1) == 0}):
               for claims in (True, False):
                 sink = torch.zeros(blocks * 256, dtype=torch.int32, device="cuda:0")
                 rc = mb.lib().mixrt_mb_gather_replay(
@@ -222,6 +227,10 @@ def test_gather_replay_loads_exactly_the_corner_entries(cfg):
     r.close()
 
 
+def _table3(name):
+    return synth.CONFIGS[name]
+
+
 BLOCK_CFGS = [
     synth.VIEW720P.replace(name="blk_720p_rows", rows=64),
     synth.VIEW720P_DENSE.replace(name="blk_dense_rows", rows=64),
@@ -229,6 +238,12 @@ BLOCK_CFGS = [
     synth.VIEW720P.replace(name="blk_k1", K=1, rows=96),
     synth.VIEW720P.replace(name="blk_ragged", H=23, W=37, views=2, K=3, gbuf="iid",
                            delta=0.5, log2_T=12, N_max=2048),
+    # 8-byte entries (fp16, F = 4): one query per pixel with the MLP, 8
+    # samples per ray (the rounds path), and a ragged frame
+    synth.TABLE3[0].replace(name="blk_f4_L8", rows=64),
+    synth.TABLE3[0].replace(name="blk_f4_k8", K=8, delta=0.05, rows=32),
+    synth.TABLE3[0].replace(name="blk_f4_ragged", H=23, W=37, views=2, K=3, gbuf="iid",
+                            delta=0.5, log2_T=12),
 ]
 
 
@@ -259,8 +274,10 @@ def test_block_gathers_give_the_same_frame(cfg):
     assert len(seen) >= 3
 
 
-def test_block_gathers_spot_check_against_the_oracle():
-    cfg = BLOCK_CFGS[1]
+@pytest.mark.parametrize("cfg", [BLOCK_CFGS[1], BLOCK_CFGS[5], BLOCK_CFGS[6]],
+                         ids=lambda c: c.name)
+def test_block_gathers_spot_check_against_the_oracle(cfg):
+    say("block gathers against the oracle", cfg.name)
     sc = synth.make_scene(cfg)
     ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
     r = mixrt.Renderer(0, sync_check=True, block_levels=cfg.L)
@@ -296,26 +313,27 @@ def test_default_round_size_follows_the_rule(cfg):
                                  synth.VIEW720P.replace(name="k1", K=1),
                                  synth.VIEW720P.replace(name="fine_spacing", delta=1e-4),
                                  synth.BATCH8X1080P, synth.BATCH8X1080P.replace(name="batch_k4", K=4),
-                                 synth.PAPER720P, synth.DEPLOYED720P, synth.TABLE3[0]],
+                                 synth.PAPER720P, synth.DEPLOYED720P, synth.TABLE3[0],
+                                 _table3("tab3_L8_T5"),
+                                 _table3("tab3_L16_T17").replace(name="tab3_L16")],
                          ids=lambda c: c.name)
 def test_default_gather_plan_follows_the_rule(cfg):
-    """Block gathers on the three finest levels (when a level's table exceeds
-    one XCD's L2: four, and eight at K >= 8) among hashed levels finer than
-    the sample spacing, 4-byte entries only; batches of 4 hashed levels only
-    for entries of 8+ bytes when that covers every hashed level."""
+    """4-byte entries: block gathers on the three finest levels (when a
+    level's table exceeds one XCD's L2: four, and eight at K >= 8) among
+    hashed levels finer than the sample spacing.  8-byte (fp16 F = 4)
+    entries: on every hashed level when there are 8 or more of them in tables
+    of 2^10 or more entries.  Batches of 4 hashed levels only for entries of
+    8+ bytes when that covers every hashed level."""
     want = {"view720p": (13, 2), "view720p_dense": (13, 2), "k1": (13, 2),
             "fine_spacing": (16, 2), "batch8x1080p": (8, 2), "batch_k4": (12, 2),
-            "paper720p": (4, 4), "deployed720p": (4, 4), "tab3_L8_T17_mlp": (8, 2)}[cfg.name]
+            "paper720p": (4, 4), "deployed720p": (4, 4), "tab3_L8_T17_mlp": (0, 2),
+            "tab3_L8_T5": (8, 2), "tab3_L16": (0, 2)}[cfg.name]
     sc = synth.make_scene(cfg.replace(H=16, W=64, views=1))
     ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
     r = mixrt.Renderer(0)
     plan = r.launch_plan(ds)
     r.close()
     assert (plan["block_from"], plan["hash_batch"]) == want, plan
-
-
-def _table3(name):
-    return synth.CONFIGS[name]
 
 
 @pytest.mark.parametrize("cfg", [synth.VIEW720P, synth.PAPER720P, synth.BATCH8X1080P,
