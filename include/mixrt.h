@@ -108,12 +108,15 @@ typedef struct {
                             least half, a quarter or fewer of the levels */
     int32_t block_levels; /* how many of the finest hash levels gather each
                             x-neighbour pair of corners as one aligned 16-byte
-                            block holding both entries (tables of 2 fp16
+                            block holding both entries (tables of 2 or 4 fp16
                             features only; speed only, never a result): > 0
                             that many (hashed levels only), < 0 none, 0 the
-                            library's choice (the three finest, four when a
-                            level's table exceeds one XCD's L2, among the
-                            hashed levels finer than a ray's sample spacing) */
+                            library's choice (2 features: the three finest,
+                            four when a level's table exceeds one XCD's L2,
+                            among the hashed levels finer than a ray's sample
+                            spacing; 4 features: every hashed level when there
+                            are 8 or more in tables of 2^10 or more entries,
+                            else none) */
 } mixrt_create_info;
 
 /* The coarse-mesh hit per pixel (Fig. 2 step 1): rasterisation output. */
