@@ -35,23 +35,46 @@ def test_library_exports_every_declared_symbol():
     assert set(declared) <= exported
 
 
+LLVM = "/opt/rocm/llvm/bin"
+
+
+def _code_object_output(obj, tool_args):
+    """Runs an LLVM tool on the gfx950 code object of one object file of this
+    build (its offload bundle) and returns what the tool printed."""
+    with tempfile.TemporaryDirectory() as d:
+        fat, co = os.path.join(d, "fat.bin"), os.path.join(d, "co.elf")
+        subprocess.run([f"{LLVM}/llvm-objcopy", f"--dump-section=.hip_fatbin={fat}", obj],
+                       check=True, capture_output=True)
+        subprocess.run([f"{LLVM}/clang-offload-bundler", "--unbundle", "--type=o",
+                        f"--input={fat}", "--targets=hipv4-amdgcn-amd-amdhsa--gfx950",
+                        f"--output={co}"], check=True, capture_output=True)
+        return subprocess.run(tool_args + [co], check=True, capture_output=True,
+                              text=True).stdout
+
+
 def _kernel_metadata(obj, field):
     """{kernel: value of an integer metadata field} of the gfx950 code in one
     object file of this build (its offload bundle's kernel metadata)."""
-    llvm = "/opt/rocm/llvm/bin"
-    with tempfile.TemporaryDirectory() as d:
-        fat, co = os.path.join(d, "fat.bin"), os.path.join(d, "co.elf")
-        subprocess.run([f"{llvm}/llvm-objcopy", f"--dump-section=.hip_fatbin={fat}", obj],
-                       check=True, capture_output=True)
-        subprocess.run([f"{llvm}/clang-offload-bundler", "--unbundle", "--type=o",
-                        f"--input={fat}", "--targets=hipv4-amdgcn-amd-amdhsa--gfx950",
-                        f"--output={co}"], check=True, capture_output=True)
-        notes = subprocess.run([f"{llvm}/llvm-readelf", "--notes", co], check=True,
-                               capture_output=True, text=True).stdout
+    notes = _code_object_output(obj, [f"{LLVM}/llvm-readelf", "--notes"])
     names = re.findall(r"^\s+\.name:\s+(\S+)", notes, flags=re.M)
     values = [int(v) for v in re.findall(rf"\.{field}:\s+(\d+)", notes)]
     assert len(names) == len(values)
     return dict(zip(names, values))
+
+
+def _kernel_disassembly(obj):
+    """{kernel: [instruction mnemonics with operands]} of the gfx950 code in
+    one object file of this build (AMD assembly of the library's own code)."""
+    text = _code_object_output(obj, [f"{LLVM}/llvm-objdump", "-d", "--no-show-raw-insn",
+                                     "--no-leading-addr"])
+    out, cur = {}, None
+    for line in text.splitlines():
+        m = re.match(r"^<(\S+)>:$", line)
+        if m:
+            cur = out.setdefault(m.group(1), [])
+        elif cur is not None and line.startswith("\t"):
+            cur.append(line.split("//")[0].strip())
+    return out
 
 
 def _kernel_private_segments(obj):
@@ -437,3 +460,45 @@ def test_flag_values_match_header():
     for name in ("MIXRT_FLAG_SYNC_CHECK", "MIXRT_FLAG_BLOCKS_FULL", "MIXRT_FLAG_BLOCKS_TWO"):
         m = re.search(rf"{name}\s*=\s*(\d+)u", text)
         assert m and int(m.group(1)) == getattr(mixrt, name), name
+
+
+def test_mlp_stage_pipeline_counts_hold():
+    """The MLP stage's tile loop waits on hand-counted vmcnt values that hold
+    only if every tile issues exactly IN / 8 row loads (into LDS) and one
+    output store, and no other vector-memory operation is in flight among
+    them.  Checked on the built code of every mlp_kernel instance (one tile
+    ahead): the weight loads all come before the first row load, no other
+    vector-memory instruction follows it, the two issue sites (the
+    prologue's tile and the loop's next tile) hold IN / 8 row loads each,
+    there is one store, and every vmcnt wait is within the pipeline's
+    depth."""
+    from paper_2312_11841_amd import build
+    obj = os.path.join(build.OBJ_DIR, "mixrt_stages.o")
+    if not os.path.exists(obj):
+        pytest.skip("library objects not built")
+    kernels = {k: v for k, v in _kernel_disassembly(obj).items() if "mlp_kernel" in k}
+    assert len(kernels) >= 6
+    vmem = re.compile(r"^(global_|buffer_|flat_|scratch_)")
+    for name, ins in kernels.items():
+        IN, HID, NHID, DEPTH = map(int, re.search(
+            r"mlp_kernelILi(\d+)ELi(\d+)ELi(\d+)ELi(\d+)E", name).groups())
+        ch = IN // 8
+        ops = [i.split()[0] for i in ins if i]
+        loads = [j for j, o in enumerate(ops) if o == "global_load_lds_dwordx4"]
+        stores = [j for j, o in enumerate(ops) if o == "global_store_dwordx4"]
+        assert DEPTH == 1 and len(loads) == 2 * ch, name
+        # each site's loads are straight-line code under the full exec mask:
+        # no branch and no exec change between them (a load skipped in some
+        # waves would leave the counted waits short)
+        for site in (loads[:ch], loads[ch:]):
+            between = ins[site[0]:site[-1] + 1]
+            assert not [i for i in between if i.startswith("s_cbranch") or "exec" in i], name
+        assert len(stores) == 1, name
+        others = [ops[j] for j in range(loads[0], len(ops))
+                  if vmem.match(ops[j]) and ops[j] not in ("global_load_lds_dwordx4",
+                                                           "global_store_dwordx4")]
+        assert others == [], (name, others)
+        for i in ins:
+            m = re.search(r"vmcnt\((\d+)\)", i)
+            if m:
+                assert int(m.group(1)) <= DEPTH * (ch + 1), (name, i)
