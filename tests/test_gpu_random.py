@@ -38,13 +38,15 @@ def test_random_workload_matches_oracle(R, seed):
     print(f"  max |gpu - oracle| = {err:.3e} over {cfg.rays} px", flush=True)
     assert err <= FRAME_TOL + cfg.t_term
     # the other evaluation order (tile path against rounds of a random size)
-    # renders the same frame bit for bit
+    # and another choice of block-gathered levels render the same frame bit
+    # for bit
     chunk = int(np.random.default_rng(seed).choice([-1, 1, 2, 4, 8, 16]))
-    r2 = mixrt.Renderer(0, sync_check=True, early_stop_chunk=chunk,
+    levels = int(np.random.default_rng(seed + 2).choice([-1, 0, 1, 2, cfg.L]))
+    r2 = mixrt.Renderer(0, sync_check=True, early_stop_chunk=chunk, block_levels=levels,
                         tile_stripe=int(np.random.default_rng(seed + 1).integers(-1, 9)))
     got2 = r2.render(ds).cpu().numpy().astype(np.float64)
     r2.close()
-    assert np.array_equal(got2, got), chunk
+    assert np.array_equal(got2, got), (chunk, levels)
 
 
 @pytest.mark.parametrize("seed", list(range(3000, 3024)))
