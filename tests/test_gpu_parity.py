@@ -281,21 +281,30 @@ def _index_table(L, T, F):
     return out.reshape(L, T, F)
 
 
-@pytest.mark.parametrize("L,log2_T,F,n_min,n_max", [(32, 14, 2, 2, 2048), (2, 26, 2, 4096, 4096)],
-                         ids=["max_levels", "max_table"])
-def test_frame_at_the_largest_grids(R, L, log2_T, F, n_min, n_max):
+@pytest.mark.parametrize("L,log2_T,F,f16,n_min,n_max",
+                         [(32, 14, 2, False, 2, 2048), (2, 26, 2, False, 4096, 4096),
+                          (8, 23, 4, True, 4096, 4096)],
+                         ids=["max_levels", "max_table", "f16_f4_blocks"])
+def test_frame_at_the_largest_grids(R, L, log2_T, F, f16, n_min, n_max):
     """The largest level count (32, dense and hashed levels) and the largest
     table (2^26 entries per level, two hashed levels; the table values depend
-    on every index bit), with the MLP removed."""
+    on every index bit), with the MLP removed; and 8 hashed levels of 2^23
+    fp16 entries of 4 features (512 MiB), which the library gathers as
+    16-byte blocks of x-neighbour pairs on every level."""
     cfg = synth.TINY64_DENSE.replace(name=f"grid_L{L}_T{log2_T}", H=24, W=40, L=L, F=F,
                                      log2_T=min(log2_T, 14), N_min=n_min, N_max=n_max,
-                                     widths=(L * F,), seed=17)
+                                     widths=(L * F,), seed=17,
+                                     table_dtype="f16" if f16 else "f32")
     sc = synth.make_scene(cfg)
     if log2_T > 14:
         sc.cfg = cfg.replace(log2_T=log2_T, disp="none")
         sc.table = _index_table(L, 1 << log2_T, F)
+        if f16:
+            sc.table = sc.table.astype(np.float16)
     say("largest grid", sc.cfg.name, sc.table.shape, sc.table.dtype)
     ds = mixrt.DeviceScene.from_scene(sc, "cuda:0")
+    if f16:
+        assert R.launch_plan(ds)["block_from"] == 0
     got = R.render(ds).cpu().numpy()
     R.sync()
     ref = oracle.OracleScene(sc).render_pixels(np.arange(cfg.rays), threads=oracle.max_threads())
