@@ -112,11 +112,12 @@ typedef struct {
                             features only; speed only, never a result): > 0
                             that many (hashed levels only), < 0 none, 0 the
                             library's choice (2 features: the three finest,
-                            four when a level's table exceeds one XCD's L2,
-                            among the hashed levels finer than a ray's sample
-                            spacing; 4 features: every hashed level when there
-                            are 8 or more in tables of 2^10 or more entries,
-                            else none) */
+                            five in rounds of one sample per ray, four when a
+                            level's table exceeds one XCD's L2 (eight at K >=
+                            8), among the hashed levels finer than a ray's
+                            sample spacing; 4 features: every hashed level
+                            when there are 8 or more in tables of 2^10 or
+                            more entries, else none) */
 } mixrt_create_info;
 
 /* The coarse-mesh hit per pixel (Fig. 2 step 1): rasterisation output. */

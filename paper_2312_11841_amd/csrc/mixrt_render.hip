@@ -647,7 +647,9 @@ static int render_chunk(const RenderLaunch &L)
 // finest levels (when a level's table exceeds one XCD's L2, whose misses
 // scatter more: four, and at K >= 8 up to eight, which took the 8-view
 // 1080p batch from 12.51 to 12.03 ms while 8 MiB levels at 720p and K = 8
-// stayed within 0.2% and at K = 4 lost 2.6%), among the hashed levels finer
+// stayed within 0.2% and at K = 4 lost 2.6%; in rounds of one sample per
+// ray, whose lanes are 64 rays whose samples lie apart on more levels: five,
+// 1-3% faster at spacing 0.25 and K 4 to 16), among the hashed levels finer
 // than a ray's sample spacing (coarser levels hand a ray's neighbouring
 // samples the same lines, where a 4-byte gather is cheaper).  Measured against single-entry gathers
 // on every level: the finest 2 to 4 levels were 2-15% faster at 720p (K 1 to
@@ -670,7 +672,8 @@ static int render_block_from(const RenderLaunch &L)
     int lo = L.gp.n_dense;
     if (L.block_levels > 0) return nl - L.block_levels > lo ? nl - L.block_levels : lo;
     const int64_t level_bytes = ((int64_t)L.gp.T_mask + 1) * 4;
-    const int kFinest = level_bytes <= L.l2_bytes ? 3 : L.rp.K >= 8 ? 8 : 4;
+    const int kFinest = level_bytes > L.l2_bytes ? (L.rp.K >= 8 ? 8 : 4)
+                        : render_chunk(L) == 1 ? 5 : 3;
     if (L.rp.K > 1) {
         const int shared = levels_shared_by_samples(L);
         if (shared > lo) lo = shared;

@@ -318,13 +318,14 @@ def test_default_round_size_follows_the_rule(cfg):
                                  _table3("tab3_L16_T17").replace(name="tab3_L16")],
                          ids=lambda c: c.name)
 def test_default_gather_plan_follows_the_rule(cfg):
-    """4-byte entries: block gathers on the three finest levels (when a
-    level's table exceeds one XCD's L2: four, and eight at K >= 8) among
-    hashed levels finer than the sample spacing.  8-byte (fp16 F = 4)
+    """4-byte entries: block gathers on the three finest levels (five in
+    rounds of one sample per ray; when a level's table exceeds one XCD's L2:
+    four, and eight at K >= 8) among hashed levels finer than the sample
+    spacing.  8-byte (fp16 F = 4)
     entries: on every hashed level when there are 8 or more of them in tables
     of 2^10 or more entries.  Batches of 4 hashed levels only for entries of
     8+ bytes when that covers every hashed level."""
-    want = {"view720p": (13, 2), "view720p_dense": (13, 2), "k1": (13, 2),
+    want = {"view720p": (13, 2), "view720p_dense": (11, 2), "k1": (13, 2),
             "fine_spacing": (16, 2), "batch8x1080p": (8, 2), "batch_k4": (12, 2),
             "paper720p": (4, 4), "deployed720p": (4, 4), "tab3_L8_T17_mlp": (0, 2),
             "tab3_L8_T5": (8, 2), "tab3_L16": (0, 2)}[cfg.name]
